@@ -1,0 +1,118 @@
+/*
+ * mea.h - memory-efficient exact attention on MI355X (gfx950), C ABI.
+ *
+ * Computes dense softmax attention exactly (Rabe & Staats, "Self-attention
+ * Does Not Need O(n^2) Memory", arXiv 2112.05682):
+ *   Section 1: s_ij = dot(q_i, k_j), w_ij = softmax_j(s_ij),
+ *              o_i = sum_j w_ij v_j;
+ *   Section 4: q is scaled before the dot product (by 1/sqrt(d) there; here
+ *              an explicit `scale`, so s_ij = scale * dot(q_i, k_j)).
+ * The keys are consumed tile by tile with the lazy softmax of Section 2
+ * (Eq. 1) made stable by the running maximum of Section 3: a running row
+ * max m, a rescaled running numerator sum_j e^{s_j - m} v_j and a running
+ * denominator sum_j e^{s_j - m}, divided once at the end.  The score matrix
+ * is never written to memory.  The backward recomputes each tile's scores
+ * (the checkpointing of Section 5.2) from the saved per-row log-sum-exp.
+ *
+ * Conventions shared by every entry point:
+ *   - Layout: contiguous row-major [batch, heads, n, d], feature index
+ *     innermost; q, o, do, dq are [B, H, n_q, d]; k, v, dk, dv are
+ *     [B, H, n_k, d]; lse is [B, H, n_q] float32.
+ *   - Pointers: q, k, v, o, do, dq, dk, dv, lse and workspace are DEVICE
+ *     pointers, 16-byte aligned.  The mea_problem pointer is a HOST pointer.
+ *   - Ownership: the caller allocates every buffer, including the workspace.
+ *     The library allocates no device memory, keeps no mutable global state
+ *     and never synchronises: work is enqueued on `stream` (0 = the null
+ *     stream) and completes asynchronously.  Calls are re-entrant.
+ *   - Outputs are overwritten, never accumulated into.
+ *   - Masking (`causal` = 1): key j is visible to query i iff j <= i,
+ *     aligned at the top-left (key 0 is always visible, so no row is empty,
+ *     also when n_q != n_k).  The paper defines no mask; this is the reading
+ *     the library adopts.
+ *   - Errors: arguments are validated before anything is launched; on a
+ *     validation error nothing is enqueued and the status says why.  A
+ *     launch failure reported by the HIP runtime returns MEA_ERR_HIP.  Errors
+ *     during kernel execution surface at the caller's next synchronisation.
+ *   - Supported: d in {64, 128}; dtype f32, f16 or bf16 (all tensors of one
+ *     call share it; lse, the workspace and all accumulation are float32).
+ *     Sizes: batch, heads, n_q, n_k >= 1; every element count must fit in
+ *     int64 and n_q, n_k <= 2^31 - 1.
+ */
+#ifndef MEA_H_
+#define MEA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MEA_OK = 0,
+  MEA_ERR_INVALID_ARG = 1, /* null/misaligned pointer, size < 1, bad scale */
+  MEA_ERR_UNSUPPORTED = 2, /* d or dtype outside the supported set */
+  MEA_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+  MEA_ERR_HIP = 4          /* the HIP runtime rejected a launch */
+} mea_status;
+
+typedef enum { MEA_F32 = 0, MEA_F16 = 1, MEA_BF16 = 2 } mea_dtype;
+
+/* Problem description (host memory, read during the call only). */
+typedef struct {
+  int64_t batch;  /* B >= 1 */
+  int64_t heads;  /* H >= 1 */
+  int64_t n_q;    /* queries per (b, h) >= 1 */
+  int64_t n_k;    /* keys = values per (b, h) >= 1 */
+  int64_t d;      /* head dimension of q, k and v: 64 or 128 */
+  int32_t dtype;  /* mea_dtype of q, k, v, o, do, dq, dk, dv */
+  int32_t causal; /* 0 = no mask, 1 = top-left causal mask (see above) */
+  float scale;    /* score scale, finite and > 0; 1/sqrt(d) in the paper */
+} mea_problem;
+
+/* Bytes of device workspace mea_attention_fwd needs for `p` (written to
+ * *bytes).  Zero unless the keys are split over several workgroups per query
+ * tile (long key sequences with few query tiles), in which case it holds the
+ * per-split partial numerators (float32 [S, B, H, n_q, d]) and running
+ * max / denominator (float32 [S, B, H, n_q] each) that the combine step of
+ * Section 4 rescales and adds.  Returns MEA_OK or a validation error. */
+mea_status mea_attention_fwd_workspace_size(const mea_problem* p, size_t* bytes);
+
+/* Bytes of device workspace mea_attention_bwd needs for `p`: the per-row
+ * D_i = sum_t dO_it O_it (float32 [B, H, n_q]), O(n) like the lse. */
+mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes);
+
+/* Forward (Sections 2-4): o = softmax(scale * q k^T) v, computed tile by
+ * tile with the running max / numerator / denominator; writes o (dtype) and,
+ * if lse != NULL, lse_i = max_j s_ij + ln sum_j e^{s_ij - max_j s_ij} in
+ * natural-log units (float32), which the backward needs.  `workspace` may be
+ * NULL only when the required size is 0. */
+mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
+                             const void* v, void* o, float* lse, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
+/* Backward (Section 5.2, recompute instead of storing the n_q x n_k matrix):
+ * given the forward's o and lse and the upstream gradient do, writes
+ *   dv_j = sum_i w_ij do_i,
+ *   dk_j = scale sum_i w_ij (do_i . v_j - D_i) q_i,
+ *   dq_i = scale sum_j w_ij (do_i . v_j - D_i) k_j,
+ * with D_i = do_i . o_i and w_ij = exp(s_ij - lse_i) recomputed per tile.
+ * All inputs must come from one mea_attention_fwd call on the same problem.
+ * dq may be NULL to skip dQ; dk and dv may be NULL together to skip dK and dV
+ * (at least one of the two groups must be requested). */
+mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
+                             const void* v, const void* o, const void* d_o,
+                             const float* lse, void* dq, void* dk, void* dv,
+                             void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* Static description of a status code (never NULL). */
+const char* mea_status_string(mea_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEA_H_ */

@@ -1,0 +1,122 @@
+"""PyTorch-facing wrapper of the C ABI: allocation of outputs and workspace
+through torch, and the current HIP stream.  Every step of the computation runs
+in the HIP kernels of ``libmea.so``; nothing here computes attention.
+
+Tensors are ``[B, H, n, d]``, contiguous, on one GPU, all of one dtype
+(float32, float16 or bfloat16); d must be 64 or 128.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import _lib
+
+_DTYPE_CODE = {torch.float32: _lib.MEA_F32, torch.float16: _lib.MEA_F16,
+               torch.bfloat16: _lib.MEA_BF16}
+
+
+def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale):
+    if q.dim() != 4 or k.dim() != 4:
+        raise ValueError("q and k must be [B, H, n, d]")
+    B, H, n_q, d = q.shape
+    n_k = k.shape[2]
+    if q.dtype not in _DTYPE_CODE:
+        raise TypeError("unsupported dtype %s" % q.dtype)
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    return _lib.problem(B, H, n_q, n_k, d, _DTYPE_CODE[q.dtype], causal, scale)
+
+
+def _check_tensors(names, tensors, dtype, device):
+    for name, t in zip(names, tensors):
+        if not t.is_cuda:
+            raise ValueError("%s must be a GPU tensor" % name)
+        if t.device != device:
+            raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
+        if t.dtype != dtype:
+            raise TypeError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % name)
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def fwd_workspace_bytes(q, k, causal=False, scale=None) -> int:
+    return _lib.fwd_workspace_size(_problem(q, k, causal, scale))
+
+
+def bwd_workspace_bytes(q, k, causal=False, scale=None) -> int:
+    return _lib.bwd_workspace_size(_problem(q, k, causal, scale))
+
+
+def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: bool = False,
+                  scale: float | None = None, need_lse: bool = True, out=None):
+    """Returns ``(o, lse)``; ``lse`` is float32 ``[B, H, n_q]`` (None if not needed)."""
+    if k.shape != v.shape or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
+        raise ValueError("shape mismatch: q %s k %s v %s" % (tuple(q.shape), tuple(k.shape),
+                                                              tuple(v.shape)))
+    _check_tensors(("q", "k", "v"), (q, k, v), q.dtype, q.device)
+    p = _problem(q, k, causal, scale)
+    o = torch.empty_like(q) if out is None else out
+    _check_tensors(("out",), (o,), q.dtype, q.device)
+    lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if need_lse else None
+    ws_bytes = _lib.fwd_workspace_size(p)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device) if ws_bytes else None
+    _lib.check("mea_attention_fwd", _lib.fwd(
+        p, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+        lse.data_ptr() if lse is not None else None,
+        ws.data_ptr() if ws is not None else None, ws_bytes, _stream(q.device)))
+    return o, lse
+
+
+def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None = None,
+                  need_dq: bool = True, need_dkdv: bool = True):
+    """Returns ``(dq, dk, dv)`` for the upstream gradient ``do``; a gradient that
+    is not needed is returned as None and its kernel is not run."""
+    _check_tensors(("q", "k", "v", "o", "do"), (q, k, v, o, do), q.dtype, q.device)
+    _check_tensors(("lse",), (lse,), torch.float32, q.device)
+    if o.shape != q.shape or do.shape != q.shape or tuple(lse.shape) != tuple(q.shape[:3]):
+        raise ValueError("o, do must match q and lse must be [B, H, n_q]")
+    if not (need_dq or need_dkdv):
+        raise ValueError("nothing to compute")
+    p = _problem(q, k, causal, scale)
+    dq = torch.empty_like(q) if need_dq else None
+    dk = torch.empty_like(k) if need_dkdv else None
+    dv = torch.empty_like(v) if need_dkdv else None
+    ws_bytes = _lib.bwd_workspace_size(p)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    _lib.check("mea_attention_bwd", _lib.bwd(
+        p, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), do.data_ptr(),
+        lse.data_ptr(), dq.data_ptr() if need_dq else None,
+        dk.data_ptr() if need_dkdv else None, dv.data_ptr() if need_dkdv else None,
+        ws.data_ptr(), ws_bytes,
+        _stream(q.device)))
+    return dq, dk, dv
+
+
+class MemoryEfficientAttention(torch.autograd.Function):
+    """Autograd wrapper: saves only q, k, v, o and the O(n) lse."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, causal=False, scale=None):
+        q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
+        o, lse = attention_fwd(q, k, v, causal, scale, need_lse=True)
+        ctx.save_for_backward(q, k, v, o, lse)
+        ctx.causal = causal
+        ctx.scale = scale
+        return o
+
+    @staticmethod
+    def backward(ctx, do):
+        q, k, v, o, lse = ctx.saved_tensors
+        dq, dk, dv = attention_bwd(q, k, v, o, lse, do.contiguous(), ctx.causal, ctx.scale)
+        return dq, dk, dv, None, None
+
+
+def attention(q, k, v, causal: bool = False, scale: float | None = None):
+    """Exact softmax attention, differentiable, O(n) extra memory."""
+    return MemoryEfficientAttention.apply(q, k, v, causal, scale)

@@ -1,0 +1,216 @@
+// C ABI of the attention library: argument validation, work planning
+// (query tiles, key splits, workspace carving) and kernel dispatch.  Nothing
+// here allocates device memory or synchronises; every launch goes onto the
+// caller's stream.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/mea.h"
+#include "kernels.hpp"
+
+namespace {
+
+using mea::BwdParams;
+using mea::FwdParams;
+
+constexpr int64_t kMaxSeq = (int64_t)1 << 31;  // n_q, n_k must stay below 2^31
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+// Shape, dtype and scale checks shared by every entry point.
+mea_status check_problem(const mea_problem* p) {
+  if (!p) return MEA_ERR_INVALID_ARG;
+  if (p->batch < 1 || p->heads < 1 || p->n_q < 1 || p->n_k < 1 || p->d < 1)
+    return MEA_ERR_INVALID_ARG;
+  if (p->n_q >= kMaxSeq || p->n_k >= kMaxSeq) return MEA_ERR_INVALID_ARG;
+  if (p->causal != 0 && p->causal != 1) return MEA_ERR_INVALID_ARG;
+  if (!(p->scale > 0.0f) || !isfinite(p->scale)) return MEA_ERR_INVALID_ARG;
+  int64_t bh, nq_d, nk_d, tot;
+  if (!mul_ok(p->batch, p->heads, &bh) || bh >= kMaxSeq) return MEA_ERR_INVALID_ARG;
+  if (!mul_ok(p->n_q, p->d, &nq_d) || !mul_ok(p->n_k, p->d, &nk_d)) return MEA_ERR_INVALID_ARG;
+  if (!mul_ok(bh, nq_d, &tot) || !mul_ok(bh, nk_d, &tot)) return MEA_ERR_INVALID_ARG;
+  if (!mul_ok(bh, p->n_q * 4, &tot)) return MEA_ERR_INVALID_ARG;
+  if (p->d != 64 && p->d != 128) return MEA_ERR_UNSUPPORTED;
+  if (p->dtype != MEA_F32 && p->dtype != MEA_F16 && p->dtype != MEA_BF16) return MEA_ERR_UNSUPPORTED;
+  return MEA_OK;
+}
+
+bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
+bool dev_ptr_ok(const void* ptr) { return ptr != nullptr && aligned16(ptr); }
+
+struct FwdPlan {
+  int bq, bk;
+  int64_t n_qtiles;
+  int n_splits;
+  int64_t keys_per_split;
+  size_t workspace;
+};
+
+void fwd_tiles(int dtype, int64_t d, int* bq, int* bk) {
+  if (dtype == MEA_F32) {
+    *bq = mea::FwdShape<float, 64>::BQ;
+    *bk = mea::FwdShape<float, 64>::BK;
+  } else if (d == 64) {
+    *bq = mea::FwdShape<__bf16, 64>::BQ;
+    *bk = mea::FwdShape<__bf16, 64>::BK;
+  } else {
+    *bq = mea::FwdShape<__bf16, 128>::BQ;
+    *bk = mea::FwdShape<__bf16, 128>::BK;
+  }
+}
+
+// Grid plan.  The chip has 256 CUs; when the query tiles alone give too few
+// workgroups, the keys are split so that each split's summary is combined
+// afterwards (Section 4 combine).
+FwdPlan plan_fwd(const mea_problem* p) {
+  FwdPlan pl;
+  fwd_tiles(p->dtype, p->d, &pl.bq, &pl.bk);
+  const int64_t bh = p->batch * p->heads;
+  pl.n_qtiles = (p->n_q + pl.bq - 1) / pl.bq;
+  const int64_t k_tiles = (p->n_k + pl.bk - 1) / pl.bk;
+  const int64_t base = bh * pl.n_qtiles;
+  int64_t splits = 1;
+  const int64_t kTargetWorkgroups = 1024;  // 4 per CU
+  const int64_t kMinTilesPerSplit = 16;
+  if (base < 512 && k_tiles >= 2 * kMinTilesPerSplit) {
+    splits = (kTargetWorkgroups + base - 1) / base;
+    const int64_t max_splits = k_tiles / kMinTilesPerSplit;
+    if (splits > max_splits) splits = max_splits;
+    if (splits > 64) splits = 64;
+    if (splits < 1) splits = 1;
+  }
+  const int64_t tiles_per_split = (k_tiles + splits - 1) / splits;
+  pl.keys_per_split = tiles_per_split * pl.bk;
+  pl.n_splits = (int)((p->n_k + pl.keys_per_split - 1) / pl.keys_per_split);
+  pl.workspace = 0;
+  if (pl.n_splits > 1) {
+    const size_t rows = (size_t)pl.n_splits * (size_t)bh * (size_t)p->n_q;
+    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256;
+  }
+  return pl;
+}
+
+size_t bwd_workspace(const mea_problem* p) {
+  return (size_t)p->batch * (size_t)p->heads * (size_t)p->n_q * 4 + 256;
+}
+
+float* align256(void* base, size_t off) {
+  uintptr_t a = (uintptr_t)base + off;
+  a = (a + 255u) & ~(uintptr_t)255u;
+  return reinterpret_cast<float*>(a);
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+}  // namespace
+
+extern "C" {
+
+const char* mea_status_string(mea_status s) {
+  switch (s) {
+    case MEA_OK: return "ok";
+    case MEA_ERR_INVALID_ARG: return "invalid argument";
+    case MEA_ERR_UNSUPPORTED: return "unsupported head dimension or dtype";
+    case MEA_ERR_WORKSPACE: return "workspace missing or too small";
+    case MEA_ERR_HIP: return "HIP runtime error at launch";
+  }
+  return "unknown status";
+}
+
+mea_status mea_attention_fwd_workspace_size(const mea_problem* p, size_t* bytes) {
+  const mea_status st = check_problem(p);
+  if (st != MEA_OK) return st;
+  if (!bytes) return MEA_ERR_INVALID_ARG;
+  *bytes = plan_fwd(p).workspace;
+  return MEA_OK;
+}
+
+mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes) {
+  const mea_status st = check_problem(p);
+  if (st != MEA_OK) return st;
+  if (!bytes) return MEA_ERR_INVALID_ARG;
+  *bytes = bwd_workspace(p);
+  return MEA_OK;
+}
+
+mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k, const void* v,
+                             void* o, float* lse, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  const mea_status st = check_problem(p);
+  if (st != MEA_OK) return st;
+  if (!dev_ptr_ok(q) || !dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(o))
+    return MEA_ERR_INVALID_ARG;
+  if (lse && !aligned16(lse)) return MEA_ERR_INVALID_ARG;
+  const FwdPlan pl = plan_fwd(p);
+  if (pl.workspace > 0 && (!workspace || workspace_bytes < pl.workspace)) return MEA_ERR_WORKSPACE;
+
+  FwdParams fp = {};
+  fp.q = q;
+  fp.k = k;
+  fp.v = v;
+  fp.o = o;
+  fp.lse = lse;
+  fp.n_q = p->n_q;
+  fp.n_k = p->n_k;
+  fp.keys_per_split = pl.keys_per_split;
+  fp.bh = (int)(p->batch * p->heads);
+  fp.n_qtiles = (int)pl.n_qtiles;
+  fp.n_splits = pl.n_splits;
+  fp.scale = p->scale;
+  fp.scale_log2 = p->scale * kLog2e;
+  if (pl.n_splits > 1) {
+    const size_t rows = (size_t)pl.n_splits * (size_t)fp.bh * (size_t)p->n_q;
+    fp.part_o = align256(workspace, 0);
+    fp.part_m = fp.part_o + rows * (size_t)p->d;
+    fp.part_l = fp.part_m + rows;
+  }
+  const int64_t grid = (int64_t)fp.n_qtiles * fp.bh * fp.n_splits;
+  if (grid >= ((int64_t)1 << 31)) return MEA_ERR_INVALID_ARG;
+  const hipError_t e = mea::launch_fwd(fp, p->dtype, (int)p->d, p->causal != 0, stream);
+  return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;
+}
+
+mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k, const void* v,
+                             const void* o, const void* d_o, const float* lse, void* dq, void* dk,
+                             void* dv, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  const mea_status st = check_problem(p);
+  if (st != MEA_OK) return st;
+  if (!dev_ptr_ok(q) || !dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(o) || !dev_ptr_ok(d_o) ||
+      !dev_ptr_ok(lse))
+    return MEA_ERR_INVALID_ARG;
+  // dq may be NULL (dQ skipped); dk and dv are both given or both NULL.
+  if ((dq && !aligned16(dq)) || (dk && !aligned16(dk)) || (dv && !aligned16(dv)))
+    return MEA_ERR_INVALID_ARG;
+  if ((dk == nullptr) != (dv == nullptr)) return MEA_ERR_INVALID_ARG;
+  if (!dq && !dk) return MEA_ERR_INVALID_ARG;
+  const size_t need = bwd_workspace(p);
+  if (!workspace || workspace_bytes < need) return MEA_ERR_WORKSPACE;
+
+  BwdParams bp = {};
+  bp.q = q;
+  bp.k = k;
+  bp.v = v;
+  bp.o = o;
+  bp.d_o = d_o;
+  bp.lse = lse;
+  bp.dq = dq;
+  bp.dk = dk;
+  bp.dv = dv;
+  bp.delta = align256(workspace, 0);
+  bp.n_q = p->n_q;
+  bp.n_k = p->n_k;
+  bp.bh = (int)(p->batch * p->heads);
+  bp.scale = p->scale;
+  bp.scale_log2 = p->scale * kLog2e;
+  const hipError_t e = mea::launch_bwd(bp, p->dtype, (int)p->d, p->causal != 0, stream);
+  if (e == hipErrorNotSupported) return MEA_ERR_UNSUPPORTED;
+  return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,493 @@
+// Backward kernels.  The paper keeps the backward memory-efficient by
+// checkpointing each chunk summary and recomputing it during
+// backpropagation (Section 5.2); here the same idea is applied per tile: the
+// forward saves only the per-row log-sum-exp, and every backward kernel
+// recomputes the tile scores S and weights P = exp(S - lse) instead of storing
+// the n_q x n_k matrix.  With D_i = dO_i . O_i the gradients are
+//   dV_j = sum_i P_ij dO_i,          dP_ij = dO_i . v_j,
+//   dS_ij = P_ij (dP_ij - D_i),      dQ_i = scale sum_j dS_ij k_j,
+//   dK_j = scale sum_i dS_ij q_i.
+// Three kernels, no atomics (bitwise reproducible):
+//   pre  : D_i for every query row;
+//   dkdv : one wave per 32 keys (K, V in registers), loop over query tiles;
+//          lane <-> key layout, so P and dS feed the dV and dK MFMAs directly;
+//   dq   : one wave per 32 queries (Q, dO in registers), loop over key tiles;
+//          lane <-> query layout, so dS^T feeds the dQ^T MFMA directly.
+#include "device.hpp"
+#include "kernels.hpp"
+
+namespace mea {
+
+// ------------------------------------------------------------------- pre
+template <typename T, int D>
+__global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
+  constexpr int E = sizeof(T);
+  constexpr int TPR = D * E / 16;  // threads per row, 16 bytes each
+  constexpr int RPB = 256 / TPR;
+  const int64_t rows = (int64_t)p.bh * p.n_q;
+  const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / TPR;
+  const int part = threadIdx.x % TPR;
+  float acc = 0.0f;
+  if (row < rows) {
+    typedef T vec16 __attribute__((ext_vector_type(16 / E)));
+    const vec16 o = *reinterpret_cast<const vec16*>(static_cast<const T*>(p.o) + row * D + part * (16 / E));
+    const vec16 g = *reinterpret_cast<const vec16*>(static_cast<const T*>(p.d_o) + row * D + part * (16 / E));
+#pragma unroll
+    for (int e = 0; e < 16 / E; ++e) acc = fmaf((float)o[e], (float)g[e], acc);
+  }
+#pragma unroll
+  for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, TPR);
+  if (row < rows && part == 0) p.delta[row] = acc;
+}
+
+// ------------------------------------------------------------------- dK, dV
+template <typename T, int D, int QS>
+struct DkdvTile {
+  static constexpr int NT = 256;
+  static constexpr int BKG = 128;      // keys per workgroup (32 per wave)
+  static constexpr int BQ = 32 * QS;   // queries per iteration
+  static constexpr int E = sizeof(T);
+  static constexpr int RS = D + 16 / E;
+  static constexpr int TILE = BQ * RS;          // Q or dO tile (elements)
+  static constexpr int CPR = D * E / 16;
+  static constexpr int CHUNKS = 2 * BQ * CPR;   // Q and dO chunks per stage
+  static constexpr int CPT = (CHUNKS + NT - 1) / NT;
+  static constexpr int STAGE_ELEMS = 2 * TILE;
+  static constexpr int STAGE_BYTES = STAGE_ELEMS * E + 2 * BQ * 4;  // + lse2, delta
+  static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+};
+
+template <typename T, int D, int QS, int OCC, bool CAUSAL>
+__global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
+  using Cfg = DkdvTile<T, D, QS>;
+  constexpr int RS = Cfg::RS;
+  constexpr int KC = D / 16;
+  constexpr int NDT = D / 32;
+  constexpr int NQC = Cfg::BQ / 16;  // 16-query chunks per iteration
+
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int h = lane >> 5, c = lane & 31;
+
+  const int w = xcd_remap(blockIdx.x, gridDim.x);
+  const int kt_idx = w % p.n_ktiles;  // heaviest (earliest keys) first under causal
+  const int bh = w / p.n_ktiles;
+  const int64_t k0 = (int64_t)kt_idx * Cfg::BKG;
+  const int64_t kw = k0 + 32 * wave;
+  const int64_t key = kw + c;
+
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const float* __restrict__ lseg = p.lse + (size_t)bh * p.n_q;
+  const float* __restrict__ deltag = p.delta + (size_t)bh * p.n_q;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+
+  // K^T and V^T as B operands: lane (h, key c) holds row `key`, k = 16kc + 8h + s.
+  Frag<T> kf[KC], vf[KC];
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (key < p.n_k) {
+      kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * D + 16 * kc + 8 * h);
+      vf[kc] = *reinterpret_cast<const Frag<T>*>(vg + key * D + 16 * kc + 8 * h);
+    } else {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        kf[kc][s] = (T)0.0f;
+        vf[kc][s] = (T)0.0f;
+      }
+    }
+  }
+
+  f32x16 dk[NDT], dv[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      dk[dt][r] = 0.0f;
+      dv[dt][r] = 0.0f;
+    }
+
+  // Queries before the first key of this tile see none of its keys.
+  const int64_t q_begin = CAUSAL ? (k0 / Cfg::BQ) * Cfg::BQ : 0;
+  const int n_iters = q_begin < p.n_q ? (int)((p.n_q - q_begin + Cfg::BQ - 1) / Cfg::BQ) : 0;
+
+  u32x4 stage[Cfg::CPT];
+  float stage_f = 0.0f;
+  auto stage_base = [&](int buf) { return smem_raw + buf * Cfg::STAGE_BYTES; };
+  auto load_stage = [&](int64_t q0) {
+#pragma unroll
+    for (int i = 0; i < Cfg::CPT; ++i) {
+      const int chunk = tid + i * Cfg::NT;
+      if (chunk < Cfg::CHUNKS) {
+        const int which = chunk / (Cfg::BQ * Cfg::CPR);  // 0 = Q, 1 = dO
+        const int rem = chunk % (Cfg::BQ * Cfg::CPR);
+        const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
+        const int64_t q = q0 + row;
+        const T* src = (which ? dog : qg) + q * D + col * (16 / Cfg::E);
+        stage[i] = q < p.n_q ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    if (tid < 2 * Cfg::BQ) {
+      const int64_t q = q0 + (tid % Cfg::BQ);
+      if (tid < Cfg::BQ)  // lse * log2(e); +inf past n_q makes those weights 0
+        stage_f = q < p.n_q ? lseg[q] * 1.4426950408889634f : INFINITY;
+      else
+        stage_f = q < p.n_q ? deltag[q] : 0.0f;
+    }
+  };
+  auto store_stage = [&](int buf) {
+    T* base = reinterpret_cast<T*>(stage_base(buf));
+#pragma unroll
+    for (int i = 0; i < Cfg::CPT; ++i) {
+      const int chunk = tid + i * Cfg::NT;
+      if (chunk < Cfg::CHUNKS) {
+        const int which = chunk / (Cfg::BQ * Cfg::CPR);
+        const int rem = chunk % (Cfg::BQ * Cfg::CPR);
+        const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
+        st16(base + which * Cfg::TILE + row * RS + col * (16 / Cfg::E), stage[i]);
+      }
+    }
+    if (tid < 2 * Cfg::BQ) {
+      float* f = reinterpret_cast<float*>(stage_base(buf) + Cfg::STAGE_ELEMS * Cfg::E);
+      f[tid] = stage_f;
+    }
+  };
+
+  const int qrow = perm32(c);
+  const float cl2 = p.scale_log2;
+
+  if (n_iters > 0) {
+    load_stage(q_begin);
+    store_stage(0);
+  }
+  __syncthreads();
+
+  for (int it = 0; it < n_iters; ++it) {
+    const int64_t q0 = q_begin + (int64_t)it * Cfg::BQ;
+    const bool has_next = it + 1 < n_iters;
+    if (has_next) load_stage(q0 + Cfg::BQ);
+
+    const T* qs_t = reinterpret_cast<const T*>(stage_base(it & 1));
+    const T* dos_t = qs_t + Cfg::TILE;
+    const float* lse2_s = reinterpret_cast<const float*>(stage_base(it & 1) + Cfg::STAGE_ELEMS * Cfg::E);
+    const float* delta_s = lse2_s + Cfg::BQ;
+
+    // Nothing to do when every query of the tile precedes this wave's keys.
+    const bool active = !CAUSAL || q0 + Cfg::BQ - 1 >= kw;
+    if (active) {
+      f32x16 s[QS], dp[QS];
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[qs][r] = 0.0f;
+          dp[qs][r] = 0.0f;
+        }
+      // S = Q K^T and dP = dO V^T (rows: queries in perm32 order; lane: key).
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs) {
+          const Frag<T> a = lds_frag<T>(qs_t + (32 * qs + qrow) * RS + 16 * kc + 8 * h);
+          s[qs] = mma(a, kf[kc], s[qs]);
+          const Frag<T> g = lds_frag<T>(dos_t + (32 * qs + qrow) * RS + 16 * kc + 8 * h);
+          dp[qs] = mma(g, vf[kc], dp[qs]);
+        }
+      }
+      const bool need_mask = CAUSAL && q0 < kw + 31;
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs) {
+        float l2[16], dl[16];
+        *reinterpret_cast<f32x4*>(&l2[0]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 8 * h);
+        *reinterpret_cast<f32x4*>(&l2[4]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 8 * h + 4);
+        *reinterpret_cast<f32x4*>(&l2[8]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 16 + 8 * h);
+        *reinterpret_cast<f32x4*>(&l2[12]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 16 + 8 * h + 4);
+        *reinterpret_cast<f32x4*>(&dl[0]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 8 * h);
+        *reinterpret_cast<f32x4*>(&dl[4]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 8 * h + 4);
+        *reinterpret_cast<f32x4*>(&dl[8]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 16 + 8 * h);
+        *reinterpret_cast<f32x4*>(&dl[12]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 16 + 8 * h + 4);
+        const int key_rel = (int)(key - q0);  // key minus the tile's first query
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pr = fast_exp2(fmaf(s[qs][r], cl2, -l2[r]));
+          if (need_mask && key_rel > 32 * qs + permuted_row(r, h)) pr = 0.0f;
+          s[qs][r] = pr;                          // P
+          dp[qs][r] = pr * (dp[qs][r] - dl[r]);   // dS
+        }
+      }
+      // dV += P^T dO and dK += dS^T Q (A: lane = key row, k = queries).
+#pragma unroll
+      for (int qc = 0; qc < NQC; ++qc) {
+        float tp[8], td[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          tp[e] = s[qc >> 1][8 * (qc & 1) + e];
+          td[e] = dp[qc >> 1][8 * (qc & 1) + e];
+        }
+        const Frag<T> pa = to_frag<T>(tp);
+        const Frag<T> da = to_frag<T>(td);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          Frag<T> bo, bq;
+          if constexpr (sizeof(T) == 2) {
+            bo = lds_col_frag<T>(dos_t, RS, 16 * qc, 32 * dt, lane);
+            bq = lds_col_frag<T>(qs_t, RS, 16 * qc, 32 * dt, lane);
+          } else {
+            bo = lds_col_frag_f32(reinterpret_cast<const float*>(dos_t), RS, 16 * qc, 32 * dt, lane);
+            bq = lds_col_frag_f32(reinterpret_cast<const float*>(qs_t), RS, 16 * qc, 32 * dt, lane);
+          }
+          dv[dt] = mma(pa, bo, dv[dt]);
+          dk[dt] = mma(da, bq, dk[dt]);
+        }
+      }
+    }
+
+    if (has_next) store_stage((it + 1) & 1);
+    __syncthreads();
+  }
+
+  // Accumulators: lane (h, feature c), register r <-> key kw + c_row(r, h).
+  T* dkg = static_cast<T*>(p.dk) + (size_t)bh * p.n_k * D;
+  T* dvg = static_cast<T*>(p.dv) + (size_t)bh * p.n_k * D;
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t kr = kw + c_row(r, h);
+      if (kr < p.n_k) {
+        dkg[kr * D + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
+        dvg[kr * D + 32 * dt + c] = (T)dv[dt][r];
+      }
+    }
+}
+
+// ------------------------------------------------------------------- dQ
+template <typename T, int D, int BK, int OCC, bool CAUSAL>
+__global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
+  constexpr int NT = 256;
+  constexpr int BQ = 128;  // 4 waves x 32 queries
+  constexpr int E = sizeof(T);
+  constexpr int RS = D + 16 / E;
+  constexpr int TILE = BK * RS;
+  constexpr int CPR = D * E / 16;
+  constexpr int CHUNKS = 2 * BK * CPR;
+  constexpr int CPT = CHUNKS / NT;
+  static_assert(CHUNKS % NT == 0, "tile must split evenly");
+  constexpr int KC = D / 16;
+  constexpr int NKT = BK / 32;
+  constexpr int NPC = BK / 16;
+  constexpr int NDT = D / 32;
+
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  T* smem = reinterpret_cast<T*>(smem_raw);
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int h = lane >> 5, c = lane & 31;
+
+  const int w = xcd_remap(blockIdx.x, gridDim.x);
+  const int qt_idx = w % p.n_qtiles;
+  const int bh = w / p.n_qtiles;
+  const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;
+  const int64_t q0 = (int64_t)qtile * BQ;
+  const int64_t qw = q0 + 32 * wave;
+  const int64_t query = qw + c;
+
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+
+  // Q^T and dO^T as B operands: lane (h, query c), k = 16kc + 8h + s.
+  Frag<T> qf[KC], gf[KC];
+  const bool valid = query < p.n_q;
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (valid) {
+      qf[kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
+      gf[kc] = *reinterpret_cast<const Frag<T>*>(dog + query * D + 16 * kc + 8 * h);
+    } else {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        qf[kc][s] = (T)0.0f;
+        gf[kc][s] = (T)0.0f;
+      }
+    }
+  }
+  const float lse2 = valid ? p.lse[(size_t)bh * p.n_q + query] * 1.4426950408889634f : INFINITY;
+  const float delta = valid ? p.delta[(size_t)bh * p.n_q + query] : 0.0f;
+
+  f32x16 acc[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[dt][r] = 0.0f;
+
+  int64_t ke = p.n_k;
+  if (CAUSAL && ke > q0 + BQ) ke = q0 + BQ;
+  const int n_tiles = (int)((ke + BK - 1) / BK);
+
+  u32x4 stage[CPT];
+  auto load_stage = [&](int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int chunk = tid + i * NT;
+      const int which = chunk / (BK * CPR);
+      const int rem = chunk % (BK * CPR);
+      const int row = rem / CPR, col = rem % CPR;
+      const int64_t kr = k0 + row;
+      const T* src = (which ? vg : kg) + kr * D + col * (16 / E);
+      stage[i] = kr < p.n_k ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store_stage = [&](int buf) {
+    T* base = smem + buf * 2 * TILE;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int chunk = tid + i * NT;
+      const int which = chunk / (BK * CPR);
+      const int rem = chunk % (BK * CPR);
+      const int row = rem / CPR, col = rem % CPR;
+      st16(base + which * TILE + row * RS + col * (16 / E), stage[i]);
+    }
+  };
+
+  const int krow = perm32(c);
+  const float cl2 = p.scale_log2;
+
+  if (n_tiles > 0) {
+    load_stage(0);
+    store_stage(0);
+  }
+  __syncthreads();
+
+  for (int it = 0; it < n_tiles; ++it) {
+    const int64_t k0 = (int64_t)it * BK;
+    const bool has_next = it + 1 < n_tiles;
+    if (has_next) load_stage(k0 + BK);
+    const T* ks = smem + (it & 1) * 2 * TILE;
+    const T* vs = ks + TILE;
+    const bool active = !CAUSAL || k0 <= qw + 31;
+    if (active) {
+      f32x16 s[NKT], dp[NKT];
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[kt][r] = 0.0f;
+          dp[kt][r] = 0.0f;
+        }
+      // S^T = K Q^T and dP^T = V dO^T (rows: keys in perm32 order; lane: query).
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) {
+          const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+          s[kt] = mma(a, qf[kc], s[kt]);
+          const Frag<T> b = lds_frag<T>(vs + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+          dp[kt] = mma(b, gf[kc], dp[kt]);
+        }
+      const bool need_mask = (k0 + BK > p.n_k) || (CAUSAL && k0 + BK - 1 > qw);
+      // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
+      // under the causal mask, visible iff x <= q_rel.
+      const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+      const int q_rel = CAUSAL ? (int)(query - k0) : BK;
+      const int lim = q_rel + 1 < key_lim ? q_rel + 1 : key_lim;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pr = fast_exp2(fmaf(s[kt][r], cl2, -lse2));
+          if (need_mask && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
+          dp[kt][r] = pr * (dp[kt][r] - delta);  // dS^T
+        }
+      // dQ^T += K^T dS^T.
+#pragma unroll
+      for (int pc = 0; pc < NPC; ++pc) {
+        float td[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) td[e] = dp[pc >> 1][8 * (pc & 1) + e];
+        const Frag<T> b = to_frag<T>(td);
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          Frag<T> a;
+          if constexpr (sizeof(T) == 2) {
+            a = lds_col_frag<T>(ks, RS, 16 * pc, 32 * dt, lane);
+          } else {
+            a = lds_col_frag_f32(reinterpret_cast<const float*>(ks), RS, 16 * pc, 32 * dt, lane);
+          }
+          acc[dt] = mma(a, b, acc[dt]);
+        }
+      }
+    }
+    if (has_next) store_stage((it + 1) & 1);
+    __syncthreads();
+  }
+
+  if (valid) {
+    T* dqg = static_cast<T*>(p.dq) + ((size_t)bh * p.n_q + query) * D;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        typename FragT<T>::half v4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = (T)(acc[dt][4 * a4 + e] * p.scale);
+        *reinterpret_cast<typename FragT<T>::half*>(dqg + 32 * dt + 8 * a4 + 4 * h) = v4;
+      }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+
+template <typename T, int D> struct BwdShape;
+template <> struct BwdShape<__bf16, 64> { static constexpr int QS = 2, BK = 64, OCC = 2; };
+template <> struct BwdShape<__bf16, 128> { static constexpr int QS = 1, BK = 64, OCC = 1; };
+template <> struct BwdShape<_Float16, 64> { static constexpr int QS = 2, BK = 64, OCC = 2; };
+template <> struct BwdShape<_Float16, 128> { static constexpr int QS = 1, BK = 64, OCC = 1; };
+template <> struct BwdShape<float, 64> { static constexpr int QS = 2, BK = 32, OCC = 1; };
+template <> struct BwdShape<float, 128> { static constexpr int QS = 1, BK = 32, OCC = 1; };
+
+template <typename T, int D, bool CAUSAL>
+static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
+  using S = BwdShape<T, D>;
+  using Dk = DkdvTile<T, D, S::QS>;
+  void* args[] = {&p};
+  const int64_t rows = (int64_t)p.bh * p.n_q;
+  constexpr int RPB = 256 / (D * (int)sizeof(T) / 16);
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<T, D>),
+                                 dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
+  if (e != hipSuccess) return e;
+  p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
+  p.n_qtiles = (int)((p.n_q + 127) / 128);
+  if (p.dk) {
+    e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, D, S::QS, S::OCC, CAUSAL>),
+                        dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
+    if (e != hipSuccess || !p.dq) return e;
+  }
+  const int dq_lds = 2 * 2 * S::BK * (D + 16 / (int)sizeof(T)) * (int)sizeof(T);
+  return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, D, S::BK, S::OCC, CAUSAL>),
+                         dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(256), args, dq_lds, stream);
+}
+
+template <typename T, int D>
+static hipError_t launch_bwd_dt(const BwdParams& p, bool causal, hipStream_t stream) {
+  return causal ? launch_bwd_impl<T, D, true>(p, stream) : launch_bwd_impl<T, D, false>(p, stream);
+}
+
+hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, hipStream_t stream) {
+  switch (dtype * 1000 + d) {
+    case 0 * 1000 + 64: return launch_bwd_dt<float, 64>(p, causal, stream);
+    case 0 * 1000 + 128: return launch_bwd_dt<float, 128>(p, causal, stream);
+    case 1 * 1000 + 64: return launch_bwd_dt<_Float16, 64>(p, causal, stream);
+    case 1 * 1000 + 128: return launch_bwd_dt<_Float16, 128>(p, causal, stream);
+    case 2 * 1000 + 64: return launch_bwd_dt<__bf16, 64>(p, causal, stream);
+    case 2 * 1000 + 128: return launch_bwd_dt<__bf16, 128>(p, causal, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace mea

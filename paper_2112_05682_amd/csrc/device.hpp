@@ -1,0 +1,143 @@
+// Device primitives for the gfx950 (CDNA4) attention kernels: MFMA fragment
+// types and wrappers, lane bookkeeping for the 32x32 MFMA tiles, LDS reads
+// (plain and transposing), wave-half exchanges and numeric helpers.
+//
+// MFMA tile conventions used by every kernel (v_mfma_f32_32x32x{16,2}):
+//   lane l = 32*h + c with h = l / 32 (lane half) and c = l % 32;
+//   A fragment: lane holds A[row c][k = 8h + s], s = 0..7;
+//   B fragment: lane holds B[k = 8h + s][col c], s = 0..7;
+//   C tile    : lane holds C[row 8*(r/4) + 4h + r%4][col c], r = 0..15.
+// A "fragment" is always 8 consecutive k values, so a 16-wide k chunk is one
+// 32x32x16 MFMA for 16-bit types and eight 32x32x2 MFMAs for float32 (MFMA s
+// consumes element s of both fragments, i.e. the k pair {s, 8 + s}).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mea {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <typename T> struct FragT;
+template <> struct FragT<__bf16> { typedef bf16x8 type; typedef bf16x4 half; };
+template <> struct FragT<_Float16> { typedef f16x8 type; typedef f16x4 half; };
+template <> struct FragT<float> { typedef f32x8 type; typedef f32x4 half; };
+template <typename T> using Frag = typename FragT<T>::type;
+
+// C += A * B over a 16-wide k chunk.
+__device__ __forceinline__ f32x16 mma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mma(const f16x8& a, const f16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mma(const f32x8& a, const f32x8& b, f32x16 c) {
+#pragma unroll
+  for (int s = 0; s < 8; ++s) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], c, 0, 0, 0);
+  return c;
+}
+
+// Row of the 32x32 C tile held in register r by a lane of half h.
+__device__ __forceinline__ constexpr int c_row(int r, int h) { return 8 * (r / 4) + 4 * h + (r % 4); }
+
+// Row permutation applied when an operand's rows are read into an A (or B)
+// fragment: with A row i taken from source row perm32(i), register r of lane
+// half h in the C tile holds source row 16*(r/8) + 8h + (r%8).  Registers
+// 8m..8m+7 of a lane then cover 8 consecutive source rows (16m + 8h + s), which
+// is exactly the k layout of a fragment: a C tile can feed the next MFMA as a
+// B (or A) operand with no data movement between lanes.
+__device__ __forceinline__ constexpr int perm32(int i) {
+  return 16 * ((i >> 3) >> 1) + 8 * ((i >> 2) & 1) + 4 * ((i >> 3) & 1) + (i & 3);
+}
+__device__ __forceinline__ constexpr int permuted_row(int r, int h) { return 16 * (r / 8) + 8 * h + (r % 8); }
+
+// Eight consecutive elements from LDS (16 B for 16-bit types, 32 B for float).
+template <typename T>
+__device__ __forceinline__ Frag<T> lds_frag(const T* p) {
+  return *reinterpret_cast<const Frag<T>*>(p);
+}
+
+// Transposing LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes,
+// lane i supplies an 8-byte address e_i and receives element (i % 4) of the
+// four chunks e_{4r + i/4}, r = 0..3.  With lane i pointing at
+// row (base_row + i/4), column (base_col + 4*(i%4)) of a row-major tile, lane
+// i receives column base_col + i of rows base_row .. base_row + 3.
+typedef short v4s_t __attribute__((__vector_size__(4 * sizeof(short))));
+__device__ __forceinline__ v4s_t lds_read_tr16(const void* p) {
+  typedef __attribute__((address_space(3))) v4s_t lds_v4s;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4s*)((__attribute__((address_space(3))) char*)((__attribute__((address_space(3))) void*)p)));
+}
+
+// Column fragment of a row-major 16-bit tile: lane (h, c) gets column col0 + c
+// of rows row0 + 8h + s, s = 0..7 (rs = row stride in elements).  Lanes are
+// grouped by 16: group g covers columns col0 + 16*(g%2) + 0..15, lane half g/2.
+template <typename T>
+__device__ __forceinline__ Frag<T> lds_col_frag(const T* tile, int rs, int row0, int col0, int lane) {
+  static_assert(sizeof(T) == 2, "transposing read is for 16-bit elements");
+  const int g = lane >> 4, i = lane & 15;
+  const int row = row0 + 8 * (g >> 1) + (i >> 2);
+  const int col = col0 + 16 * (g & 1) + 4 * (i & 3);
+  const v4s_t lo = lds_read_tr16(tile + row * rs + col);
+  const v4s_t hi = lds_read_tr16(tile + (row + 4) * rs + col);
+  typedef short v8s_t __attribute__((ext_vector_type(8)));
+  v8s_t r;
+  r[0] = lo[0]; r[1] = lo[1]; r[2] = lo[2]; r[3] = lo[3];
+  r[4] = hi[0]; r[5] = hi[1]; r[6] = hi[2]; r[7] = hi[3];
+  return __builtin_bit_cast(Frag<T>, r);
+}
+
+// Float32 column fragment: eight scalar reads.
+__device__ __forceinline__ f32x8 lds_col_frag_f32(const float* tile, int rs, int row0, int col0, int lane) {
+  const int h = lane >> 5, c = lane & 31;
+  f32x8 r;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) r[s] = tile[(row0 + 8 * h + s) * rs + col0 + c];
+  return r;
+}
+
+// Value of x in the lane of the other half (l ^ 32), via v_permlane32_swap:
+// for l < 32 the pair is (x[l], x[l+32]); for l >= 32 it is (x[l-32], x[l]).
+__device__ __forceinline__ float xhalf_max(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float xhalf_sum(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Convert eight float32 values to a fragment of T (round to nearest even).
+template <typename T>
+__device__ __forceinline__ Frag<T> to_frag(const float* x) {
+  Frag<T> r;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) r[s] = (T)x[s];
+  return r;
+}
+
+// 16-byte global load / store helpers.
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// Workgroup id remap for the 8 XCDs of the chip: hardware hands workgroup w to
+// XCD w % 8, so give each XCD a contiguous range of logical tiles (neighbours
+// share K/V in that XCD's L2).  Bijective on [0, n).
+__device__ __forceinline__ int xcd_remap(int w, int n) {
+  const int x = w & 7, i = w >> 3;
+  const int per = n >> 3, rem = n & 7;
+  return x * per + (x < rem ? x : rem) + i;
+}
+
+}  // namespace mea

@@ -1,0 +1,64 @@
+// Host-side interface between the C ABI (api.hip) and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mea {
+
+// Arguments of the forward kernels (passed by value).
+struct FwdParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;     // [B*H, n_q] or null
+  float* part_o;  // split partials [S, B*H, n_q, D] (n_splits > 1)
+  float* part_m;  // [S, B*H, n_q]
+  float* part_l;  // [S, B*H, n_q]
+  int64_t n_q;
+  int64_t n_k;
+  int64_t keys_per_split;  // multiple of the key tile
+  int bh;                  // B * H
+  int n_qtiles;
+  int n_splits;
+  float scale;       // score scale
+  float scale_log2;  // scale * log2(e)
+};
+
+// Arguments of the backward kernels.
+struct BwdParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const void* d_o;
+  const float* lse;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* delta;  // D_i = dO_i . O_i, [B*H, n_q]
+  int64_t n_q;
+  int64_t n_k;
+  int bh;
+  int n_qtiles;  // query tiles of the dQ kernel
+  int n_ktiles;  // key tiles of the dK/dV kernel
+  float scale;
+  float scale_log2;
+};
+
+// Tile shapes per (element type, head dimension); shared by the host plan
+// and the kernel instantiations.
+template <typename T, int D> struct FwdShape;
+template <> struct FwdShape<__bf16, 64> { static constexpr int QT = 2, BK = 64, BQ = 256; };
+template <> struct FwdShape<__bf16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128; };
+template <> struct FwdShape<_Float16, 64> { static constexpr int QT = 2, BK = 64, BQ = 256; };
+template <> struct FwdShape<_Float16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128; };
+template <> struct FwdShape<float, 64> { static constexpr int QT = 1, BK = 32, BQ = 128; };
+template <> struct FwdShape<float, 128> { static constexpr int QT = 1, BK = 32, BQ = 128; };
+
+// dtype codes follow mea_dtype: 0 = f32, 1 = f16, 2 = bf16.
+hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, hipStream_t stream);
+hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, hipStream_t stream);
+
+}  // namespace mea

@@ -1,0 +1,138 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/mea.h, sizes workspaces, and rejects bad arguments before
+launching anything (every case below fails validation, so no kernel runs)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2112_05682_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mea.h")
+
+FAKE = 0x10000  # aligned non-null address; only used where validation must fail first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mea_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(_lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_status_strings():
+    for s in range(5):
+        assert _lib.status_string(s)
+    assert _lib.status_string(99) == "unknown status"
+
+
+def prob(**kw):
+    base = dict(batch=1, heads=2, n_q=100, n_k=100, d=64, dtype=_lib.MEA_BF16, causal=0,
+                scale=0.125)
+    base.update(kw)
+    # built directly (no normalisation) so that invalid fields reach the library
+    return _lib.MeaProblem(base["batch"], base["heads"], base["n_q"], base["n_k"], base["d"],
+                           base["dtype"], base["causal"], base["scale"])
+
+
+def ws_status(p):
+    out = ctypes.c_size_t(0)
+    return _lib.load().mea_attention_fwd_workspace_size(ctypes.byref(p), ctypes.byref(out)), out
+
+
+def test_workspace_sizes():
+    # One query tile per head and a long key sequence: keys are split, and the
+    # per-split summaries (d + 2 floats per row and split) need workspace.
+    p = prob(heads=1, n_q=256, n_k=1 << 20)
+    ws = _lib.fwd_workspace_size(p)
+    assert ws >= 2 * 256 * (64 + 2) * 4
+    # Many query tiles: no split, no forward workspace.
+    assert _lib.fwd_workspace_size(prob(heads=16, n_q=16384, n_k=16384)) == 0
+    # Backward: D_i, one float per query row.
+    assert _lib.bwd_workspace_size(prob(heads=16, n_q=16384, n_k=16384)) >= 16 * 16384 * 4
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=32), _lib.MEA_ERR_UNSUPPORTED),
+    (dict(d=96), _lib.MEA_ERR_UNSUPPORTED),
+    (dict(dtype=7), _lib.MEA_ERR_UNSUPPORTED),
+    (dict(n_q=0), _lib.MEA_ERR_INVALID_ARG),
+    (dict(n_k=0), _lib.MEA_ERR_INVALID_ARG),
+    (dict(batch=0), _lib.MEA_ERR_INVALID_ARG),
+    (dict(heads=-1), _lib.MEA_ERR_INVALID_ARG),
+    (dict(scale=0.0), _lib.MEA_ERR_INVALID_ARG),
+    (dict(scale=-1.0), _lib.MEA_ERR_INVALID_ARG),
+    (dict(scale=float("nan")), _lib.MEA_ERR_INVALID_ARG),
+    (dict(scale=float("inf")), _lib.MEA_ERR_INVALID_ARG),
+    (dict(causal=2), _lib.MEA_ERR_INVALID_ARG),
+    (dict(n_q=1 << 31), _lib.MEA_ERR_INVALID_ARG),
+    (dict(batch=1 << 40, heads=1 << 40), _lib.MEA_ERR_INVALID_ARG),
+])
+def test_problem_validation(kw, status):
+    p = prob(**kw)
+    st, _ = ws_status(p)
+    assert st == status
+    lib = _lib.load()
+    out = ctypes.c_size_t(0)
+    assert lib.mea_attention_bwd_workspace_size(ctypes.byref(p), ctypes.byref(out)) == status
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == status
+    assert _lib.bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+                    None) == status
+
+
+def test_null_problem_and_null_size_pointer():
+    lib = _lib.load()
+    out = ctypes.c_size_t(0)
+    assert lib.mea_attention_fwd_workspace_size(None, ctypes.byref(out)) == _lib.MEA_ERR_INVALID_ARG
+    p = prob()
+    assert lib.mea_attention_fwd_workspace_size(ctypes.byref(p), None) == _lib.MEA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("which", range(4))
+def test_fwd_rejects_null_or_misaligned_pointers(which):
+    p = prob()
+    for bad in (None, FAKE + 2):
+        ptrs = [FAKE] * 4
+        ptrs[which] = bad
+        assert _lib.fwd(p, *ptrs, None, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+    # misaligned lse
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE + 4, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("which", range(6))
+def test_bwd_rejects_null_inputs(which):
+    p = prob()
+    ptrs = [FAKE] * 9
+    ptrs[which] = None
+    assert _lib.bwd(p, *ptrs, FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("grads", [(None, None, None), (FAKE, FAKE, None), (FAKE, None, FAKE),
+                                   (None, FAKE, None), (FAKE + 8, FAKE, FAKE)])
+def test_bwd_rejects_bad_gradient_pointer_sets(grads):
+    # dq optional; dk and dv both or neither; at least one group; 16 B aligned.
+    p = prob()
+    assert _lib.bwd(p, *([FAKE] * 6), *grads, FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+
+
+def test_workspace_too_small_is_rejected_before_launch():
+    p = prob(heads=1, n_q=256, n_k=1 << 20)
+    need = _lib.fwd_workspace_size(p)
+    assert need > 0
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.MEA_ERR_WORKSPACE
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == _lib.MEA_ERR_WORKSPACE
+    need_b = _lib.bwd_workspace_size(p)
+    assert _lib.bwd(p, *([FAKE] * 9), None, 0, None) == _lib.MEA_ERR_WORKSPACE
+    assert _lib.bwd(p, *([FAKE] * 9), FAKE, need_b - 1, None) == _lib.MEA_ERR_WORKSPACE

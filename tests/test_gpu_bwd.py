@@ -1,0 +1,105 @@
+"""GPU parity of the backward pass against the float64 oracle's hand-derived
+gradients.  The GPU backward consumes the GPU forward's O and LSE (as it does
+in training); the oracle recomputes everything from Q, K, V, dO."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2112_05682_amd import attention, attention_bwd, attention_fwd
+from paper_2112_05682_amd.inputs import WORKLOADS, attention_inputs, workload_inputs
+from parity_util import TOL, f64, rel_err, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_grads(g, causal):
+    o, lse = attention_fwd(g["q"], g["k"], g["v"], causal=causal)
+    dq, dk, dv = attention_bwd(g["q"], g["k"], g["v"], o, lse, g["do"], causal=causal)
+    torch.cuda.synchronize()
+    return dq, dk, dv
+
+
+def run_and_compare(B, H, nq, nk, d, dtype, causal, std=1.0, qk_mult=1.0):
+    print("case B=%d H=%d nq=%d nk=%d d=%d %s causal=%s mult=%s" % (B, H, nq, nk, d, dtype,
+                                                                     causal, qk_mult), flush=True)
+    x = attention_inputs(B, H, nq, nk, d, dtype, std, qk_mult)
+    dq, dk, dv = gpu_grads(to_gpu(x), causal)
+    rq, rk, rv = oracle.bwd(f64(x["q"]), f64(x["k"]), f64(x["v"]), f64(x["do"]),
+                            scale=d ** -0.5, causal=causal)
+    errs = {"dQ": rel_err(f64(dq), rq), "dK": rel_err(f64(dk), rk), "dV": rel_err(f64(dv), rv)}
+    print("  ", {k: "%.3g" % v for k, v in errs.items()}, flush=True)
+    for name, e in errs.items():
+        assert e <= TOL[dtype], (name, e)
+
+
+SHAPES = [(1, 1, 1, 1), (1, 2, 7, 100), (2, 3, 129, 257), (1, 1, 700, 700), (1, 2, 300, 70),
+          (1, 1, 64, 1500)]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16", "fp16"])
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_backward_small(dtype, d, causal, shape):
+    run_and_compare(*shape, d, dtype, causal)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_backward_large_logits(d):
+    run_and_compare(1, 2, 300, 500, d, "bf16", False, qk_mult=30.0)
+    run_and_compare(1, 2, 300, 500, d, "bf16", True, qk_mult=30.0)
+
+
+def test_backward_fp32_self_attention_n256():
+    w = WORKLOADS["selfattn_fp32_b1h1_n256_d64"]
+    run_and_compare(w.batch, w.heads, w.n_q, w.n_k, w.d, w.dtype, w.causal)
+
+
+def sampled(n, count, seed):
+    rng = np.random.default_rng(seed)
+    idx = rng.choice(n, size=count - 2, replace=False)
+    return np.unique(np.concatenate([[0, n - 1], idx]))
+
+
+@pytest.mark.parametrize("name", ["selfattn_bf16_b1h16_n16384_d64",
+                                  "causal_bf16_b4h32_n8192_d128"])
+def test_backward_full_size_sampled(name):
+    # Full-size workloads: the oracle recomputes sampled dQ rows and sampled
+    # dK / dV rows of a few (batch, head) slices.
+    w = WORKLOADS[name]
+    print("workload", name, flush=True)
+    x = workload_inputs(w)
+    dq, dk, dv = gpu_grads(to_gpu(x), w.causal)
+    dq, dk, dv = dq.cpu(), dk.cpu(), dv.cpu()
+    for b, h in sorted({(0, 0), (w.batch - 1, w.heads - 1)}):
+        args = (f64(x["q"][b, h]), f64(x["k"][b, h]), f64(x["v"][b, h]), f64(x["do"][b, h]))
+        rows = sampled(w.n_q, 32, 7 + h)
+        keys = sampled(w.n_k, 32, 9 + h)
+        rq = oracle.bwd_dq_rows(*args, rows, scale=w.d ** -0.5, causal=w.causal)
+        rk, rv = oracle.bwd_dkdv_keys(*args, keys, scale=w.d ** -0.5, causal=w.causal)
+        errs = (rel_err(f64(dq[b, h, rows]), rq), rel_err(f64(dk[b, h, keys]), rk),
+                rel_err(f64(dv[b, h, keys]), rv))
+        print("  slice", (b, h), "dQ %.3g dK %.3g dV %.3g" % errs, flush=True)
+        assert max(errs) <= TOL[w.dtype], errs
+    for t in (dq, dk, dv):
+        assert torch.isfinite(t).all()
+
+
+def test_backward_is_deterministic():
+    g = to_gpu(attention_inputs(1, 3, 900, 1100, 64, "bf16"))
+    a = gpu_grads(g, True)
+    b = gpu_grads(g, True)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_autograd_function_matches_direct_calls():
+    g = to_gpu(attention_inputs(2, 2, 200, 300, 64, "bf16"))
+    q = g["q"].clone().requires_grad_()
+    k = g["k"].clone().requires_grad_()
+    v = g["v"].clone().requires_grad_()
+    o = attention(q, k, v, causal=True)
+    o.backward(g["do"])
+    dq, dk, dv = gpu_grads(g, True)
+    assert torch.equal(q.grad, dq) and torch.equal(k.grad, dk) and torch.equal(v.grad, dv)
