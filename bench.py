@@ -62,30 +62,30 @@ def load_traffic(kernel: str):
     return ent.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, seconds_hint: float):
-    """Time the float64 oracle (forward + backward) on one (batch, head) slice
-    of the workload, restricted to the first n_s query rows and keys."""
-    import numpy as np
-
+def cpu_baseline(w):
+    """Time the float64 oracle (forward + backward) on whole (batch, head)
+    slices of the workload (heads are independent, so a slice is exact)."""
     import oracle
     from paper_2112_05682_amd.inputs import attention_inputs
 
-    n_s = int(os.environ.get("MEA_CPU_SAMPLE_N", "8192"))
-    x = attention_inputs(1, 1, n_s, n_s, w.d, w.dtype, w.std, w.qk_mult)
+    # Two full heads of the workload: about 10 s on 16 host threads.
+    heads = int(os.environ.get("MEA_CPU_SAMPLE_HEADS", "2"))
+    x = attention_inputs(1, heads, w.n_q, w.n_k, w.d, w.dtype, w.std, w.qk_mult)
     q, k, v, do = (x[n].double().numpy() for n in ("q", "k", "v", "do"))
     t0 = time.perf_counter()
     oracle.fwd(q, k, v, scale=w.d ** -0.5, causal=w.causal)
     oracle.bwd(q, k, v, do, scale=w.d ** -0.5, causal=w.causal)
     dt = time.perf_counter() - t0
-    pairs = n_s * n_s if not w.causal else n_s * (n_s + 1) // 2
+    pairs = heads * (w.n_q * w.n_k if not w.causal else w.n_q * (w.n_q + 1) // 2)
     flops = 14.0 * w.d * pairs
     return {
         "value": flops / dt / 1e12,
         "unit": "TFLOP/s",
         "cores": oracle.num_threads(),
         "kind": "oracle",
-        "sample": "one head, n_q = n_k = %d, d = %d, float64 forward + backward (%.1f s); "
-                  "credited 14*d*pairs flop / time" % (n_s, w.d, dt),
+        "sample": "%d of %d heads (n_q = %d, n_k = %d, d = %d), float64 forward + backward "
+                  "(%.1f s); credited 14*d*pairs flop / time" % (heads, w.heads, w.n_q, w.n_k,
+                                                                 w.d, dt),
         "seconds": dt,
         "host_cpu": platform.processor() or platform.machine(),
     }
@@ -138,14 +138,17 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
 
-    # Peak memory above inputs and outputs during one step (the paper's
-    # "memory overhead", Section 5.1), from torch's allocator.
+    # Peak memory in excess of inputs and outputs (the paper's "memory
+    # overhead", Section 5.1) during one forward + backward with every output
+    # kept alive, from torch's allocator.
     torch.cuda.reset_peak_memory_stats(dev)
     base_alloc = torch.cuda.memory_allocated(dev)
-    step()
+    o_, lse_ = attention_fwd(q, k, v, causal=w.causal)
+    grads_ = attention_bwd(q, k, v, o_, lse_, do, causal=w.causal)
     torch.cuda.synchronize()
     peak_extra = torch.cuda.max_memory_allocated(dev) - base_alloc
-    out_bytes = (2 * q.numel() + k.numel() + v.numel()) * q.element_size()  # o, dq, dk, dv
+    out_bytes = sum(t.numel() * t.element_size() for t in (o_, *grads_))  # o, dq, dk, dv
+    del o_, lse_, grads_
 
     t_fwd = t_dkdv = t_dq = 0.0
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -225,7 +228,7 @@ def main() -> int:
                      "traffic": traffic},
     }
     if not args.no_cpu_baseline:
-        cb = cpu_baseline(w, 20.0)
+        cb = cpu_baseline(w)
         out["cpu_baseline"] = {kk: (round(vv, 6) if isinstance(vv, float) else vv)
                                for kk, vv in cb.items() if kk not in ("host_cpu",)}
     print(json.dumps(out), flush=True)

@@ -33,8 +33,9 @@
  *     validation error nothing is enqueued and the status says why.  A
  *     launch failure reported by the HIP runtime returns MEA_ERR_HIP.  Errors
  *     during kernel execution surface at the caller's next synchronisation.
- *   - Supported: d in {64, 128}; dtype f32, f16 or bf16 (all tensors of one
- *     call share it; lse, the workspace and all accumulation are float32).
+ *   - Supported: d in {64, 128}; dtype f32, f16 or bf16 (q, k, v and the
+ *     gradients share it; o and do share it too unless out_f32 asks for
+ *     float32; lse, the workspace and all accumulation are float32).
  *     Sizes: batch, heads, n_q, n_k >= 1; every element count must fit in
  *     int64 and n_q, n_k <= 2^31 - 1.
  */
@@ -67,9 +68,12 @@ typedef struct {
   int64_t n_q;    /* queries per (b, h) >= 1 */
   int64_t n_k;    /* keys = values per (b, h) >= 1 */
   int64_t d;      /* head dimension of q, k and v: 64 or 128 */
-  int32_t dtype;  /* mea_dtype of q, k, v, o, do, dq, dk, dv */
-  int32_t causal; /* 0 = no mask, 1 = top-left causal mask (see above) */
-  float scale;    /* score scale, finite and > 0; 1/sqrt(d) in the paper */
+  int32_t dtype;   /* mea_dtype of q, k, v, dq, dk, dv (and of o, do unless out_f32) */
+  int32_t causal;  /* 0 = no mask, 1 = top-left causal mask (see above) */
+  float scale;     /* score scale, finite and > 0; 1/sqrt(d) in the paper */
+  int32_t out_f32; /* 0: o and do in `dtype`; 1: o and do in float32 (the
+                      paper's experiments use 16-bit inputs with a float32
+                      output, Section 5.1); ignored when dtype is MEA_F32 */
 } mea_problem;
 
 /* Bytes of device workspace mea_attention_fwd needs for `p` (written to
@@ -85,7 +89,8 @@ mea_status mea_attention_fwd_workspace_size(const mea_problem* p, size_t* bytes)
 mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes);
 
 /* Forward (Sections 2-4): o = softmax(scale * q k^T) v, computed tile by
- * tile with the running max / numerator / denominator; writes o (dtype) and,
+ * tile with the running max / numerator / denominator; writes o (in dtype, or
+ * float32 with out_f32) and,
  * if lse != NULL, lse_i = max_j s_ij + ln sum_j e^{s_ij - max_j s_ij} in
  * natural-log units (float32), which the backward needs.  `workspace` may be
  * NULL only when the required size is 0. */
@@ -94,7 +99,8 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
                              size_t workspace_bytes, hipStream_t stream);
 
 /* Backward (Section 5.2, recompute instead of storing the n_q x n_k matrix):
- * given the forward's o and lse and the upstream gradient do, writes
+ * given the forward's o and lse and the upstream gradient do (both in the
+ * output dtype), writes
  *   dv_j = sum_i w_ij do_i,
  *   dk_j = scale sum_i w_ij (do_i . v_j - D_i) q_i,
  *   dq_i = scale sum_j w_ij (do_i . v_j - D_i) k_j,

@@ -41,6 +41,7 @@ class MeaProblem(ctypes.Structure):
         ("dtype", ctypes.c_int32),
         ("causal", ctypes.c_int32),
         ("scale", ctypes.c_float),
+        ("out_f32", ctypes.c_int32),
     ]
 
 
@@ -87,9 +88,9 @@ def check(name: str, status: int) -> None:
         raise MeaError(name, status, status_string(status))
 
 
-def problem(batch, heads, n_q, n_k, d, dtype, causal, scale) -> MeaProblem:
+def problem(batch, heads, n_q, n_k, d, dtype, causal, scale, out_f32=False) -> MeaProblem:
     return MeaProblem(int(batch), int(heads), int(n_q), int(n_k), int(d), int(dtype),
-                      int(bool(causal)), float(scale))
+                      int(bool(causal)), float(scale), int(bool(out_f32)))
 
 
 def fwd_workspace_size(p: MeaProblem) -> int:

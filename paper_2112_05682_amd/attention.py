@@ -2,8 +2,10 @@
 through torch, and the current HIP stream.  Every step of the computation runs
 in the HIP kernels of ``libmea.so``; nothing here computes attention.
 
-Tensors are ``[B, H, n, d]``, contiguous, on one GPU, all of one dtype
-(float32, float16 or bfloat16); d must be 64 or 128.
+Tensors are ``[B, H, n, d]``, contiguous, on one GPU; q, k, v and the
+gradients share one dtype (float32, float16 or bfloat16), o and do share it or
+are float32 (16-bit inputs with a float32 output, as in the paper's
+experiments); d must be 64 or 128.
 """
 from __future__ import annotations
 
@@ -17,7 +19,7 @@ _DTYPE_CODE = {torch.float32: _lib.MEA_F32, torch.float16: _lib.MEA_F16,
                torch.bfloat16: _lib.MEA_BF16}
 
 
-def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale):
+def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: bool = False):
     if q.dim() != 4 or k.dim() != 4:
         raise ValueError("q and k must be [B, H, n, d]")
     B, H, n_q, d = q.shape
@@ -26,7 +28,8 @@ def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale):
         raise TypeError("unsupported dtype %s" % q.dtype)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
-    return _lib.problem(B, H, n_q, n_k, d, _DTYPE_CODE[q.dtype], causal, scale)
+    return _lib.problem(B, H, n_q, n_k, d, _DTYPE_CODE[q.dtype], causal, scale,
+                        out_f32 and q.dtype != torch.float32)
 
 
 def _check_tensors(names, tensors, dtype, device):
@@ -54,15 +57,20 @@ def bwd_workspace_bytes(q, k, causal=False, scale=None) -> int:
 
 
 def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: bool = False,
-                  scale: float | None = None, need_lse: bool = True, out=None):
-    """Returns ``(o, lse)``; ``lse`` is float32 ``[B, H, n_q]`` (None if not needed)."""
+                  scale: float | None = None, need_lse: bool = True, out=None,
+                  out_dtype: torch.dtype | None = None):
+    """Returns ``(o, lse)``; ``lse`` is float32 ``[B, H, n_q]`` (None if not needed).
+    ``out_dtype`` is q's dtype (default) or torch.float32."""
     if k.shape != v.shape or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
         raise ValueError("shape mismatch: q %s k %s v %s" % (tuple(q.shape), tuple(k.shape),
                                                               tuple(v.shape)))
     _check_tensors(("q", "k", "v"), (q, k, v), q.dtype, q.device)
-    p = _problem(q, k, causal, scale)
-    o = torch.empty_like(q) if out is None else out
-    _check_tensors(("out",), (o,), q.dtype, q.device)
+    out_dtype = q.dtype if out_dtype is None else out_dtype
+    if out_dtype not in (q.dtype, torch.float32):
+        raise TypeError("out_dtype must be q's dtype or float32")
+    p = _problem(q, k, causal, scale, out_dtype == torch.float32)
+    o = torch.empty(q.shape, dtype=out_dtype, device=q.device) if out is None else out
+    _check_tensors(("out",), (o,), out_dtype, q.device)
     lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if need_lse else None
     ws_bytes = _lib.fwd_workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device) if ws_bytes else None
@@ -77,13 +85,16 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
                   need_dq: bool = True, need_dkdv: bool = True):
     """Returns ``(dq, dk, dv)`` for the upstream gradient ``do``; a gradient that
     is not needed is returned as None and its kernel is not run."""
-    _check_tensors(("q", "k", "v", "o", "do"), (q, k, v, o, do), q.dtype, q.device)
+    _check_tensors(("q", "k", "v"), (q, k, v), q.dtype, q.device)
+    if o.dtype not in (q.dtype, torch.float32):
+        raise TypeError("o must have q's dtype or float32")
+    _check_tensors(("o", "do"), (o, do), o.dtype, q.device)
     _check_tensors(("lse",), (lse,), torch.float32, q.device)
     if o.shape != q.shape or do.shape != q.shape or tuple(lse.shape) != tuple(q.shape[:3]):
         raise ValueError("o, do must match q and lse must be [B, H, n_q]")
     if not (need_dq or need_dkdv):
         raise ValueError("nothing to compute")
-    p = _problem(q, k, causal, scale)
+    p = _problem(q, k, causal, scale, o.dtype == torch.float32)
     dq = torch.empty_like(q) if need_dq else None
     dk = torch.empty_like(k) if need_dkdv else None
     dv = torch.empty_like(v) if need_dkdv else None
@@ -102,9 +113,9 @@ class MemoryEfficientAttention(torch.autograd.Function):
     """Autograd wrapper: saves only q, k, v, o and the O(n) lse."""
 
     @staticmethod
-    def forward(ctx, q, k, v, causal=False, scale=None):
+    def forward(ctx, q, k, v, causal=False, scale=None, out_dtype=None):
         q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
-        o, lse = attention_fwd(q, k, v, causal, scale, need_lse=True)
+        o, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out_dtype=out_dtype)
         ctx.save_for_backward(q, k, v, o, lse)
         ctx.causal = causal
         ctx.scale = scale
@@ -113,10 +124,12 @@ class MemoryEfficientAttention(torch.autograd.Function):
     @staticmethod
     def backward(ctx, do):
         q, k, v, o, lse = ctx.saved_tensors
-        dq, dk, dv = attention_bwd(q, k, v, o, lse, do.contiguous(), ctx.causal, ctx.scale)
-        return dq, dk, dv, None, None
+        dq, dk, dv = attention_bwd(q, k, v, o, lse, do.to(o.dtype).contiguous(), ctx.causal,
+                                   ctx.scale)
+        return dq, dk, dv, None, None, None
 
 
-def attention(q, k, v, causal: bool = False, scale: float | None = None):
+def attention(q, k, v, causal: bool = False, scale: float | None = None,
+              out_dtype: torch.dtype | None = None):
     """Exact softmax attention, differentiable, O(n) extra memory."""
-    return MemoryEfficientAttention.apply(q, k, v, causal, scale)
+    return MemoryEfficientAttention.apply(q, k, v, causal, scale, out_dtype)

@@ -29,6 +29,7 @@ mea_status check_problem(const mea_problem* p) {
     return MEA_ERR_INVALID_ARG;
   if (p->n_q >= kMaxSeq || p->n_k >= kMaxSeq) return MEA_ERR_INVALID_ARG;
   if (p->causal != 0 && p->causal != 1) return MEA_ERR_INVALID_ARG;
+  if (p->out_f32 != 0 && p->out_f32 != 1) return MEA_ERR_INVALID_ARG;
   if (!(p->scale > 0.0f) || !isfinite(p->scale)) return MEA_ERR_INVALID_ARG;
   int64_t bh, nq_d, nk_d, tot;
   if (!mul_ok(p->batch, p->heads, &bh) || bh >= kMaxSeq) return MEA_ERR_INVALID_ARG;
@@ -171,7 +172,7 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
   }
   const int64_t grid = (int64_t)fp.n_qtiles * fp.bh * fp.n_splits;
   if (grid >= ((int64_t)1 << 31)) return MEA_ERR_INVALID_ARG;
-  const hipError_t e = mea::launch_fwd(fp, p->dtype, (int)p->d, p->causal != 0, stream);
+  const hipError_t e = mea::launch_fwd(fp, p->dtype, (int)p->d, p->causal != 0, p->out_f32 != 0, stream);
   return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;
 }
 
@@ -208,7 +209,7 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   bp.bh = (int)(p->batch * p->heads);
   bp.scale = p->scale;
   bp.scale_log2 = p->scale * kLog2e;
-  const hipError_t e = mea::launch_bwd(bp, p->dtype, (int)p->d, p->causal != 0, stream);
+  const hipError_t e = mea::launch_bwd(bp, p->dtype, (int)p->d, p->causal != 0, p->out_f32 != 0, stream);
   if (e == hipErrorNotSupported) return MEA_ERR_UNSUPPORTED;
   return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;
 }

@@ -19,8 +19,9 @@
 namespace mea {
 
 // ------------------------------------------------------------------- pre
-template <typename T, int D>
+template <typename TO, int D>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
+  using T = TO;  // o and do share the output dtype
   constexpr int E = sizeof(T);
   constexpr int TPR = D * E / 16;  // threads per row, 16 bytes each
   constexpr int RPB = 256 / TPR;
@@ -57,7 +58,7 @@ struct DkdvTile {
   static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
 };
 
-template <typename T, int D, int QS, int OCC, bool CAUSAL>
+template <typename T, typename TO, int D, int QS, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   using Cfg = DkdvTile<T, D, QS>;
   constexpr int RS = Cfg::RS;
@@ -79,7 +80,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   const int64_t key = kw + c;
 
   const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + (size_t)bh * p.n_q * D;
   const float* __restrict__ lseg = p.lse + (size_t)bh * p.n_q;
   const float* __restrict__ deltag = p.delta + (size_t)bh * p.n_q;
   const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
@@ -126,8 +127,11 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
         const int rem = chunk % (Cfg::BQ * Cfg::CPR);
         const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
         const int64_t q = q0 + row;
-        const T* src = (which ? dog : qg) + q * D + col * (16 / Cfg::E);
-        stage[i] = q < p.n_q ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
+        const int64_t off = q * D + col * (16 / Cfg::E);
+        if (q >= p.n_q)
+          stage[i] = u32x4{0u, 0u, 0u, 0u};
+        else
+          stage[i] = which ? ld_chunk_as<T, TO>(dog + off) : ld16(qg + off);
       }
     }
     if (tid < 2 * Cfg::BQ) {
@@ -265,7 +269,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------------- dQ
-template <typename T, int D, int BK, int OCC, bool CAUSAL>
+template <typename T, typename TO, int D, int BK, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   constexpr int NT = 256;
   constexpr int BQ = 128;  // 4 waves x 32 queries
@@ -297,7 +301,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   const int64_t query = qw + c;
 
   const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + (size_t)bh * p.n_q * D;
   const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
   const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
 
@@ -308,7 +312,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   for (int kc = 0; kc < KC; ++kc) {
     if (valid) {
       qf[kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
-      gf[kc] = *reinterpret_cast<const Frag<T>*>(dog + query * D + 16 * kc + 8 * h);
+      gf[kc] = ld_frag_as<T, TO>(dog + query * D + 16 * kc + 8 * h);
     } else {
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
@@ -451,41 +455,47 @@ template <> struct BwdShape<_Float16, 128> { static constexpr int QS = 1, BK = 6
 template <> struct BwdShape<float, 64> { static constexpr int QS = 2, BK = 32, OCC = 1; };
 template <> struct BwdShape<float, 128> { static constexpr int QS = 1, BK = 32, OCC = 1; };
 
-template <typename T, int D, bool CAUSAL>
+template <typename T, typename TO, int D, bool CAUSAL>
 static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   using S = BwdShape<T, D>;
   using Dk = DkdvTile<T, D, S::QS>;
   void* args[] = {&p};
   const int64_t rows = (int64_t)p.bh * p.n_q;
-  constexpr int RPB = 256 / (D * (int)sizeof(T) / 16);
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<T, D>),
+  constexpr int RPB = 256 / (D * (int)sizeof(TO) / 16);
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, D>),
                                  dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
   if (e != hipSuccess) return e;
   p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
   p.n_qtiles = (int)((p.n_q + 127) / 128);
   if (p.dk) {
-    e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, D, S::QS, S::OCC, CAUSAL>),
+    e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, S::QS, S::OCC, CAUSAL>),
                         dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
     if (e != hipSuccess || !p.dq) return e;
   }
   const int dq_lds = 2 * 2 * S::BK * (D + 16 / (int)sizeof(T)) * (int)sizeof(T);
-  return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, D, S::BK, S::OCC, CAUSAL>),
+  return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, S::BK, S::OCC, CAUSAL>),
                          dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(256), args, dq_lds, stream);
 }
 
-template <typename T, int D>
+template <typename T, typename TO, int D>
 static hipError_t launch_bwd_dt(const BwdParams& p, bool causal, hipStream_t stream) {
-  return causal ? launch_bwd_impl<T, D, true>(p, stream) : launch_bwd_impl<T, D, false>(p, stream);
+  return causal ? launch_bwd_impl<T, TO, D, true>(p, stream) : launch_bwd_impl<T, TO, D, false>(p, stream);
 }
 
-hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, hipStream_t stream) {
+template <typename T, int D>
+static hipError_t launch_bwd_out(const BwdParams& p, bool causal, bool out_f32, hipStream_t stream) {
+  return out_f32 ? launch_bwd_dt<T, float, D>(p, causal, stream) : launch_bwd_dt<T, T, D>(p, causal, stream);
+}
+
+hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, bool out_f32,
+                      hipStream_t stream) {
   switch (dtype * 1000 + d) {
-    case 0 * 1000 + 64: return launch_bwd_dt<float, 64>(p, causal, stream);
-    case 0 * 1000 + 128: return launch_bwd_dt<float, 128>(p, causal, stream);
-    case 1 * 1000 + 64: return launch_bwd_dt<_Float16, 64>(p, causal, stream);
-    case 1 * 1000 + 128: return launch_bwd_dt<_Float16, 128>(p, causal, stream);
-    case 2 * 1000 + 64: return launch_bwd_dt<__bf16, 64>(p, causal, stream);
-    case 2 * 1000 + 128: return launch_bwd_dt<__bf16, 128>(p, causal, stream);
+    case 0 * 1000 + 64: return launch_bwd_dt<float, float, 64>(p, causal, stream);
+    case 0 * 1000 + 128: return launch_bwd_dt<float, float, 128>(p, causal, stream);
+    case 1 * 1000 + 64: return launch_bwd_out<_Float16, 64>(p, causal, out_f32, stream);
+    case 1 * 1000 + 128: return launch_bwd_out<_Float16, 128>(p, causal, out_f32, stream);
+    case 2 * 1000 + 64: return launch_bwd_out<__bf16, 64>(p, causal, out_f32, stream);
+    case 2 * 1000 + 128: return launch_bwd_out<__bf16, 128>(p, causal, out_f32, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -131,6 +131,40 @@ __device__ __forceinline__ Frag<T> to_frag(const float* x) {
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
+// 16/sizeof(T) consecutive elements read from an array of TO and returned in
+// T format (TO is T, or float for a 16-bit T: 32 bytes read and rounded).
+template <typename T, typename TO>
+__device__ __forceinline__ u32x4 ld_chunk_as(const TO* src) {
+  if constexpr (__is_same(T, TO)) {
+    return ld16(src);
+  } else {
+    static_assert(__is_same(TO, float) && sizeof(T) == 2, "float -> 16-bit only");
+    const f32x4 a = *reinterpret_cast<const f32x4*>(src);
+    const f32x4 b = *reinterpret_cast<const f32x4*>(src + 4);
+    Frag<T> f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[e] = (T)a[e];
+      f[4 + e] = (T)b[e];
+    }
+    return __builtin_bit_cast(u32x4, f);
+  }
+}
+
+// Eight consecutive elements of a TO array as a fragment of T.
+template <typename T, typename TO>
+__device__ __forceinline__ Frag<T> ld_frag_as(const TO* src) {
+  if constexpr (__is_same(T, TO)) {
+    return *reinterpret_cast<const Frag<T>*>(src);
+  } else {
+    const f32x8 x = *reinterpret_cast<const f32x8*>(src);
+    Frag<T> f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = (T)x[e];
+    return f;
+  }
+}
+
 // Workgroup id remap for the 8 XCDs of the chip: hardware hands workgroup w to
 // XCD w % 8, so give each XCD a contiguous range of logical tiles (neighbours
 // share K/V in that XCD's L2).  Bijective on [0, n).

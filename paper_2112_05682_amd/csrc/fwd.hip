@@ -43,7 +43,7 @@ struct FwdTile {
   static_assert(BK % 32 == 0 && D % 32 == 0, "tile shapes are multiples of 32");
 };
 
-template <typename T, int D, int QT, int BK, bool CAUSAL>
+template <typename T, typename TO, int D, int QT, int BK, bool CAUSAL>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   using Cfg = FwdTile<T, D, QT, BK>;
   constexpr int RS = Cfg::RS;
@@ -262,15 +262,15 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     if (row >= p.n_q) continue;
     if (p.n_splits == 1) {
       const float inv = 1.0f / l_tot;
-      T* og = static_cast<T*>(p.o) + ((size_t)bh * p.n_q + row) * D;
+      TO* og = static_cast<TO*>(p.o) + ((size_t)bh * p.n_q + row) * D;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int a4 = 0; a4 < 4; ++a4) {
-          typename FragT<T>::half v4;
+          typename FragT<TO>::half v4;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v4[e] = (T)(acc[t][dt][4 * a4 + e] * inv);
-          *reinterpret_cast<typename FragT<T>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
+          for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
+          *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
         }
       if (h == 0 && p.lse) p.lse[(size_t)bh * p.n_q + row] = m_run[t] * p.scale + logf(l_tot);
     } else {
@@ -296,7 +296,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 // Combine of the per-split summaries (Section 4): global max, rescale each
 // split's numerator and denominator by e^{m_s - m_g}, add, divide.  One thread
 // per (row, 4 features).
-template <typename T, int D>
+template <typename TO, int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
   constexpr int G = D / 4;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -317,46 +317,52 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
     o += wgt * ps;
   }
   const float inv = 1.0f / l;
-  typename FragT<T>::half out;
+  typename FragT<TO>::half out;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) out[e] = (T)(o[e] * inv);
-  *reinterpret_cast<typename FragT<T>::half*>(static_cast<T*>(p.o) + row * D + f0) = out;
+  for (int e = 0; e < 4; ++e) out[e] = (TO)(o[e] * inv);
+  *reinterpret_cast<typename FragT<TO>::half*>(static_cast<TO*>(p.o) + row * D + f0) = out;
   if (f0 == 0 && p.lse) p.lse[row] = m_g * p.scale + logf(l);
 }
 
 // ---------------------------------------------------------------- launchers
 
-template <typename T, int D, int QT, int BK, bool CAUSAL>
+template <typename T, typename TO, int D, int QT, int BK, bool CAUSAL>
 static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
   using Cfg = FwdTile<T, D, QT, BK>;
-  auto kern = attn_fwd_kernel<T, D, QT, BK, CAUSAL>;
+  auto kern = attn_fwd_kernel<T, TO, D, QT, BK, CAUSAL>;
   const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
   FwdParams pc = p;
   void* args[] = {&pc};
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid),
                                  dim3(Cfg::NT), args, Cfg::LDS_BYTES, stream);
   if (e != hipSuccess || p.n_splits == 1) return e;
-  auto comb = attn_combine_kernel<T, D>;
+  auto comb = attn_combine_kernel<TO, D>;
   const int64_t threads = (int64_t)p.bh * p.n_q * (D / 4);
   return hipLaunchKernel(reinterpret_cast<const void*>(comb), dim3((unsigned)((threads + 255) / 256)),
                          dim3(256), args, 0, stream);
 }
 
-template <typename T, int D>
+template <typename T, typename TO, int D>
 static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t stream) {
   constexpr int QT = FwdShape<T, D>::QT, BK = FwdShape<T, D>::BK;
-  return causal ? launch_fwd_impl<T, D, QT, BK, true>(p, stream)
-                : launch_fwd_impl<T, D, QT, BK, false>(p, stream);
+  return causal ? launch_fwd_impl<T, TO, D, QT, BK, true>(p, stream)
+                : launch_fwd_impl<T, TO, D, QT, BK, false>(p, stream);
 }
 
-hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, hipStream_t stream) {
+template <typename T, int D>
+static hipError_t launch_fwd_out(const FwdParams& p, bool causal, bool out_f32, hipStream_t stream) {
+  return out_f32 ? launch_fwd_dt<T, float, D>(p, causal, stream) : launch_fwd_dt<T, T, D>(p, causal, stream);
+}
+
+hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, bool out_f32,
+                      hipStream_t stream) {
   switch (dtype * 1000 + d) {
-    case 0 * 1000 + 64: return launch_fwd_dt<float, 64>(p, causal, stream);
-    case 0 * 1000 + 128: return launch_fwd_dt<float, 128>(p, causal, stream);
-    case 1 * 1000 + 64: return launch_fwd_dt<_Float16, 64>(p, causal, stream);
-    case 1 * 1000 + 128: return launch_fwd_dt<_Float16, 128>(p, causal, stream);
-    case 2 * 1000 + 64: return launch_fwd_dt<__bf16, 64>(p, causal, stream);
-    case 2 * 1000 + 128: return launch_fwd_dt<__bf16, 128>(p, causal, stream);
+    case 0 * 1000 + 64: return launch_fwd_dt<float, float, 64>(p, causal, stream);
+    case 0 * 1000 + 128: return launch_fwd_dt<float, float, 128>(p, causal, stream);
+    case 1 * 1000 + 64: return launch_fwd_out<_Float16, 64>(p, causal, out_f32, stream);
+    case 1 * 1000 + 128: return launch_fwd_out<_Float16, 128>(p, causal, out_f32, stream);
+    case 2 * 1000 + 64: return launch_fwd_out<__bf16, 64>(p, causal, out_f32, stream);
+    case 2 * 1000 + 128: return launch_fwd_out<__bf16, 128>(p, causal, out_f32, stream);
     default: return hipErrorInvalidValue;
   }
 }

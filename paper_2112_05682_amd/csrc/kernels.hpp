@@ -58,7 +58,10 @@ template <> struct FwdShape<float, 64> { static constexpr int QT = 1, BK = 32, B
 template <> struct FwdShape<float, 128> { static constexpr int QT = 1, BK = 32, BQ = 128; };
 
 // dtype codes follow mea_dtype: 0 = f32, 1 = f16, 2 = bf16.
-hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, hipStream_t stream);
-hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, hipStream_t stream);
+// out_f32: o (and, in the backward, do) are float32 instead of the input dtype.
+hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, bool out_f32,
+                      hipStream_t stream);
+hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, bool out_f32,
+                      hipStream_t stream);
 
 }  // namespace mea

@@ -40,11 +40,11 @@ def test_status_strings():
 
 def prob(**kw):
     base = dict(batch=1, heads=2, n_q=100, n_k=100, d=64, dtype=_lib.MEA_BF16, causal=0,
-                scale=0.125)
+                scale=0.125, out_f32=0)
     base.update(kw)
     # built directly (no normalisation) so that invalid fields reach the library
     return _lib.MeaProblem(base["batch"], base["heads"], base["n_q"], base["n_k"], base["d"],
-                           base["dtype"], base["causal"], base["scale"])
+                           base["dtype"], base["causal"], base["scale"], base["out_f32"])
 
 
 def ws_status(p):
@@ -77,6 +77,7 @@ def test_workspace_sizes():
     (dict(scale=float("nan")), _lib.MEA_ERR_INVALID_ARG),
     (dict(scale=float("inf")), _lib.MEA_ERR_INVALID_ARG),
     (dict(causal=2), _lib.MEA_ERR_INVALID_ARG),
+    (dict(out_f32=3), _lib.MEA_ERR_INVALID_ARG),
     (dict(n_q=1 << 31), _lib.MEA_ERR_INVALID_ARG),
     (dict(batch=1 << 40, heads=1 << 40), _lib.MEA_ERR_INVALID_ARG),
 ])
@@ -136,3 +137,28 @@ def test_workspace_too_small_is_rejected_before_launch():
     need_b = _lib.bwd_workspace_size(p)
     assert _lib.bwd(p, *([FAKE] * 9), None, 0, None) == _lib.MEA_ERR_WORKSPACE
     assert _lib.bwd(p, *([FAKE] * 9), FAKE, need_b - 1, None) == _lib.MEA_ERR_WORKSPACE
+
+
+def test_problem_struct_layout_matches_the_header(tmp_path):
+    # Compile a probe against include/mea.h with the host C compiler and compare
+    # the struct layout with the ctypes mirror used by the binding.
+    import shutil
+    import subprocess
+    if not shutil.which("gcc") or not os.path.isdir("/opt/rocm/include"):
+        pytest.skip("needs gcc and the ROCm headers")
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "mea.h"\n'
+        'int main(void) { printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(mea_problem), '
+        'offsetof(mea_problem, batch), offsetof(mea_problem, heads), offsetof(mea_problem, n_q), '
+        'offsetof(mea_problem, n_k), offsetof(mea_problem, d), offsetof(mea_problem, dtype), '
+        'offsetof(mea_problem, causal), offsetof(mea_problem, scale), '
+        'offsetof(mea_problem, out_f32)); return 0; }\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROOT, "include"),
+                    "-I/opt/rocm/include", str(src), "-o", str(exe)], check=True)
+    got = [int(t) for t in subprocess.run([str(exe)], check=True, capture_output=True,
+                                          text=True).stdout.split()]
+    M = _lib.MeaProblem
+    want = [ctypes.sizeof(M)] + [getattr(M, f).offset for f, _ in M._fields_]
+    assert got == want

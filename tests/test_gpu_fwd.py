@@ -16,13 +16,15 @@ from parity_util import TOL, f64, rel_err, to_gpu
 pytestmark = pytest.mark.gpu
 
 
-def run_and_compare(B, H, nq, nk, d, dtype, causal, std=1.0, qk_mult=1.0, seeds=(0, 1, 2, 3)):
-    print("case B=%d H=%d nq=%d nk=%d d=%d %s causal=%s mult=%s" % (B, H, nq, nk, d, dtype,
-                                                                     causal, qk_mult), flush=True)
+def run_and_compare(B, H, nq, nk, d, dtype, causal, std=1.0, qk_mult=1.0, seeds=(0, 1, 2, 3),
+                    out_dtype=None):
+    print("case B=%d H=%d nq=%d nk=%d d=%d %s causal=%s mult=%s out=%s" % (
+        B, H, nq, nk, d, dtype, causal, qk_mult, out_dtype), flush=True)
     x = attention_inputs(B, H, nq, nk, d, dtype, std, qk_mult, seeds, with_grad=False)
     g = to_gpu(x)
-    o, lse = attention_fwd(g["q"], g["k"], g["v"], causal=causal)
+    o, lse = attention_fwd(g["q"], g["k"], g["v"], causal=causal, out_dtype=out_dtype)
     torch.cuda.synchronize()
+    assert o.dtype == (out_dtype or g["q"].dtype)
     ro, rl = oracle.fwd(f64(x["q"]), f64(x["k"]), f64(x["v"]), scale=d ** -0.5, causal=causal)
     eo, el = rel_err(f64(o), ro), rel_err(f64(lse), rl)
     assert np.all(np.isfinite(f64(o))) and np.all(np.isfinite(f64(lse)))
@@ -43,6 +45,16 @@ def test_forward_small(dtype, d, causal, shape):
     run_and_compare(*shape, d, dtype, causal)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("shape", [(1, 2, 7, 100), (2, 1, 300, 257), (1, 1, 64, 3000)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_forward_float32_output(dtype, d, causal, shape):
+    # 16-bit inputs, float32 output: the setting of the paper's experiments.
+    run_and_compare(*shape, d, dtype, causal, out_dtype=torch.float32)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 @pytest.mark.parametrize("causal", [False, True])
 def test_forward_key_splits(dtype, causal):
@@ -56,6 +68,10 @@ def test_forward_key_splits(dtype, causal):
 def test_forward_key_splits_causal_rows_without_keys_in_a_split():
     # Causal with splits: early query rows see no key of the later splits.
     run_and_compare(1, 1, 600, 5000, 64, "bf16", True)
+
+
+def test_forward_key_splits_float32_output():
+    run_and_compare(1, 1, 256, 40000, 128, "bf16", False, out_dtype=torch.float32)
 
 
 @pytest.mark.parametrize("d", [64, 128])
