@@ -18,6 +18,8 @@
 
 namespace mea {
 
+template <bool B> struct BoolC { static constexpr bool value = B; };
+
 // ------------------------------------------------------------------- pre
 template <typename TO, int D>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
@@ -54,7 +56,7 @@ struct DkdvTile {
   static constexpr int CHUNKS = 2 * BQ * CPR;   // Q and dO chunks per stage
   static constexpr int CPT = (CHUNKS + NT - 1) / NT;
   static constexpr int STAGE_ELEMS = 2 * TILE;
-  static constexpr int STAGE_BYTES = STAGE_ELEMS * E + 2 * BQ * 4;  // + lse2, delta
+  static constexpr int STAGE_BYTES = STAGE_ELEMS * E + 2 * BQ * 4;  // + accumulator initial values
   static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
 };
 
@@ -136,10 +138,13 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
     }
     if (tid < 2 * Cfg::BQ) {
       const int64_t q = q0 + (tid % Cfg::BQ);
-      if (tid < Cfg::BQ)  // lse * log2(e); +inf past n_q makes those weights 0
-        stage_f = q < p.n_q ? lseg[q] * 1.4426950408889634f : INFINITY;
+      // Initial values of the score and dP accumulators: S - lse/scale makes
+      // P = 2^(c*acc) (c = scale*log2 e), dP - D makes dS = P*acc.  Rows past
+      // n_q start at -inf, so their weights are 0.
+      if (tid < Cfg::BQ)
+        stage_f = q < p.n_q ? -lseg[q] / p.scale : -INFINITY;
       else
-        stage_f = q < p.n_q ? deltag[q] : 0.0f;
+        stage_f = q < p.n_q ? -deltag[q] : 0.0f;
     }
   };
   auto store_stage = [&](int buf) {
@@ -176,21 +181,31 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 
     const T* qs_t = reinterpret_cast<const T*>(stage_base(it & 1));
     const T* dos_t = qs_t + Cfg::TILE;
-    const float* lse2_s = reinterpret_cast<const float*>(stage_base(it & 1) + Cfg::STAGE_ELEMS * Cfg::E);
-    const float* delta_s = lse2_s + Cfg::BQ;
+    const float* sinit_s = reinterpret_cast<const float*>(stage_base(it & 1) + Cfg::STAGE_ELEMS * Cfg::E);
+    const float* dpinit_s = sinit_s + Cfg::BQ;
 
     // Nothing to do when every query of the tile precedes this wave's keys.
     const bool active = !CAUSAL || q0 + Cfg::BQ - 1 >= kw;
     if (active) {
+      // Accumulators start at -lse/scale and -D of their query rows (register r
+      // of lane half h holds query 32 qs + permuted_row(r, h)).
       f32x16 s[QS], dp[QS];
 #pragma unroll
-      for (int qs = 0; qs < QS; ++qs)
+      for (int qs = 0; qs < QS; ++qs) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          s[qs][r] = 0.0f;
-          dp[qs][r] = 0.0f;
+        for (int j = 0; j < 4; ++j) {
+          const int row = 32 * qs + 16 * (j >> 1) + 8 * h + 4 * (j & 1);
+          const f32x4 a = *reinterpret_cast<const f32x4*>(sinit_s + row);
+          const f32x4 b = *reinterpret_cast<const f32x4*>(dpinit_s + row);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s[qs][4 * j + e] = a[e];
+            dp[qs][4 * j + e] = b[e];
+          }
         }
-      // S = Q K^T and dP = dO V^T (rows: queries in perm32 order; lane: key).
+      }
+      // S = Q K^T - lse/scale and dP = dO V^T - D (rows: queries in perm32
+      // order; lane: key).
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc) {
 #pragma unroll
@@ -204,22 +219,13 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       const bool need_mask = CAUSAL && q0 < kw + 31;
 #pragma unroll
       for (int qs = 0; qs < QS; ++qs) {
-        float l2[16], dl[16];
-        *reinterpret_cast<f32x4*>(&l2[0]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 8 * h);
-        *reinterpret_cast<f32x4*>(&l2[4]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 8 * h + 4);
-        *reinterpret_cast<f32x4*>(&l2[8]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 16 + 8 * h);
-        *reinterpret_cast<f32x4*>(&l2[12]) = *reinterpret_cast<const f32x4*>(lse2_s + 32 * qs + 16 + 8 * h + 4);
-        *reinterpret_cast<f32x4*>(&dl[0]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 8 * h);
-        *reinterpret_cast<f32x4*>(&dl[4]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 8 * h + 4);
-        *reinterpret_cast<f32x4*>(&dl[8]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 16 + 8 * h);
-        *reinterpret_cast<f32x4*>(&dl[12]) = *reinterpret_cast<const f32x4*>(delta_s + 32 * qs + 16 + 8 * h + 4);
         const int key_rel = (int)(key - q0);  // key minus the tile's first query
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float pr = fast_exp2(fmaf(s[qs][r], cl2, -l2[r]));
+          float pr = fast_exp2(s[qs][r] * cl2);
           if (need_mask && key_rel > 32 * qs + permuted_row(r, h)) pr = 0.0f;
-          s[qs][r] = pr;                          // P
-          dp[qs][r] = pr * (dp[qs][r] - dl[r]);   // dS
+          s[qs][r] = pr;                // P
+          dp[qs][r] = pr * dp[qs][r];   // dS = P (dP - D)
         }
       }
       // dV += P^T dO and dK += dS^T Q (A: lane = key row, k = queries).
@@ -321,8 +327,10 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
       }
     }
   }
-  const float lse2 = valid ? p.lse[(size_t)bh * p.n_q + query] * 1.4426950408889634f : INFINITY;
-  const float delta = valid ? p.delta[(size_t)bh * p.n_q + query] : 0.0f;
+  // Initial values of the S^T and dP^T accumulators of this lane's query:
+  // -lse/scale (P = 2^(c*acc)) and -D (dS = P*acc); -inf for a padding row.
+  const float s_init = valid ? -p.lse[(size_t)bh * p.n_q + query] / p.scale : -INFINITY;
+  const float dp_init = valid ? -p.delta[(size_t)bh * p.n_q + query] : 0.0f;
 
   f32x16 acc[NDT];
 #pragma unroll
@@ -368,68 +376,85 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   }
   __syncthreads();
 
-  for (int it = 0; it < n_tiles; ++it) {
+  // Leading tiles that need no mask (all keys exist and, causal, precede the
+  // workgroup's first query); masked tiles run in a second loop.
+  int n_plain = (int)(p.n_k / BK);
+  if (n_plain > n_tiles) n_plain = n_tiles;
+  if (CAUSAL) {
+    const int below = (int)((q0 + 1) / BK);
+    if (below < n_plain) n_plain = below;
+  }
+
+  auto tile = [&](auto mask_tag, int it) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int64_t k0 = (int64_t)it * BK;
-    const bool has_next = it + 1 < n_tiles;
-    if (has_next) load_stage(k0 + BK);
     const T* ks = smem + (it & 1) * 2 * TILE;
     const T* vs = ks + TILE;
-    const bool active = !CAUSAL || k0 <= qw + 31;
-    if (active) {
-      f32x16 s[NKT], dp[NKT];
+    if (MASK && CAUSAL && k0 > qw + 31) return;  // all keys after this wave's queries
+    f32x16 s[NKT], dp[NKT];
 #pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          s[kt][r] = 0.0f;
-          dp[kt][r] = 0.0f;
-        }
-      // S^T = K Q^T and dP^T = V dO^T (rows: keys in perm32 order; lane: query).
+      for (int r = 0; r < 16; ++r) {
+        s[kt][r] = s_init;
+        dp[kt][r] = dp_init;
+      }
+    // S^T = K Q^T - lse/scale and dP^T = V dO^T - D (rows: keys in perm32
+    // order; lane: query).
 #pragma unroll
-      for (int kc = 0; kc < KC; ++kc)
+    for (int kc = 0; kc < KC; ++kc)
 #pragma unroll
-        for (int kt = 0; kt < NKT; ++kt) {
-          const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
-          s[kt] = mma(a, qf[kc], s[kt]);
-          const Frag<T> b = lds_frag<T>(vs + (32 * kt + krow) * RS + 16 * kc + 8 * h);
-          dp[kt] = mma(b, gf[kc], dp[kt]);
-        }
-      const bool need_mask = (k0 + BK > p.n_k) || (CAUSAL && k0 + BK - 1 > qw);
-      // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
-      // under the causal mask, visible iff x <= q_rel.
+      for (int kt = 0; kt < NKT; ++kt) {
+        const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+        s[kt] = mma(a, qf[kc], s[kt]);
+        const Frag<T> b = lds_frag<T>(vs + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+        dp[kt] = mma(b, gf[kc], dp[kt]);
+      }
+    // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
+    // under the causal mask, visible iff x <= query - k0.
+    int lim = BK;
+    if constexpr (MASK) {
       const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
       const int q_rel = CAUSAL ? (int)(query - k0) : BK;
-      const int lim = q_rel + 1 < key_lim ? q_rel + 1 : key_lim;
+      lim = q_rel + 1 < key_lim ? q_rel + 1 : key_lim;
+    }
 #pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float pr = fast_exp2(fmaf(s[kt][r], cl2, -lse2));
-          if (need_mask && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
-          dp[kt][r] = pr * (dp[kt][r] - delta);  // dS^T
+      for (int r = 0; r < 16; ++r) {
+        float pr = fast_exp2(s[kt][r] * cl2);
+        if (MASK && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
+        dp[kt][r] = pr * dp[kt][r];  // dS^T
+      }
+    // dQ^T += K^T dS^T.
+#pragma unroll
+    for (int pc = 0; pc < NPC; ++pc) {
+      float td[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) td[e] = dp[pc >> 1][8 * (pc & 1) + e];
+      const Frag<T> b = to_frag<T>(td);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        Frag<T> a;
+        if constexpr (sizeof(T) == 2) {
+          a = lds_col_frag<T>(ks, RS, 16 * pc, 32 * dt, lane);
+        } else {
+          a = lds_col_frag_f32(reinterpret_cast<const float*>(ks), RS, 16 * pc, 32 * dt, lane);
         }
-      // dQ^T += K^T dS^T.
-#pragma unroll
-      for (int pc = 0; pc < NPC; ++pc) {
-        float td[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) td[e] = dp[pc >> 1][8 * (pc & 1) + e];
-        const Frag<T> b = to_frag<T>(td);
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          Frag<T> a;
-          if constexpr (sizeof(T) == 2) {
-            a = lds_col_frag<T>(ks, RS, 16 * pc, 32 * dt, lane);
-          } else {
-            a = lds_col_frag_f32(reinterpret_cast<const float*>(ks), RS, 16 * pc, 32 * dt, lane);
-          }
-          acc[dt] = mma(a, b, acc[dt]);
-        }
+        acc[dt] = mma(a, b, acc[dt]);
       }
     }
+  };
+  auto step = [&](auto mask_tag, int it) {
+    const bool has_next = it + 1 < n_tiles;
+    if (has_next) load_stage((int64_t)(it + 1) * BK);
+    tile(mask_tag, it);
     if (has_next) store_stage((it + 1) & 1);
     __syncthreads();
-  }
+  };
+  int it = 0;
+  for (; it < n_plain; ++it) step(BoolC<false>{}, it);
+  for (; it < n_tiles; ++it) step(BoolC<true>{}, it);
 
   if (valid) {
     T* dqg = static_cast<T*>(p.dq) + ((size_t)bh * p.n_q + query) * D;

@@ -127,6 +127,36 @@ __device__ __forceinline__ Frag<T> to_frag(const float* x) {
   return r;
 }
 
+// acc + the sum of the eight weights of a P fragment.  For 16-bit types the
+// already-rounded fragment is summed with packed dot products against 1, so
+// the denominator adds exactly the weights the PV MFMA multiplies; float32
+// fragments are summed directly.
+__device__ __forceinline__ float frag_sum(const bf16x8& f, const float*, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 pr = {f[2 * i], f[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
+  }
+  return acc;
+}
+__device__ __forceinline__ float frag_sum(const f16x8& f, const float*, float acc) {
+  typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+  const f16x2 one = {(_Float16)1.0f, (_Float16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f16x2 pr = {f[2 * i], f[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2(pr, one, acc, false);
+  }
+  return acc;
+}
+__device__ __forceinline__ float frag_sum(const f32x8&, const float* x, float acc) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc += x[i];
+  return acc;
+}
+
 // 16-byte global load / store helpers.
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }

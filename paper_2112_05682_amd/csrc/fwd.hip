@@ -27,6 +27,13 @@
 
 namespace mea {
 
+// A tile raises the reference maximum only when one of its scores exceeds it
+// by more than this many powers of two (weights then stay <= 2^8).
+constexpr float kRescaleSlack = 8.0f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <bool B> struct BoolC { static constexpr bool value = B; };
+
 template <typename T, int D, int QT, int BK>
 struct FwdTile {
   static constexpr int NW = 4;
@@ -102,10 +109,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[t][dt][r] = 0.0f;
-  float m_run[QT], l_run[QT];
+  // Reference maximum (in units of scale * log2 e) and denominator per
+  // query; each lane half accumulates the denominator of its own keys.
+  float m_ref[QT], l_run[QT];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    m_run[t] = -INFINITY;
+    m_ref[t] = -INFINITY;
     l_run[t] = 0.0f;
   }
 
@@ -138,102 +147,98 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int krow = perm32(c);  // key row this lane feeds into the A operand
   const float cl2 = p.scale_log2;
 
-  if (n_tiles > 0) {
-    load_stage(kb);
-    store_stage(0);
+  // Number of leading tiles that need no mask: every key exists (no ragged
+  // tail) and, under the causal mask, precedes the workgroup's first query.
+  int n_plain = n_tiles;
+  {
+    const int64_t full = (p.n_k - kb) / BK;
+    if (full < n_plain) n_plain = (int)full;
+    if (CAUSAL) {
+      const int64_t below = q0 - kb + 1 > 0 ? (q0 - kb + 1) / BK : 0;
+      if (below < n_plain) n_plain = (int)below;
+    }
   }
-  __syncthreads();
 
-  for (int it = 0; it < n_tiles; ++it) {
+  // One K/V tile (LDS stage it & 1): S^T = K Q^T, (mask), online softmax with a
+  // lazily raised reference maximum, O^T += V^T P^T.
+  auto tile = [&](auto mask_tag, int it) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int64_t k0 = kb + (int64_t)it * BK;
-    const bool has_next = it + 1 < n_tiles;
-    if (has_next) load_stage(k0 + BK);
-
     const T* ks = smem + (it & 1) * 2 * Cfg::TILE;
     const T* vs = ks + Cfg::TILE;
     // A wave whose queries all precede the tile's first key has nothing to do.
-    const bool active = !CAUSAL || k0 <= qw + QT * 32 - 1;
-    if (active) {
-      // ---- S^T = K Q^T for BK keys x (32*QT) queries.
-      f32x16 s[NKT][QT];
+    if (MASK && CAUSAL && k0 > qw + QT * 32 - 1) return;
+
+    f32x16 s[NKT][QT];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kt][t][r] = 0.0f;
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
+      }
+    }
+
+    if constexpr (MASK) {
+      // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
+      // under the causal mask, visible to query qw + 32t + c iff x <= q_rel + 32t.
+      const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+      const int q_rel = CAUSAL ? (int)(qw - k0) + c : BK;
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const int lim_c = q_rel + 32 * t + 1;
+        const int lim = CAUSAL && lim_c < key_lim ? lim_c : key_lim;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (32 * kt + permuted_row(r, h) >= lim) s[kt][t][r] = -INFINITY;
+      }
+    }
+
+    // Online softmax, one query per lane.  The reference maximum m_ref (kept
+    // pre-multiplied by scale*log2 e) is raised only when a score exceeds it by
+    // more than kRescaleSlack powers of two: weights stay <= 2^kRescaleSlack,
+    // numerator and denominator share the reference, so the result is the same
+    // and the accumulator rescale is skipped on most tiles.
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-        for (int t = 0; t < QT; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s[kt][t][r] = 0.0f;
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-#pragma unroll
-        for (int kt = 0; kt < NKT; ++kt) {
-          const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
-#pragma unroll
-          for (int t = 0; t < QT; ++t) s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
-        }
-      }
-
-      // ---- mask: ragged key tail and the causal diagonal only.
-      const bool need_mask = (k0 + BK > p.n_k) || (CAUSAL && k0 + BK - 1 > qw);
-      if (need_mask) {
-        // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
-        // under the causal mask, visible to query qw + 32t + c iff x <= q_rel + 32t.
-        const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
-        const int q_rel = CAUSAL ? (int)(qw - k0) + c : BK;
-#pragma unroll
-        for (int t = 0; t < QT; ++t) {
-          const int lim_c = q_rel + 32 * t + 1;
-          const int lim = CAUSAL && lim_c < key_lim ? lim_c : key_lim;
-#pragma unroll
-          for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-              if (32 * kt + permuted_row(r, h) >= lim) s[kt][t][r] = -INFINITY;
-        }
-      }
-
-      // ---- online softmax per query (per lane), P overwrites S.
-#pragma unroll
-      for (int t = 0; t < QT; ++t) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][t][r]);
-        mx = xhalf_max(mx);
-        const float m_new = fmaxf(m_run[t], mx);
-        // A query that has seen no visible key yet keeps m = -inf; use 0 as
-        // the reference so that every exponent is -inf (weight 0), not NaN.
-        const float m_ref = m_new == -INFINITY ? 0.0f : m_new;
-        const float alpha = fast_exp2((m_run[t] - m_ref) * cl2);
-        const float neg = -m_ref * cl2;
-        float rs = 0.0f;
-#pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float e = fast_exp2(fmaf(s[kt][t][r], cl2, neg));
-            s[kt][t][r] = e;
-            rs += e;
-          }
-        l_run[t] = l_run[t] * alpha + rs;
-        m_run[t] = m_new;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][t][r]);
+      const float mx_c = xhalf_max(mx) * cl2;
+      const bool raise = mx_c > m_ref[t] + kRescaleSlack;
+      if (__builtin_amdgcn_ballot_w64(raise)) {
+        const float m_new = raise ? mx_c : m_ref[t];
+        const float alpha = fast_exp2(m_ref[t] - m_new);  // 0 on the first raise
+        l_run[t] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
           for (int r = 0; r < 16; ++r) acc[t][dt][r] *= alpha;
+        m_ref[t] = m_new;
       }
-
-      // ---- O^T += V^T P^T.
-      Frag<T> pf[QT][NPC];
+      // A row with no visible key so far keeps m_ref = -inf; offset 0 keeps
+      // its (all -inf) exponents at weight 0 instead of NaN.
+      const float neg = (MASK && m_ref[t] == -INFINITY) ? 0.0f : -m_ref[t];
+      Frag<T> pf[NPC];
 #pragma unroll
-      for (int t = 0; t < QT; ++t)
+      for (int pc = 0; pc < NPC; ++pc) {
+        float e8[8];
 #pragma unroll
-        for (int pc = 0; pc < NPC; ++pc) {
-          float tmp[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) tmp[e] = s[pc >> 1][t][8 * (pc & 1) + e];
-          pf[t][pc] = to_frag<T>(tmp);
-        }
+        for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg));
+        pf[pc] = to_frag<T>(e8);
+        l_run[t] = frag_sum(pf[pc], e8, l_run[t]);
+      }
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
 #pragma unroll
@@ -244,15 +249,30 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
           } else {
             a = lds_col_frag_f32(reinterpret_cast<const float*>(vs), RS, 16 * pc, 32 * dt, lane);
           }
-#pragma unroll
-          for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, pf[t][pc], acc[t][dt]);
+          acc[t][dt] = mma(a, pf[pc], acc[t][dt]);
         }
       }
     }
+  };
 
+  // Double-buffered pipeline: the next tile is fetched into registers while
+  // the current one is computed, then written to the other LDS stage.  Masked
+  // tiles (ragged tail, causal diagonal) run in a separate second loop.
+  auto step = [&](auto mask_tag, int it) {
+    const bool has_next = it + 1 < n_tiles;
+    if (has_next) load_stage(kb + (int64_t)(it + 1) * BK);
+    tile(mask_tag, it);
     if (has_next) store_stage((it + 1) & 1);
     __syncthreads();
+  };
+  if (n_tiles > 0) {
+    load_stage(kb);
+    store_stage(0);
   }
+  __syncthreads();
+  int it = 0;
+  for (; it < n_plain; ++it) step(BoolC<false>{}, it);
+  for (; it < n_tiles; ++it) step(BoolC<true>{}, it);
 
   // ---- epilogue.
 #pragma unroll
@@ -272,7 +292,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
           for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
           *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
         }
-      if (h == 0 && p.lse) p.lse[(size_t)bh * p.n_q + row] = m_run[t] * p.scale + logf(l_tot);
+      if (h == 0 && p.lse)
+        p.lse[(size_t)bh * p.n_q + row] = (m_ref[t] + __log2f(l_tot)) * kLn2;
     } else {
       const size_t prow = ((size_t)split * p.bh + bh) * p.n_q + row;
       float* po = p.part_o + prow * D;
@@ -286,7 +307,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
           *reinterpret_cast<f32x4*>(po + 32 * dt + 8 * a4 + 4 * h) = v4;
         }
       if (h == 0) {
-        p.part_m[prow] = m_run[t];
+        p.part_m[prow] = m_ref[t];  // log2 units (scaled), -inf if no visible key
         p.part_l[prow] = l_tot;
       }
     }
@@ -311,7 +332,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
   f32x4 o = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int s = 0; s < p.n_splits; ++s) {
     const float ms = p.part_m[s * stride + row];
-    const float wgt = ms == -INFINITY ? 0.0f : fast_exp2((ms - m_g) * p.scale_log2);
+    const float wgt = ms == -INFINITY ? 0.0f : fast_exp2(ms - m_g);
     l += wgt * p.part_l[s * stride + row];
     const f32x4 ps = *reinterpret_cast<const f32x4*>(p.part_o + (s * stride + row) * D + f0);
     o += wgt * ps;
@@ -321,7 +342,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) out[e] = (TO)(o[e] * inv);
   *reinterpret_cast<typename FragT<TO>::half*>(static_cast<TO*>(p.o) + row * D + f0) = out;
-  if (f0 == 0 && p.lse) p.lse[row] = m_g * p.scale + logf(l);
+  if (f0 == 0 && p.lse) p.lse[row] = (m_g + __log2f(l)) * kLn2;
 }
 
 // ---------------------------------------------------------------- launchers
