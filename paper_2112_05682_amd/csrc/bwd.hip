@@ -104,6 +104,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
     }
   }
 
+  wait_global_loads();
+
   f32x16 dk[NDT], dv[NDT];
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
@@ -119,6 +121,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 
   u32x4 stage[Cfg::CPT];
   float stage_f = 0.0f;
+  const float inv_scale = 1.0f / p.scale;
   auto stage_base = [&](int buf) { return smem_raw + buf * Cfg::STAGE_BYTES; };
   auto load_stage = [&](int64_t q0) {
 #pragma unroll
@@ -137,14 +140,13 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       }
     }
     if (tid < 2 * Cfg::BQ) {
+      // Raw lse (or D) of the row; transformed only when written to LDS, so
+      // that nothing waits on this load before the tile's compute.
       const int64_t q = q0 + (tid % Cfg::BQ);
-      // Initial values of the score and dP accumulators: S - lse/scale makes
-      // P = 2^(c*acc) (c = scale*log2 e), dP - D makes dS = P*acc.  Rows past
-      // n_q start at -inf, so their weights are 0.
       if (tid < Cfg::BQ)
-        stage_f = q < p.n_q ? -lseg[q] / p.scale : -INFINITY;
+        stage_f = q < p.n_q ? lseg[q] : INFINITY;
       else
-        stage_f = q < p.n_q ? -deltag[q] : 0.0f;
+        stage_f = q < p.n_q ? deltag[q] : 0.0f;
     }
   };
   auto store_stage = [&](int buf) {
@@ -160,8 +162,11 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       }
     }
     if (tid < 2 * Cfg::BQ) {
+      // Initial values of the score and dP accumulators: S - lse/scale makes
+      // P = 2^(c*acc) (c = scale*log2 e), dP - D makes dS = P*acc.  Rows past
+      // n_q start at -inf, so their weights are 0.
       float* f = reinterpret_cast<float*>(stage_base(buf) + Cfg::STAGE_ELEMS * Cfg::E);
-      f[tid] = stage_f;
+      f[tid] = tid < Cfg::BQ ? -stage_f * inv_scale : -stage_f;
     }
   };
 
@@ -275,10 +280,10 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------------- dQ
-template <typename T, typename TO, int D, int BK, int OCC, bool CAUSAL>
+template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   constexpr int NT = 256;
-  constexpr int BQ = 128;  // 4 waves x 32 queries
+  constexpr int BQ = 128 * QT;  // 4 waves x QT x 32 queries
   constexpr int E = sizeof(T);
   constexpr int RS = D + 16 / E;
   constexpr int TILE = BK * RS;
@@ -303,40 +308,47 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   const int bh = w / p.n_qtiles;
   const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;
   const int64_t q0 = (int64_t)qtile * BQ;
-  const int64_t qw = q0 + 32 * wave;
-  const int64_t query = qw + c;
+  const int64_t qw = q0 + 32 * QT * wave;  // first query of this wave
 
   const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
   const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + (size_t)bh * p.n_q * D;
   const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
   const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
 
-  // Q^T and dO^T as B operands: lane (h, query c), k = 16kc + 8h + s.
-  Frag<T> qf[KC], gf[KC];
-  const bool valid = query < p.n_q;
+  // Q^T and dO^T as B operands: lane (h, query c of sub-tile t), k = 16kc + 8h + s.
+  // Initial values of the S^T and dP^T accumulators of each query: -lse/scale
+  // (P = 2^(c*acc)) and -D (dS = P*acc); -inf for a padding row.
+  Frag<T> qf[QT][KC], gf[QT][KC];
+  float s_init[QT], dp_init[QT];
 #pragma unroll
-  for (int kc = 0; kc < KC; ++kc) {
-    if (valid) {
-      qf[kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
-      gf[kc] = ld_frag_as<T, TO>(dog + query * D + 16 * kc + 8 * h);
-    } else {
+  for (int t = 0; t < QT; ++t) {
+    const int64_t query = qw + 32 * t + c;
+    const bool valid = query < p.n_q;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        qf[kc][s] = (T)0.0f;
-        gf[kc][s] = (T)0.0f;
+    for (int kc = 0; kc < KC; ++kc) {
+      if (valid) {
+        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
+        gf[t][kc] = ld_frag_as<T, TO>(dog + query * D + 16 * kc + 8 * h);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          qf[t][kc][e] = (T)0.0f;
+          gf[t][kc][e] = (T)0.0f;
+        }
       }
     }
+    s_init[t] = valid ? -p.lse[(size_t)bh * p.n_q + query] / p.scale : -INFINITY;
+    dp_init[t] = valid ? -p.delta[(size_t)bh * p.n_q + query] : 0.0f;
   }
-  // Initial values of the S^T and dP^T accumulators of this lane's query:
-  // -lse/scale (P = 2^(c*acc)) and -D (dS = P*acc); -inf for a padding row.
-  const float s_init = valid ? -p.lse[(size_t)bh * p.n_q + query] / p.scale : -INFINITY;
-  const float dp_init = valid ? -p.delta[(size_t)bh * p.n_q + query] : 0.0f;
+  wait_global_loads();
 
-  f32x16 acc[NDT];
+  f32x16 acc[QT][NDT];
 #pragma unroll
-  for (int dt = 0; dt < NDT; ++dt)
+  for (int t = 0; t < QT; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[dt][r] = 0.0f;
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[t][dt][r] = 0.0f;
 
   int64_t ke = p.n_k;
   if (CAUSAL && ke > q0 + BQ) ke = q0 + BQ;
@@ -390,15 +402,17 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
     const int64_t k0 = (int64_t)it * BK;
     const T* ks = smem + (it & 1) * 2 * TILE;
     const T* vs = ks + TILE;
-    if (MASK && CAUSAL && k0 > qw + 31) return;  // all keys after this wave's queries
-    f32x16 s[NKT], dp[NKT];
+    if (MASK && CAUSAL && k0 > qw + 32 * QT - 1) return;  // all keys after this wave's queries
+    f32x16 s[NKT][QT], dp[NKT][QT];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[kt][r] = s_init;
-        dp[kt][r] = dp_init;
-      }
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[kt][t][r] = s_init[t];
+          dp[kt][t][r] = dp_init[t];
+        }
     // S^T = K Q^T - lse/scale and dP^T = V dO^T - D (rows: keys in perm32
     // order; lane: query).
 #pragma unroll
@@ -406,33 +420,44 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) {
         const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
-        s[kt] = mma(a, qf[kc], s[kt]);
         const Frag<T> b = lds_frag<T>(vs + (32 * kt + krow) * RS + 16 * kc + 8 * h);
-        dp[kt] = mma(b, gf[kc], dp[kt]);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) {
+          s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
+          dp[kt][t] = mma(b, gf[t][kc], dp[kt][t]);
+        }
       }
     // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
-    // under the causal mask, visible iff x <= query - k0.
-    int lim = BK;
+    // under the causal mask, visible to query qw + 32t + c iff x <= q_rel + 32t.
+    int key_lim = BK, q_rel = BK;
     if constexpr (MASK) {
-      const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
-      const int q_rel = CAUSAL ? (int)(query - k0) : BK;
-      lim = q_rel + 1 < key_lim ? q_rel + 1 : key_lim;
+      key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+      if (CAUSAL) q_rel = (int)(qw - k0) + c;
     }
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt)
+    for (int t = 0; t < QT; ++t) {
+      int lim = key_lim;
+      if (MASK && CAUSAL && q_rel + 32 * t + 1 < lim) lim = q_rel + 32 * t + 1;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float pr = fast_exp2(s[kt][r] * cl2);
-        if (MASK && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
-        dp[kt][r] = pr * dp[kt][r];  // dS^T
-      }
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pr = fast_exp2(s[kt][t][r] * cl2);
+          if (MASK && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
+          dp[kt][t][r] = pr * dp[kt][t][r];  // dS^T
+        }
+    }
     // dQ^T += K^T dS^T.
 #pragma unroll
     for (int pc = 0; pc < NPC; ++pc) {
-      float td[8];
+      Frag<T> b[QT];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) td[e] = dp[pc >> 1][8 * (pc & 1) + e];
-      const Frag<T> b = to_frag<T>(td);
+      for (int t = 0; t < QT; ++t) {
+        float td[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) td[e] = dp[pc >> 1][t][8 * (pc & 1) + e];
+        b[t] = to_frag<T>(td);
+      }
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         Frag<T> a;
@@ -441,7 +466,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
         } else {
           a = lds_col_frag_f32(reinterpret_cast<const float*>(ks), RS, 16 * pc, 32 * dt, lane);
         }
-        acc[dt] = mma(a, b, acc[dt]);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, b[t], acc[t][dt]);
       }
     }
   };
@@ -456,7 +482,10 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   for (; it < n_plain; ++it) step(BoolC<false>{}, it);
   for (; it < n_tiles; ++it) step(BoolC<true>{}, it);
 
-  if (valid) {
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int64_t query = qw + 32 * t + c;
+    if (query >= p.n_q) continue;
     T* dqg = static_cast<T*>(p.dq) + ((size_t)bh * p.n_q + query) * D;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -464,7 +493,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
       for (int a4 = 0; a4 < 4; ++a4) {
         typename FragT<T>::half v4;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v4[e] = (T)(acc[dt][4 * a4 + e] * p.scale);
+        for (int e = 0; e < 4; ++e) v4[e] = (T)(acc[t][dt][4 * a4 + e] * p.scale);
         *reinterpret_cast<typename FragT<T>::half*>(dqg + 32 * dt + 8 * a4 + 4 * h) = v4;
       }
   }
@@ -472,13 +501,41 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 
 // ---------------------------------------------------------------- launchers
 
+// Tile choices.  dK/dV: QS query sub-tiles of 32 per stage; dQ: QT query
+// sub-tiles of 32 per wave and BK keys per stage; OCC = workgroups per CU the
+// register budget is sized for.  The d = 64 16-bit choices can be overridden
+// at build time for tuning sweeps.
+#ifndef MEA_T64_DKDV_QS
+#define MEA_T64_DKDV_QS 2
+#endif
+#ifndef MEA_T64_DKDV_OCC
+#define MEA_T64_DKDV_OCC 2
+#endif
+#ifndef MEA_T64_DQ_QT
+#define MEA_T64_DQ_QT 1
+#endif
+#ifndef MEA_T64_DQ_BK
+#define MEA_T64_DQ_BK 64
+#endif
+#ifndef MEA_T64_DQ_OCC
+#define MEA_T64_DQ_OCC 2
+#endif
 template <typename T, int D> struct BwdShape;
-template <> struct BwdShape<__bf16, 64> { static constexpr int QS = 2, BK = 64, OCC = 2; };
-template <> struct BwdShape<__bf16, 128> { static constexpr int QS = 1, BK = 64, OCC = 1; };
-template <> struct BwdShape<_Float16, 64> { static constexpr int QS = 2, BK = 64, OCC = 2; };
-template <> struct BwdShape<_Float16, 128> { static constexpr int QS = 1, BK = 64, OCC = 1; };
-template <> struct BwdShape<float, 64> { static constexpr int QS = 2, BK = 32, OCC = 1; };
-template <> struct BwdShape<float, 128> { static constexpr int QS = 1, BK = 32, OCC = 1; };
+template <> struct BwdShape<__bf16, 64> {
+  static constexpr int QS = MEA_T64_DKDV_QS, KV_OCC = MEA_T64_DKDV_OCC;
+  static constexpr int QT = MEA_T64_DQ_QT, BK = MEA_T64_DQ_BK, Q_OCC = MEA_T64_DQ_OCC;
+};
+template <> struct BwdShape<__bf16, 128> {
+  static constexpr int QS = 1, KV_OCC = 1, QT = 1, BK = 64, Q_OCC = 1;
+};
+template <> struct BwdShape<_Float16, 64> : BwdShape<__bf16, 64> {};
+template <> struct BwdShape<_Float16, 128> : BwdShape<__bf16, 128> {};
+template <> struct BwdShape<float, 64> {
+  static constexpr int QS = 2, KV_OCC = 1, QT = 1, BK = 32, Q_OCC = 2;
+};
+template <> struct BwdShape<float, 128> {
+  static constexpr int QS = 1, KV_OCC = 1, QT = 1, BK = 32, Q_OCC = 1;
+};
 
 template <typename T, typename TO, int D, bool CAUSAL>
 static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
@@ -491,14 +548,14 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
                                  dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
   if (e != hipSuccess) return e;
   p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
-  p.n_qtiles = (int)((p.n_q + 127) / 128);
+  p.n_qtiles = (int)((p.n_q + 128 * S::QT - 1) / (128 * S::QT));
   if (p.dk) {
-    e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, S::QS, S::OCC, CAUSAL>),
+    e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, S::QS, S::KV_OCC, CAUSAL>),
                         dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
     if (e != hipSuccess || !p.dq) return e;
   }
   const int dq_lds = 2 * 2 * S::BK * (D + 16 / (int)sizeof(T)) * (int)sizeof(T);
-  return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, S::BK, S::OCC, CAUSAL>),
+  return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, S::QT, S::BK, S::Q_OCC, CAUSAL>),
                          dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(256), args, dq_lds, stream);
 }
 

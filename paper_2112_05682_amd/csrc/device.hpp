@@ -118,6 +118,13 @@ __device__ __forceinline__ float xhalf_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Wait until every outstanding global load of this wave has completed
+// (s_waitcnt vmcnt(0), other counters unconstrained).  Issued once after the
+// loads of a kernel's register-resident operands, so that the main loop does
+// not re-wait for them -- the counter is in order, and a wait for an early
+// load inside the loop would also drain the prefetch of the next tile.
+__device__ __forceinline__ void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Convert eight float32 values to a fragment of T (round to nearest even).
 template <typename T>
 __device__ __forceinline__ Frag<T> to_frag(const float* x) {

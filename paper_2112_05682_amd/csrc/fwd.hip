@@ -102,6 +102,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     }
   }
 
+  wait_global_loads();
+
   f32x16 acc[QT][NDT];
 #pragma unroll
   for (int t = 0; t < QT; ++t)
@@ -208,6 +210,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     // more than kRescaleSlack powers of two: weights stay <= 2^kRescaleSlack,
     // numerator and denominator share the reference, so the result is the same
     // and the accumulator rescale is skipped on most tiles.
+    Frag<T> pf[QT][NPC];
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       float mx = -INFINITY;
@@ -230,27 +233,28 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       // A row with no visible key so far keeps m_ref = -inf; offset 0 keeps
       // its (all -inf) exponents at weight 0 instead of NaN.
       const float neg = (MASK && m_ref[t] == -INFINITY) ? 0.0f : -m_ref[t];
-      Frag<T> pf[NPC];
 #pragma unroll
       for (int pc = 0; pc < NPC; ++pc) {
         float e8[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg));
-        pf[pc] = to_frag<T>(e8);
-        l_run[t] = frag_sum(pf[pc], e8, l_run[t]);
+        pf[t][pc] = to_frag<T>(e8);
+        l_run[t] = frag_sum(pf[t][pc], e8, l_run[t]);
       }
+    }
+    // O^T += V^T P^T; each V^T fragment feeds every query sub-tile.
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
+    for (int dt = 0; dt < NDT; ++dt) {
 #pragma unroll
-        for (int pc = 0; pc < NPC; ++pc) {
-          Frag<T> a;
-          if constexpr (sizeof(T) == 2) {
-            a = lds_col_frag<T>(vs, RS, 16 * pc, 32 * dt, lane);
-          } else {
-            a = lds_col_frag_f32(reinterpret_cast<const float*>(vs), RS, 16 * pc, 32 * dt, lane);
-          }
-          acc[t][dt] = mma(a, pf[pc], acc[t][dt]);
+      for (int pc = 0; pc < NPC; ++pc) {
+        Frag<T> a;
+        if constexpr (sizeof(T) == 2) {
+          a = lds_col_frag<T>(vs, RS, 16 * pc, 32 * dt, lane);
+        } else {
+          a = lds_col_frag_f32(reinterpret_cast<const float*>(vs), RS, 16 * pc, 32 * dt, lane);
         }
+#pragma unroll
+        for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, pf[t][pc], acc[t][dt]);
       }
     }
   };
