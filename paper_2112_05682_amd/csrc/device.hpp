@@ -124,6 +124,35 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // not re-wait for them -- the counter is in order, and a wait for an early
 // load inside the loop would also drain the prefetch of the next tile.
 __device__ __forceinline__ void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// Wait until at most N vector-memory operations of this wave are in flight
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_global_loads_upto() {
+  static_assert(N >= 0 && N < 16, "vmcnt immediate");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+// LDS byte address of a pointer into shared memory (the low 32 bits of its
+// generic address).
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return static_cast<unsigned>(reinterpret_cast<uintptr_t>(p));
+}
+
+// Asynchronous copy global -> LDS of 16 bytes per lane (global_load_lds_dwordx4):
+// lane l's bytes land at lds_base + 16 l, lds_base being wave-uniform.  It is
+// issued from inline assembly so that the compiler adds no waits of its own
+// for it: the caller waits (wait_global_loads) and synchronises before the
+// data is read.  M0 carries the LDS address and needs one wait state before
+// the copy that reads it.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void copy_to_lds16(const void* src, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds_base)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
 
 // Convert eight float32 values to a fragment of T (round to nearest even).
 template <typename T>
@@ -132,6 +161,15 @@ __device__ __forceinline__ Frag<T> to_frag(const float* x) {
 #pragma unroll
   for (int s = 0; s < 8; ++s) r[s] = (T)x[s];
   return r;
+}
+
+// Two float32 values rounded to T (nearest even) and packed low, high.
+template <typename T>
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  static_assert(sizeof(T) == 2, "16-bit types only");
+  typedef T t2 __attribute__((ext_vector_type(2)));
+  const t2 v = {(T)a, (T)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // acc + the sum of the eight weights of a P fragment.  For 16-bit types the

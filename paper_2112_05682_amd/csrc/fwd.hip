@@ -30,9 +30,11 @@ namespace mea {
 // A tile raises the reference maximum only when one of its scores exceeds it
 // by more than this many powers of two (weights then stay <= 2^8).
 constexpr float kRescaleSlack = 8.0f;
+constexpr float kRescaleBound = 256.0f;  // 2^kRescaleSlack
 constexpr float kLn2 = 0.6931471805599453f;
 
 template <bool B> struct BoolC { static constexpr bool value = B; };
+template <int I> struct IntC { static constexpr int value = I; };
 
 template <typename T, int D, int QT, int BK>
 struct FwdTile {
@@ -50,8 +52,8 @@ struct FwdTile {
   static_assert(BK % 32 == 0 && D % 32 == 0, "tile shapes are multiples of 32");
 };
 
-template <typename T, typename TO, int D, int QT, int BK, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
+template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
+__global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   using Cfg = FwdTile<T, D, QT, BK>;
   constexpr int RS = Cfg::RS;
   constexpr int KC = D / 16;    // 16-wide k chunks of the QK^T contraction
@@ -318,6 +320,414 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Forward for 16-bit inputs at d = 64: two wave groups in opposite phases.
+//
+// A workgroup is 8 waves; wave w and wave w + 4 share a SIMD.  Waves 0-3
+// (group 0) and 4-7 (group 1) alternate between an MFMA phase (scores of key
+// tile j and the PV product of tile j-1) and a vector phase (the lazy softmax
+// of the tile whose scores they computed), one barrier between phases, so that
+// on every SIMD one wave feeds the matrix cores while the other runs the
+// exponentials.  Group 1 runs one phase behind group 0.  K and V tiles go from
+// memory to LDS with global_load_lds (no staging registers), issued by group 1
+// during its vector phase two phases before they are read; rows are stored
+// unpadded with an XOR swizzle of their 16-byte chunks that keeps both the
+// row-fragment reads of K and the transposing reads of V free of bank
+// conflicts.
+// ---------------------------------------------------------------------------
+namespace pp {
+constexpr int D = 64, QT = 2, BK = 64, NW = 8, BQ = NW * QT * 32, NSTAGE = 3;
+constexpr int ROWB = D * 2;          // bytes per LDS row (unpadded)
+constexpr int TILEB = BK * ROWB;     // 8 KiB per K or V tile
+// Physical 16-byte chunk of logical chunk x in row r.
+__device__ __forceinline__ int swz_k(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ int swz_v(int r) { return ((r >> 1) & 1) << 2; }
+}  // namespace pp
+
+template <typename T, typename TO, bool CAUSAL>
+__global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
+  using namespace pp;
+  constexpr int KC = D / 16, NKT = BK / 32, NPC = BK / 16, NDT = D / 32;
+  static_assert(sizeof(T) == 2, "16-bit inputs only");
+
+  // Three stages each of K and V: tile j of K lives in kst[j % 3], of V in
+  // vst[j % 3].
+  __shared__ __align__(16) unsigned char kst[NSTAGE * TILEB], vst[NSTAGE * TILEB];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int grp = wave >> 2;
+  const int lane = tid & 63;
+  const int h = lane >> 5, c = lane & 31;
+
+  const int w = xcd_remap(blockIdx.x, gridDim.x);
+  const int qt_idx = w % p.n_qtiles;
+  const int rest = w / p.n_qtiles;
+  const int bh = rest % p.bh;
+  const int split = rest / p.bh;
+  const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;
+  const int64_t q0 = (int64_t)qtile * BQ;
+  const int64_t qw = q0 + (int64_t)wave * QT * 32;
+
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+
+  const int64_t kb = (int64_t)split * p.keys_per_split;
+  int64_t ke = kb + p.keys_per_split;
+  if (ke > p.n_k) ke = p.n_k;
+  if (CAUSAL && ke > q0 + BQ) ke = q0 + BQ;
+  const int n_tiles = ke > kb ? (int)((ke - kb + BK - 1) / BK) : 0;
+  int n_plain = n_tiles;
+  {
+    const int64_t full = (p.n_k - kb) / BK;
+    if (full < n_plain) n_plain = (int)full;
+    if (CAUSAL) {
+      const int64_t below = q0 - kb + 1 > 0 ? (q0 - kb + 1) / BK : 0;
+      if (below < n_plain) n_plain = (int)below;
+    }
+  }
+
+  Frag<T> qf[QT][KC];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int64_t row = qw + 32 * t + c;
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      if (row < p.n_q) {
+        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + row * D + 16 * kc + 8 * h);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[t][kc][e] = (T)0.0f;
+      }
+    }
+  }
+  wait_global_loads();
+
+  f32x16 acc[QT][NDT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t)
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[t][dt][r] = 0.0f;
+  float m_ref[QT], l_run[QT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_ref[t] = -INFINITY;
+    l_run[t] = 0.0f;
+  }
+  const float cl2 = p.scale_log2;
+
+  auto kstage = [&](int j) { return kst + (j % NSTAGE) * TILEB; };
+  auto vstage = [&](int j) { return vst + (j % NSTAGE) * TILEB; };
+
+  // Asynchronous copy of rows [k0, k0 + BK) of K or V into an LDS stage.  One
+  // instruction moves 1 KiB = 8 rows; the lane writing physical chunk x of row
+  // r fetches logical chunk x ^ swz(r).  Rows past n_k repeat the last key row
+  // (finite data; those keys are masked).
+  auto load_tile = [&](const T* g, int64_t k0, unsigned char* stage, bool is_v, int part, int nparts)
+                       __attribute__((always_inline)) {
+    for (int ii = part; ii < BK / 8; ii += nparts) {
+      const int row = 8 * ii + (lane >> 3);
+      const int x = lane & 7;
+      const int lchunk = x ^ (is_v ? swz_v(row) : swz_k(row));
+      int64_t key = k0 + row;
+      if (key > p.n_k - 1) key = p.n_k - 1;
+      const T* src = g + key * D + lchunk * 8;
+      copy_to_lds16(src, __builtin_amdgcn_readfirstlane(lds_addr(stage) + ii * 1024));
+    }
+  };
+
+  // S^T of tile j for both query sub-tiles.
+  auto scores = [&](const unsigned char* ks, f32x16 (&s)[NKT][QT]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kt][t][r] = 0.0f;
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        const int row = 32 * kt + perm32(c);
+        const int x = (2 * kc + h) ^ swz_k(row);
+        const Frag<T> a = *reinterpret_cast<const Frag<T>*>(ks + row * ROWB + x * 16);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
+      }
+    }
+  };
+
+  // O^T += V^T P^T for tile j: the V^T column fragments come from the
+  // transposing LDS read (see lds_col_frag), with the V swizzle applied.
+  auto pv = [&](const unsigned char* vs, Frag<T> (&pf)[QT][NPC]) __attribute__((always_inline)) {
+    const int g = lane >> 4, i = lane & 15;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+#pragma unroll
+      for (int pc = 0; pc < NPC; ++pc) {
+        const int row = 16 * pc + 8 * (g >> 1) + (i >> 2);
+        const int colb = 2 * (32 * dt + 16 * (g & 1) + 4 * (i & 3));
+        const int addr_lo = row * ROWB + (((colb >> 4) ^ swz_v(row)) << 4) + (colb & 15);
+        const int addr_hi = (row + 4) * ROWB + (((colb >> 4) ^ swz_v(row + 4)) << 4) + (colb & 15);
+        const v4s_t lo = lds_read_tr16(vs + addr_lo);
+        const v4s_t hi = lds_read_tr16(vs + addr_hi);
+        typedef short v8s_t __attribute__((ext_vector_type(8)));
+        v8s_t r8;
+        r8[0] = lo[0]; r8[1] = lo[1]; r8[2] = lo[2]; r8[3] = lo[3];
+        r8[4] = hi[0]; r8[5] = hi[1]; r8[6] = hi[2]; r8[7] = hi[3];
+        const Frag<T> a = __builtin_bit_cast(Frag<T>, r8);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, pf[t][pc], acc[t][dt]);
+      }
+    }
+  };
+
+  // Lazy softmax (Section 3) of query sub-tile t of tile j: P = 2^(c s - m)
+  // against the current reference m, rounded into pfo[t], and the lane's
+  // partial row sum added to l.  The reference has to rise only when a weight
+  // would exceed 2^kRescaleSlack; a lane sum above that bound (or not finite,
+  // or no reference yet) flags it, and the flagged sub-tile is redone against
+  // the tile's true maximum, rescaling the running numerator and denominator.
+  // The common path thus needs no row maximum at all.
+  auto mask_sub = [&](int j, auto t_tag, f32x16 (&s)[NKT][QT]) __attribute__((always_inline)) {
+    constexpr int t = decltype(t_tag)::value;
+    const int64_t k0 = kb + (int64_t)j * BK;
+    const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+    const int lim_c = CAUSAL ? (int)(qw - k0) + c + 32 * t + 1 : BK;
+    const int lim = lim_c < key_lim ? lim_c : key_lim;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (32 * kt + permuted_row(r, h) >= lim) s[kt][t][r] = -INFINITY;
+  };
+  auto weights = [&](auto t_tag, f32x16 (&s)[NKT][QT], Frag<T> (&pfo)[QT][NPC], float neg)
+                     __attribute__((always_inline)) {
+    constexpr int t = decltype(t_tag)::value;
+    float sum0 = 0.0f, sum1 = 0.0f;
+#pragma unroll
+    for (int pc = 0; pc < NPC; ++pc) {
+      float e8[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg));
+      pfo[t][pc] = to_frag<T>(e8);
+      if (pc & 1) sum1 = frag_sum(pfo[t][pc], e8, sum1);
+      else sum0 = frag_sum(pfo[t][pc], e8, sum0);
+    }
+    return sum0 + sum1;
+  };
+  auto finish_sub = [&](auto t_tag, f32x16 (&s)[NKT][QT], Frag<T> (&pfo)[QT][NPC], float tsum)
+                        __attribute__((always_inline)) {
+    constexpr int t = decltype(t_tag)::value;
+    const bool redo = !(tsum <= kRescaleBound) || m_ref[t] == -INFINITY;
+    if (__builtin_amdgcn_ballot_w64(redo)) {
+      // Rare path: keep it a branch (an empty volatile statement cannot be
+      // speculated, so the compiler does not flatten it into the common path).
+      asm volatile("");
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kt][t][r]);
+      const float m_new = fmaxf(m_ref[t], xhalf_max(mx) * cl2);
+      const float alpha = m_new == -INFINITY ? 1.0f : fast_exp2(m_ref[t] - m_new);
+      l_run[t] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[t][dt][r] *= alpha;
+      m_ref[t] = m_new;
+      tsum = weights(t_tag, s, pfo, m_new == -INFINITY ? 0.0f : -m_new);
+    }
+    l_run[t] += tsum;
+  };
+  // O += V(j-1) P(j-1) for both sub-tiles, interleaved step by step with the
+  // weights of sub-tile 0 of tile j (a wave issues VALU work slowly, so it
+  // fills the gaps between its own MFMAs).  Returns that sub-tile's lane sum.
+  auto pv_weights0 = [&](const unsigned char* vs, Frag<T> (&pf_old)[QT][NPC], Frag<T> (&pf_new)[QT][NPC],
+                         f32x16 (&s)[NKT][QT], float neg) __attribute__((always_inline)) {
+    constexpr int NSTEP = NDT * NPC;
+    const int g = lane >> 4, i4 = lane & 15;
+    auto vfrag = [&](int step) __attribute__((always_inline)) {
+      const int dt = step / NPC, pc = step % NPC;
+      const int row = 16 * pc + 8 * (g >> 1) + (i4 >> 2);
+      const int colb = 2 * (32 * dt + 16 * (g & 1) + 4 * (i4 & 3));
+      const int addr_lo = row * ROWB + (((colb >> 4) ^ swz_v(row)) << 4) + (colb & 15);
+      const int addr_hi = (row + 4) * ROWB + (((colb >> 4) ^ swz_v(row + 4)) << 4) + (colb & 15);
+      const v4s_t lo = lds_read_tr16(vs + addr_lo);
+      const v4s_t hi = lds_read_tr16(vs + addr_hi);
+      typedef short v8s_t __attribute__((ext_vector_type(8)));
+      v8s_t r8;
+      r8[0] = lo[0]; r8[1] = lo[1]; r8[2] = lo[2]; r8[3] = lo[3];
+      r8[4] = hi[0]; r8[5] = hi[1]; r8[6] = hi[2]; r8[7] = hi[3];
+      return __builtin_bit_cast(Frag<T>, r8);
+    };
+    Frag<T> vf[2];
+    vf[0] = vfrag(0);
+    u32x4 packed;
+    float sum0 = 0.0f, sum1 = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NSTEP; ++i) {
+      const int dt = i / NPC, pcv = i % NPC;
+      if (i + 1 < NSTEP) vf[(i + 1) & 1] = vfrag(i + 1);
+      const int pcs = i >> 1, half = i & 1;
+      acc[0][dt] = mma(vf[i & 1], pf_old[0][pcv], acc[0][dt]);
+      float e4[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        e4[e] = fast_exp2(fmaf(s[pcs >> 1][0][8 * (pcs & 1) + 4 * half + e], cl2, neg));
+      packed[2 * half] = pack2<T>(e4[0], e4[1]);
+      packed[2 * half + 1] = pack2<T>(e4[2], e4[3]);
+      acc[1][dt] = mma(vf[i & 1], pf_old[1][pcv], acc[1][dt]);
+      if (half) {
+        pf_new[0][pcs] = __builtin_bit_cast(Frag<T>, packed);
+        if (pcs & 1) sum1 = frag_sum(pf_new[0][pcs], nullptr, sum1);
+        else sum0 = frag_sum(pf_new[0][pcs], nullptr, sum0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    return sum0 + sum1;
+  };
+  // The copies into LDS are invisible to the compiler (inline assembly), so
+  // the barrier also fences the compiler: no LDS access moves across it.
+  auto barrier = [&]() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
+  };
+
+  // Every wave runs the same sequence -- MFMA phase of tile j, barrier,
+  // softmax phase of tile j, barrier -- and group 1 starts one barrier later,
+  // so its MFMA phases coincide with group 0's softmax phases.  A wave issues
+  // at most about one VALU instruction per 7 cycles, so the softmax is split:
+  // sub-tile 0 is computed in the MFMA phase, interleaved with O += V P of the
+  // previous tile, and sub-tile 1 in the softmax phase.  Group 1 also moves the
+  // tiles: in its softmax phase of tile j it issues K(j+3) (into the stage of
+  // K(j)) and V(j+2) (into the stage of V(j-1)); K(j) and V(j-1) are last read
+  // in global phases 2j and 2j+1.  Before the barrier that ends its MFMA phase
+  // of tile j it waits for K(j+1) and V(j), issued two softmax phases earlier,
+  // letting the copies of the last softmax phase run on.
+  f32x16 s[NKT][QT];
+  Frag<T> pfa[QT][NPC], pfb[QT][NPC];
+#pragma unroll
+  for (int t = 0; t < QT; ++t)
+#pragma unroll
+    for (int pc = 0; pc < NPC; ++pc)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pfb[t][pc][e] = (T)0.0f;
+  // Tile 0 multiplies the V(-1) stage by zero weights: clear it so that it
+  // holds finite values.
+  reinterpret_cast<u32x4*>(vstage(NSTAGE - 1))[tid] = u32x4{0u, 0u, 0u, 0u};
+  static_assert(NW * 64 * 16 == TILEB, "one 16-byte store per thread clears a stage");
+  if (n_tiles > 0) load_tile(kg, kb, kstage(0), false, wave, NW);  // K(0): one instruction per wave
+  // The barrier's fence does not cover copies the compiler cannot see.
+  wait_global_loads();
+  __syncthreads();
+  // Group 1 issues two waves of copies ahead, as if from softmax phases -2
+  // and -1, and starts one phase behind group 0.
+  auto issue = [&](int j) __attribute__((always_inline)) {
+    if (j + 3 < n_tiles) load_tile(kg, kb + (int64_t)(j + 3) * BK, kstage(j + 3), false, wave - 4, 4);
+    if (j + 2 < n_tiles) load_tile(vg, kb + (int64_t)(j + 2) * BK, vstage(j + 2), true, wave - 4, 4);
+  };
+  if (grp == 1) {
+    issue(-2);
+    issue(-1);
+    barrier();
+  }
+  // pf_old holds P(j-1) and pf_new receives P(j).
+  auto iteration = [&](auto mask_tag, int j, Frag<T> (&pf_old)[QT][NPC], Frag<T> (&pf_new)[QT][NPC])
+                       __attribute__((always_inline)) {
+    const unsigned char* kcur = kstage(j);
+    const unsigned char* vprev = vstage(j + NSTAGE - 1);
+    constexpr bool MASK = decltype(mask_tag)::value;
+    scores(kcur, s);
+    if constexpr (MASK) mask_sub(j, IntC<0>{}, s);
+    finish_sub(IntC<0>{}, s, pf_new, pv_weights0(vprev, pf_old, pf_new, s, -m_ref[0]));
+    // Only group 1 has copies in flight (two per wave per tile); the wait is
+    // a no-op for group 0.
+    if (j + 2 < n_tiles) wait_global_loads_upto<4>();
+    else if (j + 1 < n_tiles) wait_global_loads_upto<2>();
+    else wait_global_loads();
+    barrier();
+    if constexpr (MASK) mask_sub(j, IntC<1>{}, s);
+    finish_sub(IntC<1>{}, s, pf_new, weights(IntC<1>{}, s, pf_new, -m_ref[1]));
+    if (grp == 1) issue(j);
+    barrier();
+  };
+  auto copy_p = [&](Frag<T> (&dst)[QT][NPC], const Frag<T> (&src)[QT][NPC]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+#pragma unroll
+      for (int pc = 0; pc < NPC; ++pc) dst[t][pc] = src[t][pc];
+  };
+  // Plain tiles and masked tiles (ragged tail, causal diagonal) run in
+  // separate loops; a per-tile branch between the two softmax variants would
+  // keep both variants' registers live.  The plain loop is unrolled by two so
+  // that the weight buffers it touches are known at compile time.
+  int j = 0;
+  for (; j + 2 <= n_plain; j += 2) {
+    iteration(BoolC<false>{}, j, pfb, pfa);
+    iteration(BoolC<false>{}, j + 1, pfa, pfb);
+  }
+  // Here and after every later tile, pfb holds the weights of tile j - 1.
+  if (j < n_plain) {
+    iteration(BoolC<false>{}, j, pfb, pfa);
+    copy_p(pfb, pfa);
+    ++j;
+  }
+  for (; j < n_tiles; ++j) {
+    iteration(BoolC<true>{}, j, pfb, pfa);
+    copy_p(pfb, pfa);
+  }
+  if (n_tiles > 0) pv(vstage(n_tiles - 1), pfb);
+  barrier();
+  barrier();
+  if (grp == 0) barrier();  // same number of barriers in both groups
+
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const float l_tot = xhalf_sum(l_run[t]);
+    const int64_t row = qw + 32 * t + c;
+    if (row >= p.n_q) continue;
+    if (p.n_splits == 1) {
+      const float inv = 1.0f / l_tot;
+      TO* og = static_cast<TO*>(p.o) + ((size_t)bh * p.n_q + row) * D;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          typename FragT<TO>::half v4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
+          *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
+        }
+      if (h == 0 && p.lse)
+        p.lse[(size_t)bh * p.n_q + row] = (m_ref[t] + __log2f(l_tot)) * kLn2;
+    } else {
+      const size_t prow = ((size_t)split * p.bh + bh) * p.n_q + row;
+      float* po = p.part_o + prow * D;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          f32x4 v4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v4[e] = acc[t][dt][4 * a4 + e];
+          *reinterpret_cast<f32x4*>(po + 32 * dt + 8 * a4 + 4 * h) = v4;
+        }
+      if (h == 0) {
+        p.part_m[prow] = m_ref[t];
+        p.part_l[prow] = l_tot;
+      }
+    }
+  }
+}
+
 // Combine of the per-split summaries (Section 4): global max, rescale each
 // split's numerator and denominator by e^{m_s - m_g}, add, divide.  One thread
 // per (row, 4 features).
@@ -351,10 +761,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
 
 // ---------------------------------------------------------------- launchers
 
-template <typename T, typename TO, int D, int QT, int BK, bool CAUSAL>
+template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
 static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
   using Cfg = FwdTile<T, D, QT, BK>;
-  auto kern = attn_fwd_kernel<T, TO, D, QT, BK, CAUSAL>;
+  auto kern = attn_fwd_kernel<T, TO, D, QT, BK, OCC, CAUSAL>;
   const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
   FwdParams pc = p;
   void* args[] = {&pc};
@@ -367,11 +777,30 @@ static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
                          dim3(256), args, 0, stream);
 }
 
+template <typename T, typename TO, bool CAUSAL>
+static hipError_t launch_fwd_pp(const FwdParams& p, hipStream_t stream) {
+  auto kern = attn_fwd_pp_kernel<T, TO, CAUSAL>;
+  const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
+  FwdParams pc = p;
+  void* args[] = {&pc};
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid),
+                                 dim3(pp::NW * 64), args, 0, stream);
+  if (e != hipSuccess || p.n_splits == 1) return e;
+  auto comb = attn_combine_kernel<TO, pp::D>;
+  const int64_t threads = (int64_t)p.bh * p.n_q * (pp::D / 4);
+  return hipLaunchKernel(reinterpret_cast<const void*>(comb), dim3((unsigned)((threads + 255) / 256)),
+                         dim3(256), args, 0, stream);
+}
+
 template <typename T, typename TO, int D>
 static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t stream) {
-  constexpr int QT = FwdShape<T, D>::QT, BK = FwdShape<T, D>::BK;
-  return causal ? launch_fwd_impl<T, TO, D, QT, BK, true>(p, stream)
-                : launch_fwd_impl<T, TO, D, QT, BK, false>(p, stream);
+  if constexpr (sizeof(T) == 2 && D == 64 && FwdShape<T, D>::BQ == pp::BQ) {
+    return causal ? launch_fwd_pp<T, TO, true>(p, stream) : launch_fwd_pp<T, TO, false>(p, stream);
+  } else {
+    constexpr int QT = FwdShape<T, D>::QT, BK = FwdShape<T, D>::BK, OCC = FwdShape<T, D>::OCC;
+    return causal ? launch_fwd_impl<T, TO, D, QT, BK, OCC, true>(p, stream)
+                  : launch_fwd_impl<T, TO, D, QT, BK, OCC, false>(p, stream);
+  }
 }
 
 template <typename T, int D>

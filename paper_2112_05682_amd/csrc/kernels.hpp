@@ -49,13 +49,26 @@ struct BwdParams {
 
 // Tile shapes per (element type, head dimension); shared by the host plan
 // and the kernel instantiations.
+// 16-bit d = 64 forward: BQ = 512 selects the two-group ping-pong kernel
+// (8 waves); otherwise the 4-wave kernel runs with QT = BQ / 128 query
+// sub-tiles per wave and MEA_T64_FWD_OCC workgroups per CU.
+#ifndef MEA_T64_FWD_BQ
+#define MEA_T64_FWD_BQ 512
+#endif
+#ifndef MEA_T64_FWD_OCC
+#define MEA_T64_FWD_OCC 2
+#endif
 template <typename T, int D> struct FwdShape;
-template <> struct FwdShape<__bf16, 64> { static constexpr int QT = 2, BK = 64, BQ = 256; };
-template <> struct FwdShape<__bf16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128; };
-template <> struct FwdShape<_Float16, 64> { static constexpr int QT = 2, BK = 64, BQ = 256; };
-template <> struct FwdShape<_Float16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128; };
-template <> struct FwdShape<float, 64> { static constexpr int QT = 1, BK = 32, BQ = 128; };
-template <> struct FwdShape<float, 128> { static constexpr int QT = 1, BK = 32, BQ = 128; };
+template <> struct FwdShape<__bf16, 64> {
+  static constexpr int BQ = MEA_T64_FWD_BQ, QT = BQ == 512 ? 2 : BQ / 128, BK = 64, OCC = MEA_T64_FWD_OCC;
+};
+template <> struct FwdShape<__bf16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128, OCC = 2; };
+template <> struct FwdShape<_Float16, 64> {
+  static constexpr int BQ = MEA_T64_FWD_BQ, QT = BQ == 512 ? 2 : BQ / 128, BK = 64, OCC = MEA_T64_FWD_OCC;
+};
+template <> struct FwdShape<_Float16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128, OCC = 2; };
+template <> struct FwdShape<float, 64> { static constexpr int QT = 1, BK = 32, BQ = 128, OCC = 2; };
+template <> struct FwdShape<float, 128> { static constexpr int QT = 1, BK = 32, BQ = 128, OCC = 2; };
 
 // dtype codes follow mea_dtype: 0 = f32, 1 = f16, 2 = bf16.
 // out_f32: o (and, in the backward, do) are float32 instead of the input dtype.
