@@ -84,8 +84,10 @@ typedef struct {
  * Section 4 rescales and adds.  Returns MEA_OK or a validation error. */
 mea_status mea_attention_fwd_workspace_size(const mea_problem* p, size_t* bytes);
 
-/* Bytes of device workspace mea_attention_bwd needs for `p`: the per-row
- * D_i = sum_t dO_it O_it (float32 [B, H, n_q]), O(n) like the lse. */
+/* Bytes of device workspace mea_attention_bwd needs for `p`: two per-row
+ * float32 arrays of B*H*ceil(n_q/64)*64 entries each, holding -lse/scale and
+ * -D_i with D_i = sum_t dO_it O_it (Section 5.2's recompute needs only these
+ * and the inputs), O(n) like the lse. */
 mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes);
 
 /* Forward (Sections 2-4): o = softmax(scale * q k^T) v, computed tile by

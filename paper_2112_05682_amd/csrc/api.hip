@@ -96,8 +96,17 @@ FwdPlan plan_fwd(const mea_problem* p) {
   return pl;
 }
 
+int64_t bwd_row_pad(int64_t n_q) { return (n_q + mea::kBwdRowPad - 1) / mea::kBwdRowPad * mea::kBwdRowPad; }
+
+// Bytes of one per-row backward array, rounded to 256.
+size_t bwd_row_array_bytes(const mea_problem* p) {
+  const size_t b = (size_t)p->batch * (size_t)p->heads * (size_t)bwd_row_pad(p->n_q) * 4;
+  return (b + 255) / 256 * 256;
+}
+
 size_t bwd_workspace(const mea_problem* p) {
-  return (size_t)p->batch * (size_t)p->heads * (size_t)p->n_q * 4 + 256;
+  // s_init and dp_init, [B*H, n_q_pad] float32 each, 256-byte aligned.
+  return 2 * bwd_row_array_bytes(p) + 256;
 }
 
 float* align256(void* base, size_t off) {
@@ -203,7 +212,9 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   bp.dq = dq;
   bp.dk = dk;
   bp.dv = dv;
-  bp.delta = align256(workspace, 0);
+  bp.n_q_pad = bwd_row_pad(p->n_q);
+  bp.s_init = align256(workspace, 0);
+  bp.dp_init = bp.s_init + bwd_row_array_bytes(p) / 4;
   bp.n_q = p->n_q;
   bp.n_k = p->n_k;
   bp.bh = (int)(p->batch * p->heads);

@@ -21,17 +21,21 @@ namespace mea {
 template <bool B> struct BoolC { static constexpr bool value = B; };
 
 // ------------------------------------------------------------------- pre
+// D_i = dO_i . O_i and the accumulator initial values of every (padded) row.
 template <typename TO, int D>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
   using T = TO;  // o and do share the output dtype
   constexpr int E = sizeof(T);
   constexpr int TPR = D * E / 16;  // threads per row, 16 bytes each
   constexpr int RPB = 256 / TPR;
-  const int64_t rows = (int64_t)p.bh * p.n_q;
-  const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / TPR;
+  const int64_t rows = (int64_t)p.bh * p.n_q_pad;
+  const int64_t prow = (int64_t)blockIdx.x * RPB + threadIdx.x / TPR;  // padded row
+  const int64_t bh = prow / p.n_q_pad, i = prow % p.n_q_pad;
+  const bool real = prow < rows && i < p.n_q;
+  const int64_t row = bh * p.n_q + i;
   const int part = threadIdx.x % TPR;
   float acc = 0.0f;
-  if (row < rows) {
+  if (real) {
     typedef T vec16 __attribute__((ext_vector_type(16 / E)));
     const vec16 o = *reinterpret_cast<const vec16*>(static_cast<const T*>(p.o) + row * D + part * (16 / E));
     const vec16 g = *reinterpret_cast<const vec16*>(static_cast<const T*>(p.d_o) + row * D + part * (16 / E));
@@ -40,7 +44,10 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
   }
 #pragma unroll
   for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, TPR);
-  if (row < rows && part == 0) p.delta[row] = acc;
+  if (prow < rows && part == 0) {
+    p.s_init[prow] = real ? -p.lse[row] / p.scale : -INFINITY;
+    p.dp_init[prow] = real ? -acc : 0.0f;
+  }
 }
 
 // ------------------------------------------------------------------- dK, dV
@@ -58,6 +65,7 @@ struct DkdvTile {
   static constexpr int STAGE_ELEMS = 2 * TILE;
   static constexpr int STAGE_BYTES = STAGE_ELEMS * E + 2 * BQ * 4;  // + accumulator initial values
   static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+  static_assert(kBwdRowPad % BQ == 0, "query tiles must not pass the padded row count");
 };
 
 template <typename T, typename TO, int D, int QS, int OCC, bool CAUSAL>
@@ -83,8 +91,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 
   const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
   const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + (size_t)bh * p.n_q * D;
-  const float* __restrict__ lseg = p.lse + (size_t)bh * p.n_q;
-  const float* __restrict__ deltag = p.delta + (size_t)bh * p.n_q;
+  const float* __restrict__ sinitg = p.s_init + (size_t)bh * p.n_q_pad;
+  const float* __restrict__ dpinitg = p.dp_init + (size_t)bh * p.n_q_pad;
   const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
   const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
 
@@ -121,7 +129,6 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 
   u32x4 stage[Cfg::CPT];
   float stage_f = 0.0f;
-  const float inv_scale = 1.0f / p.scale;
   auto stage_base = [&](int buf) { return smem_raw + buf * Cfg::STAGE_BYTES; };
   auto load_stage = [&](int64_t q0) {
 #pragma unroll
@@ -140,13 +147,9 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       }
     }
     if (tid < 2 * Cfg::BQ) {
-      // Raw lse (or D) of the row; transformed only when written to LDS, so
-      // that nothing waits on this load before the tile's compute.
+      // Accumulator initial value of the row (rows up to n_q_pad exist).
       const int64_t q = q0 + (tid % Cfg::BQ);
-      if (tid < Cfg::BQ)
-        stage_f = q < p.n_q ? lseg[q] : INFINITY;
-      else
-        stage_f = q < p.n_q ? deltag[q] : 0.0f;
+      stage_f = tid < Cfg::BQ ? sinitg[q] : dpinitg[q];
     }
   };
   auto store_stage = [&](int buf) {
@@ -166,7 +169,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       // P = 2^(c*acc) (c = scale*log2 e), dP - D makes dS = P*acc.  Rows past
       // n_q start at -inf, so their weights are 0.
       float* f = reinterpret_cast<float*>(stage_base(buf) + Cfg::STAGE_ELEMS * Cfg::E);
-      f[tid] = tid < Cfg::BQ ? -stage_f * inv_scale : -stage_f;
+      f[tid] = stage_f;
     }
   };
 
@@ -337,8 +340,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
         }
       }
     }
-    s_init[t] = valid ? -p.lse[(size_t)bh * p.n_q + query] / p.scale : -INFINITY;
-    dp_init[t] = valid ? -p.delta[(size_t)bh * p.n_q + query] : 0.0f;
+    s_init[t] = valid ? p.s_init[(size_t)bh * p.n_q_pad + query] : -INFINITY;
+    dp_init[t] = valid ? p.dp_init[(size_t)bh * p.n_q_pad + query] : 0.0f;
   }
   wait_global_loads();
 
@@ -542,7 +545,7 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   using S = BwdShape<T, D>;
   using Dk = DkdvTile<T, D, S::QS>;
   void* args[] = {&p};
-  const int64_t rows = (int64_t)p.bh * p.n_q;
+  const int64_t rows = (int64_t)p.bh * p.n_q_pad;
   constexpr int RPB = 256 / (D * (int)sizeof(TO) / 16);
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, D>),
                                  dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);

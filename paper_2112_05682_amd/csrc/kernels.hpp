@@ -37,7 +37,14 @@ struct BwdParams {
   void* dq;
   void* dk;
   void* dv;
-  float* delta;  // D_i = dO_i . O_i, [B*H, n_q]
+  // Per-row initial values of the score and dP accumulators, written by the
+  // preprocess kernel, [B*H, n_q_pad] float32: s_init = -lse / scale (so that
+  // P = 2^(c * (S + s_init)), c = scale * log2 e) and dp_init = -D with
+  // D_i = dO_i . O_i (so that dS = P * (dP + dp_init)).  Rows n_q .. n_q_pad - 1
+  // hold -inf and 0: they contribute nothing.
+  float* s_init;
+  float* dp_init;
+  int64_t n_q_pad;  // n_q rounded up to kBwdRowPad
   int64_t n_q;
   int64_t n_k;
   int bh;
@@ -46,6 +53,10 @@ struct BwdParams {
   float scale;
   float scale_log2;
 };
+
+// Row padding of the backward's per-row arrays (a multiple of every query
+// tile the backward kernels stage).
+constexpr int kBwdRowPad = 64;
 
 // Tile shapes per (element type, head dimension); shared by the host plan
 // and the kernel instantiations.
