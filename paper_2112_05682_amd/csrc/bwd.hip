@@ -282,6 +282,300 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
     }
 }
 
+// -------------------------------------------------- dK, dV (two groups)
+// 16-bit inputs and outputs, d = 64.  Eight waves of 32 keys each (K and V in
+// registers, dK and dV accumulated in registers) in two groups of four that
+// alternate an MFMA phase and a VALU phase, separated by workgroup barriers;
+// group 1 runs one phase behind group 0, so waves w and w + 4, which share a
+// SIMD, always have different roles.  MFMA phase of query tile i: dV += P^T dO
+// and dK += dS^T Q for tile i - 1, then S = Q K^T and dP = dO V^T for tile i.
+// VALU phase of tile i: P = 2^(c S), dS = P dP (the accumulators start at
+// -lse/scale and -D), rounded into the operands of the next MFMA phase.
+// Q, dO and the initial values stream through a four-stage LDS ring with
+// asynchronous global -> LDS copies issued by group 1.
+namespace kvpp {
+constexpr int D = 64, NW = 8, BKG = NW * 32, BQ = 64, QS = BQ / 32, NSTAGE = 4;
+constexpr int RSB = 144;                      // bytes per LDS row (128 + 16 pad)
+constexpr int TILEB = BQ * RSB;               // one Q or dO tile: 9 KiB
+constexpr int INITB = 2 * BQ * 4;             // s_init and dp_init of the tile
+constexpr int STAGEB = 2 * TILEB + INITB;     // 18944 bytes
+constexpr int UNITS = 2 * TILEB / 1024 + 1;   // 1 KiB copies per stage (18 + 1)
+static_assert(TILEB % 1024 == 0 && INITB == 512, "stage layout");
+}  // namespace kvpp
+
+template <typename T, bool CAUSAL>
+__global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
+  using namespace kvpp;
+  static_assert(sizeof(T) == 2, "16-bit inputs only");
+  constexpr int KC = D / 16, NDT = D / 32, NQC = BQ / 16;
+  __shared__ __align__(16) unsigned char smem[NSTAGE * STAGEB];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;
+  const int lane = tid & 63;
+  const int h = lane >> 5, c = lane & 31;
+
+  const int w = xcd_remap(blockIdx.x, gridDim.x);
+  const int kt_idx = w % p.n_ktiles;
+  const int bh = w / p.n_ktiles;
+  const int64_t k0 = (int64_t)kt_idx * BKG;
+  const int64_t kw = k0 + 32 * wave;
+  const int64_t key = kw + c;
+
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const float* __restrict__ sinitg = p.s_init + (size_t)bh * p.n_q_pad;
+  const float* __restrict__ dpinitg = p.dp_init + (size_t)bh * p.n_q_pad;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+
+  Frag<T> kf[KC], vf[KC];
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (key < p.n_k) {
+      kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * D + 16 * kc + 8 * h);
+      vf[kc] = *reinterpret_cast<const Frag<T>*>(vg + key * D + 16 * kc + 8 * h);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        kf[kc][e] = (T)0.0f;
+        vf[kc][e] = (T)0.0f;
+      }
+    }
+  }
+  wait_global_loads();
+
+  f32x16 dk[NDT], dv[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      dk[dt][r] = 0.0f;
+      dv[dt][r] = 0.0f;
+    }
+
+  // Queries before the workgroup's first key see none of its keys (causal).
+  const int64_t q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
+  const int n_iters = q_begin < p.n_q ? (int)((p.n_q - q_begin + BQ - 1) / BQ) : 0;
+  auto stage = [&](int i) { return smem + (i % NSTAGE) * STAGEB; };
+
+  // Copy unit u (0 <= u < UNITS) of query tile i into its stage: units 0..8
+  // are the Q tile, 9..17 the dO tile (lane slot s = 64 (u % 9) + lane is row
+  // s / 9, 16-byte chunk s % 9; chunk 8 is the row pad and gets a copy of
+  // chunk 7), unit 18 the initial values (lanes 0..15 s_init, 16..31 dp_init;
+  // the padded arrays hold every row of the tile).  Query rows past n_q repeat
+  // the last row (finite values; their weights are 0).
+  auto unit_row = [&](int u) { return (64 * (u % 9) + lane) / 9; };
+  auto unit_col = [&](int u) {
+    const int ch = (64 * (u % 9) + lane) % 9;
+    return 8 * (ch < 8 ? ch : 7);
+  };
+  auto copy_unit = [&](int i, int u, int row, int col) __attribute__((always_inline)) {
+    const int64_t q0 = q_begin + (int64_t)i * BQ;
+    unsigned char* st = stage(i);
+    if (u < UNITS - 1) {
+      const int which = u >= 9, v9 = u - 9 * which;
+      int64_t q = q0 + row;
+      if (q > p.n_q - 1) q = p.n_q - 1;
+      const T* src = (which ? dog : qg) + q * D + col;
+      copy_to_lds16(src, __builtin_amdgcn_readfirstlane(lds_addr(st + which * TILEB + 1024 * v9)));
+    } else {
+      const unsigned base = __builtin_amdgcn_readfirstlane(lds_addr(st + 2 * TILEB));
+      if (lane < 32) copy_to_lds16((lane < 16 ? sinitg : dpinitg) + q0 + 4 * (lane & 15), base);
+    }
+  };
+  // Each wave's share of the copies of a tile: units wave + 8k (three for
+  // waves 0..2, two for the others), with the lane's row and column of each
+  // unit computed once.
+  constexpr int MAXU = (UNITS + NW - 1) / NW;
+  const int n_units = (UNITS - wave + NW - 1) / NW;
+  int urow[MAXU], ucol[MAXU];
+#pragma unroll
+  for (int k = 0; k < MAXU; ++k) {
+    const int u = wave + NW * k;
+    urow[k] = u < UNITS - 1 ? unit_row(u) : 0;
+    ucol[k] = u < UNITS - 1 ? unit_col(u) : 0;
+  }
+  auto issue = [&](int i) __attribute__((always_inline)) {
+    if (i < n_iters) {
+#pragma unroll
+      for (int k = 0; k < MAXU; ++k)
+        if (wave + NW * k < UNITS) copy_unit(i, wave + NW * k, urow[k], ucol[k]);
+    }
+  };
+  // Wait until this wave's copies of older tiles have landed; those of the
+  // tile issued last (`recent` says whether it exists) may still run.
+  auto wait_copies = [&](bool recent) __attribute__((always_inline)) {
+    if (!recent) wait_global_loads();
+    else if (n_units == 3) wait_global_loads_upto<3>();
+    else wait_global_loads_upto<2>();
+  };
+  auto barrier = [&]() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
+  };
+
+  // Copy schedule: group 1 issues its share of tile j in its VALU phase of
+  // tile j - 3, group 0 in its VALU phase of tile j - 2; each group waits for
+  // its share before the barrier that precedes group 0's first read of tile j
+  // (the end of group 1's MFMA phase, and of group 0's VALU phase, of tile
+  // j - 1).  A stage is overwritten only after group 1's MFMA phase of the
+  // tile four earlier, its last reader, has ended.
+  // Prologue: all waves copy tile 0; group 1 then issues its shares of tiles
+  // 1 and 2, group 0 its share of tile 1, and group 1 starts one phase behind.
+  if (n_iters > 0)
+    for (int u = wave; u < UNITS; u += NW) copy_unit(0, u, unit_row(u), unit_col(u));
+  wait_global_loads();
+  __syncthreads();
+  if (grp == 1) {
+    issue(1);
+    issue(2);
+    barrier();
+  } else {
+    issue(1);
+  }
+
+  const int qrow = perm32(c);
+  const float cl2 = p.scale_log2;
+  f32x16 s[QS], dp[QS];
+  Frag<T> pa[NQC], da[NQC];
+  // Whether any query of tile i sees any key of this wave (causal).
+  auto active = [&](int i) { return !CAUSAL || q_begin + (int64_t)i * BQ + BQ - 1 >= kw; };
+  // The MFMA phase issues each LDS fragment read two steps before its MFMA
+  // (scheduling fences between steps), so that a wave alone on the matrix pipe
+  // does not wait for LDS latency.
+  // dV += P^T dO and dK += dS^T Q for tile i (column fragments: k = queries).
+  auto dvdk = [&](int i) __attribute__((always_inline)) {
+    const unsigned char* st = stage(i);
+    const T* qs_t = reinterpret_cast<const T*>(st);
+    const T* dos_t = reinterpret_cast<const T*>(st + TILEB);
+    constexpr int NSTEP = NQC * NDT;
+    Frag<T> bo[3], bq[3];
+    auto fetch = [&](int step) __attribute__((always_inline)) {
+      const int qc = step / NDT, dt = step % NDT;
+      bo[step % 3] = lds_col_frag<T>(dos_t, RSB / 2, 16 * qc, 32 * dt, lane);
+      bq[step % 3] = lds_col_frag<T>(qs_t, RSB / 2, 16 * qc, 32 * dt, lane);
+    };
+    fetch(0);
+    fetch(1);
+#pragma unroll
+    for (int step = 0; step < NSTEP; ++step) {
+      if (step + 2 < NSTEP) fetch(step + 2);
+      const int qc = step / NDT, dt = step % NDT;
+      dv[dt] = mma(pa[qc], bo[step % 3], dv[dt]);
+      dk[dt] = mma(da[qc], bq[step % 3], dk[dt]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // S = Q K^T + s_init and dP = dO V^T + dp_init for tile i (row fragments).
+  auto sdp = [&](int i) __attribute__((always_inline)) {
+    const unsigned char* st = stage(i);
+    const T* qs_t = reinterpret_cast<const T*>(st);
+    const T* dos_t = reinterpret_cast<const T*>(st + TILEB);
+    const float* sinit_s = reinterpret_cast<const float*>(st + 2 * TILEB);
+    const float* dpinit_s = sinit_s + BQ;
+    constexpr int NSTEP = KC * QS;
+    Frag<T> fa[3], fg[3];
+    auto fetch = [&](int step) __attribute__((always_inline)) {
+      const int kc = step / QS, qs = step % QS;
+      fa[step % 3] = lds_frag<T>(qs_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
+      fg[step % 3] = lds_frag<T>(dos_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
+    };
+    fetch(0);
+    fetch(1);
+#pragma unroll
+    for (int qs = 0; qs < QS; ++qs)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = 32 * qs + 16 * (j >> 1) + 8 * h + 4 * (j & 1);
+        const f32x4 a = *reinterpret_cast<const f32x4*>(sinit_s + row);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(dpinit_s + row);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s[qs][4 * j + e] = a[e];
+          dp[qs][4 * j + e] = b[e];
+        }
+      }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int step = 0; step < NSTEP; ++step) {
+      if (step + 2 < NSTEP) fetch(step + 2);
+      const int kc = step / QS, qs = step % QS;
+      s[qs] = mma(fa[step % 3], kf[kc], s[qs]);
+      dp[qs] = mma(fg[step % 3], vf[kc], dp[qs]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  for (int i = 0; i < n_iters; ++i) {
+    const int64_t q0 = q_begin + (int64_t)i * BQ;
+    // ---- MFMA phase
+    if (i >= 1 && active(i - 1)) dvdk(i - 1);
+    if (active(i)) sdp(i);
+    // Group 1: tile i + 1 must land before this barrier (its share of tile
+    // i + 2 may still run).
+    if (grp == 1) wait_copies(i + 2 < n_iters);
+    barrier();
+    // ---- VALU phase
+    if (active(i)) {
+      const bool need_mask = CAUSAL && q0 < kw + 31;
+      const int key_rel = (int)(key - q0);  // key minus the tile's first query
+#pragma unroll
+      for (int qs = 0; qs < QS; ++qs)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pr = fast_exp2(s[qs][r] * cl2);
+          if (need_mask && key_rel > 32 * qs + permuted_row(r, h)) pr = 0.0f;
+          s[qs][r] = pr;
+          dp[qs][r] = pr * dp[qs][r];
+        }
+#pragma unroll
+      for (int qc = 0; qc < NQC; ++qc) {
+        float tp[8], td[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          tp[e] = s[qc >> 1][8 * (qc & 1) + e];
+          td[e] = dp[qc >> 1][8 * (qc & 1) + e];
+        }
+        pa[qc] = to_frag<T>(tp);
+        da[qc] = to_frag<T>(td);
+        keep_here(pa[qc]);  // the conversions belong to this phase
+        keep_here(da[qc]);
+      }
+    }
+    if (grp == 1) {
+      issue(i + 3);
+    } else {
+      // Group 0: its share of tile i + 2, then wait for tile i + 1.
+      issue(i + 2);
+      wait_copies(i + 2 < n_iters);
+    }
+    barrier();
+  }
+  // dV/dK of the last tile.
+  if (n_iters > 0 && active(n_iters - 1)) dvdk(n_iters - 1);
+  // Group 0 issued one barrier fewer (group 1's start delay): balance it so
+  // that no wave leaves while the other group still waits at a barrier.
+  if (grp == 0) barrier();
+
+  T* dkg = static_cast<T*>(p.dk) + (size_t)bh * p.n_k * D;
+  T* dvg = static_cast<T*>(p.dv) + (size_t)bh * p.n_k * D;
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t kr = kw + c_row(r, h);
+      if (kr < p.n_k) {
+        dkg[kr * D + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
+        dvg[kr * D + 32 * dt + c] = (T)dv[dt][r];
+      }
+    }
+}
+
 // ------------------------------------------------------------------- dQ
 template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
@@ -508,6 +802,11 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 // sub-tiles of 32 per wave and BK keys per stage; OCC = workgroups per CU the
 // register budget is sized for.  The d = 64 16-bit choices can be overridden
 // at build time for tuning sweeps.
+// 16-bit d = 64 dK/dV with 16-bit outputs: 1 selects the two-group kernel,
+// 0 the 4-wave kernel.
+#ifndef MEA_T64_DKDV_PP
+#define MEA_T64_DKDV_PP 1
+#endif
 #ifndef MEA_T64_DKDV_QS
 #define MEA_T64_DKDV_QS 2
 #endif
@@ -553,8 +852,14 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
   p.n_qtiles = (int)((p.n_q + 128 * S::QT - 1) / (128 * S::QT));
   if (p.dk) {
-    e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, S::QS, S::KV_OCC, CAUSAL>),
-                        dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
+    if constexpr (sizeof(T) == 2 && D == 64 && __is_same(T, TO) && MEA_T64_DKDV_PP) {
+      p.n_ktiles = (int)((p.n_k + kvpp::BKG - 1) / kvpp::BKG);
+      e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_pp_kernel<T, CAUSAL>),
+                          dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(kvpp::NW * 64), args, 0, stream);
+    } else {
+      e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, S::QS, S::KV_OCC, CAUSAL>),
+                          dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
+    }
     if (e != hipSuccess || !p.dq) return e;
   }
   const int dq_lds = 2 * 2 * S::BK * (D + 16 / (int)sizeof(T)) * (int)sizeof(T);

@@ -132,6 +132,14 @@ __device__ __forceinline__ void wait_global_loads_upto() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | N);
 }
 
+// Materialise v in registers at this point: an empty statement that takes v
+// as input, so that the computation of v cannot be sunk past what follows
+// (for example past a barrier into the next phase of a phase-split kernel).
+template <typename V>
+__device__ __forceinline__ void keep_here(const V& v) {
+  asm volatile("" ::"v"(v));
+}
+
 // LDS byte address of a pointer into shared memory (the low 32 bits of its
 // generic address).
 __device__ __forceinline__ unsigned lds_addr(const void* p) {
