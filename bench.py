@@ -177,9 +177,11 @@ def main() -> int:
                    "includes": "D preprocess; executes 6*d*P, credited 2*d*P"},
     }
     dom = max(("fwd", "bwd_dkdv"), key=lambda n_: kernels[n_]["ms"])
-    # 16-bit d = 64 forwards run the two-group kernel; other shapes the 4-wave one.
-    fwd_name = "attn_fwd_pp_kernel" if w.d == 64 else "attn_fwd_kernel"
-    dom_kernel_name = {"fwd": fwd_name, "bwd_dkdv": "attn_bwd_dkdv_kernel"}[dom]
+    # 16-bit d = 64 runs the two-group forward and dK/dV kernels; other shapes
+    # the 4-wave ones.
+    two_group = w.d == 64
+    dom_kernel_name = {"fwd": "attn_fwd_pp_kernel" if two_group else "attn_fwd_kernel",
+                       "bwd_dkdv": "attn_bwd_dkdv_pp_kernel" if two_group else "attn_bwd_dkdv_kernel"}[dom]
     achieved = kernels[dom]["tflops"]
     traffic = load_traffic(dom_kernel_name)
 

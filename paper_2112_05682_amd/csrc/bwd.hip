@@ -16,6 +16,15 @@
 #include "device.hpp"
 #include "kernels.hpp"
 
+// 16-bit d = 64 dK/dV with 16-bit outputs: 1 selects the two-group kernel,
+// 0 the 4-wave kernel; AHEAD is its LDS prefetch distance in steps.
+#ifndef MEA_T64_DKDV_PP
+#define MEA_T64_DKDV_PP 1
+#endif
+#ifndef MEA_T64_DKDV_AHEAD
+#define MEA_T64_DKDV_AHEAD 2
+#endif
+
 namespace mea {
 
 template <bool B> struct BoolC { static constexpr bool value = B; };
@@ -445,29 +454,31 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   Frag<T> pa[NQC], da[NQC];
   // Whether any query of tile i sees any key of this wave (causal).
   auto active = [&](int i) { return !CAUSAL || q_begin + (int64_t)i * BQ + BQ - 1 >= kw; };
-  // The MFMA phase issues each LDS fragment read two steps before its MFMA
-  // (scheduling fences between steps), so that a wave alone on the matrix pipe
-  // does not wait for LDS latency.
+  // The MFMA phase issues each LDS fragment read AHEAD steps (two MFMAs each)
+  // before its MFMAs (scheduling fences between steps), so that a wave alone
+  // on the matrix pipe does not wait for LDS latency.  The causal variant keeps
+  // a shorter distance for its larger register footprint.
+  constexpr int AHEAD = CAUSAL ? 2 : MEA_T64_DKDV_AHEAD;
   // dV += P^T dO and dK += dS^T Q for tile i (column fragments: k = queries).
   auto dvdk = [&](int i) __attribute__((always_inline)) {
     const unsigned char* st = stage(i);
     const T* qs_t = reinterpret_cast<const T*>(st);
     const T* dos_t = reinterpret_cast<const T*>(st + TILEB);
     constexpr int NSTEP = NQC * NDT;
-    Frag<T> bo[3], bq[3];
+    Frag<T> bo[AHEAD + 1], bq[AHEAD + 1];
     auto fetch = [&](int step) __attribute__((always_inline)) {
       const int qc = step / NDT, dt = step % NDT;
-      bo[step % 3] = lds_col_frag<T>(dos_t, RSB / 2, 16 * qc, 32 * dt, lane);
-      bq[step % 3] = lds_col_frag<T>(qs_t, RSB / 2, 16 * qc, 32 * dt, lane);
+      bo[step % (AHEAD + 1)] = lds_col_frag<T>(dos_t, RSB / 2, 16 * qc, 32 * dt, lane);
+      bq[step % (AHEAD + 1)] = lds_col_frag<T>(qs_t, RSB / 2, 16 * qc, 32 * dt, lane);
     };
-    fetch(0);
-    fetch(1);
+#pragma unroll
+    for (int step = 0; step < AHEAD; ++step) fetch(step);
 #pragma unroll
     for (int step = 0; step < NSTEP; ++step) {
-      if (step + 2 < NSTEP) fetch(step + 2);
+      if (step + AHEAD < NSTEP) fetch(step + AHEAD);
       const int qc = step / NDT, dt = step % NDT;
-      dv[dt] = mma(pa[qc], bo[step % 3], dv[dt]);
-      dk[dt] = mma(da[qc], bq[step % 3], dk[dt]);
+      dv[dt] = mma(pa[qc], bo[step % (AHEAD + 1)], dv[dt]);
+      dk[dt] = mma(da[qc], bq[step % (AHEAD + 1)], dk[dt]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -479,14 +490,14 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
     const float* sinit_s = reinterpret_cast<const float*>(st + 2 * TILEB);
     const float* dpinit_s = sinit_s + BQ;
     constexpr int NSTEP = KC * QS;
-    Frag<T> fa[3], fg[3];
+    Frag<T> fa[AHEAD + 1], fg[AHEAD + 1];
     auto fetch = [&](int step) __attribute__((always_inline)) {
       const int kc = step / QS, qs = step % QS;
-      fa[step % 3] = lds_frag<T>(qs_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
-      fg[step % 3] = lds_frag<T>(dos_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
+      fa[step % (AHEAD + 1)] = lds_frag<T>(qs_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
+      fg[step % (AHEAD + 1)] = lds_frag<T>(dos_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
     };
-    fetch(0);
-    fetch(1);
+#pragma unroll
+    for (int step = 0; step < AHEAD; ++step) fetch(step);
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
@@ -503,10 +514,10 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int step = 0; step < NSTEP; ++step) {
-      if (step + 2 < NSTEP) fetch(step + 2);
+      if (step + AHEAD < NSTEP) fetch(step + AHEAD);
       const int kc = step / QS, qs = step % QS;
-      s[qs] = mma(fa[step % 3], kf[kc], s[qs]);
-      dp[qs] = mma(fg[step % 3], vf[kc], dp[qs]);
+      s[qs] = mma(fa[step % (AHEAD + 1)], kf[kc], s[qs]);
+      dp[qs] = mma(fg[step % (AHEAD + 1)], vf[kc], dp[qs]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -802,11 +813,6 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 // sub-tiles of 32 per wave and BK keys per stage; OCC = workgroups per CU the
 // register budget is sized for.  The d = 64 16-bit choices can be overridden
 // at build time for tuning sweeps.
-// 16-bit d = 64 dK/dV with 16-bit outputs: 1 selects the two-group kernel,
-// 0 the 4-wave kernel.
-#ifndef MEA_T64_DKDV_PP
-#define MEA_T64_DKDV_PP 1
-#endif
 #ifndef MEA_T64_DKDV_QS
 #define MEA_T64_DKDV_QS 2
 #endif
