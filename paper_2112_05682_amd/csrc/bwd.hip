@@ -21,6 +21,9 @@
 #ifndef MEA_T64_DKDV_PP
 #define MEA_T64_DKDV_PP 1
 #endif
+#ifndef MEA_T64_DQ_PP
+#define MEA_T64_DQ_PP 1
+#endif
 #ifndef MEA_T64_DKDV_AHEAD
 #define MEA_T64_DKDV_AHEAD 2
 #endif
@@ -807,6 +810,270 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   }
 }
 
+// ------------------------------------------------------- dQ (two groups)
+// 16-bit inputs and outputs, d = 64.  Eight waves of 32 queries each (Q, dO
+// and the accumulator initial values in registers, dQ accumulated in
+// registers) in two groups of four that alternate an MFMA phase and a VALU
+// phase like the two-group dK/dV kernel.  MFMA phase of key tile j:
+// dQ^T += K^T dS^T for tile j - 1, then S^T = K Q^T and dP^T = V dO^T for
+// tile j.  VALU phase: P = 2^(c S), dS = P dP, rounded into the operands of
+// the next MFMA phase.  K and V stream through a four-stage LDS ring.
+namespace qpp {
+constexpr int D = 64, NW = 8, BQG = NW * 32, BK = 64, NKT = BK / 32, NSTAGE = 4;
+constexpr int RSB = 144;                 // bytes per LDS row (128 + 16 pad)
+constexpr int TILEB = BK * RSB;          // one K or V tile: 9 KiB
+constexpr int STAGEB = 2 * TILEB;
+constexpr int UNITS = 2 * TILEB / 1024;  // 1 KiB copies per stage (18)
+static_assert(TILEB % 1024 == 0, "stage layout");
+}  // namespace qpp
+
+template <typename T, bool CAUSAL>
+__global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
+  using namespace qpp;
+  static_assert(sizeof(T) == 2, "16-bit inputs only");
+  constexpr int KC = D / 16, NDT = D / 32, NPC = BK / 16;
+  __shared__ __align__(16) unsigned char smem[NSTAGE * STAGEB];
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;
+  const int lane = tid & 63;
+  const int h = lane >> 5, c = lane & 31;
+
+  const int w = xcd_remap(blockIdx.x, gridDim.x);
+  const int qt_idx = w % p.n_qtiles;
+  const int bh = w / p.n_qtiles;
+  const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;  // heaviest first
+  const int64_t q0 = (int64_t)qtile * BQG;
+  const int64_t qw = q0 + 32 * wave;  // first query of this wave
+  const int64_t query = qw + c;
+
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+
+  // Q^T and dO^T as B operands: lane (h, query c), k = 16 kc + 8 h + s.
+  Frag<T> qf[KC], gf[KC];
+  const bool valid = query < p.n_q;
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (valid) {
+      qf[kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
+      gf[kc] = *reinterpret_cast<const Frag<T>*>(dog + query * D + 16 * kc + 8 * h);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        qf[kc][e] = (T)0.0f;
+        gf[kc][e] = (T)0.0f;
+      }
+    }
+  }
+  const float s_init = valid ? p.s_init[(size_t)bh * p.n_q_pad + query] : -INFINITY;
+  const float dp_init = valid ? p.dp_init[(size_t)bh * p.n_q_pad + query] : 0.0f;
+  wait_global_loads();
+
+  f32x16 acc[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[dt][r] = 0.0f;
+
+  // Keys after the workgroup's last query are invisible to all of it (causal).
+  int64_t ke = p.n_k;
+  if (CAUSAL && ke > q0 + BQG) ke = q0 + BQG;
+  const int n_tiles = (int)((ke + BK - 1) / BK);
+  auto stage = [&](int j) { return smem + (j % NSTAGE) * STAGEB; };
+
+  // Copy unit u (0 <= u < UNITS) of key tile j: units 0..8 are the K tile,
+  // 9..17 the V tile (lane slot s = 64 (u % 9) + lane is row s / 9, 16-byte
+  // chunk s % 9; chunk 8 is the row pad and gets a copy of chunk 7).  Rows past
+  // n_k repeat the last key (finite values; masked).
+  auto unit_row = [&](int u) { return (64 * (u % 9) + lane) / 9; };
+  auto unit_col = [&](int u) {
+    const int ch = (64 * (u % 9) + lane) % 9;
+    return 8 * (ch < 8 ? ch : 7);
+  };
+  auto copy_unit = [&](int j, int u, int row, int col) __attribute__((always_inline)) {
+    const int which = u >= 9, v9 = u - 9 * which;
+    int64_t key = (int64_t)j * BK + row;
+    if (key > p.n_k - 1) key = p.n_k - 1;
+    const T* src = (which ? vg : kg) + key * D + col;
+    copy_to_lds16(src, __builtin_amdgcn_readfirstlane(lds_addr(stage(j) + which * TILEB + 1024 * v9)));
+  };
+  constexpr int MAXU = (UNITS + NW - 1) / NW;
+  const int n_units = (UNITS - wave + NW - 1) / NW;
+  int urow[MAXU], ucol[MAXU];
+#pragma unroll
+  for (int k = 0; k < MAXU; ++k) {
+    const int u = wave + NW * k;
+    urow[k] = u < UNITS ? unit_row(u) : 0;
+    ucol[k] = u < UNITS ? unit_col(u) : 0;
+  }
+  auto issue = [&](int j) __attribute__((always_inline)) {
+    if (j < n_tiles) {
+#pragma unroll
+      for (int k = 0; k < MAXU; ++k)
+        if (wave + NW * k < UNITS) copy_unit(j, wave + NW * k, urow[k], ucol[k]);
+    }
+  };
+  auto wait_copies = [&](bool recent) __attribute__((always_inline)) {
+    if (!recent) wait_global_loads();
+    else if (n_units == 3) wait_global_loads_upto<3>();
+    else wait_global_loads_upto<2>();
+  };
+  auto barrier = [&]() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" ::: "memory");
+  };
+
+  // Copy schedule as in the two-group dK/dV kernel: group 1 issues its share
+  // of tile j in its VALU phase of tile j - 3, group 0 in its VALU phase of
+  // tile j - 2; both wait for tile j before the barrier that precedes group
+  // 0's MFMA phase of tile j.
+  if (n_tiles > 0)
+    for (int u = wave; u < UNITS; u += NW) copy_unit(0, u, unit_row(u), unit_col(u));
+  wait_global_loads();
+  __syncthreads();
+  if (grp == 1) {
+    issue(1);
+    issue(2);
+    barrier();
+  } else {
+    issue(1);
+  }
+
+  const int krow = perm32(c);
+  const float cl2 = p.scale_log2;
+  f32x16 s[NKT], dp[NKT];
+  Frag<T> dsf[NPC];
+  // Whether any key of tile j is visible to any query of this wave (causal).
+  auto active = [&](int j) { return !CAUSAL || (int64_t)j * BK <= qw + 31; };
+  // Whether tile j needs the elementwise mask (ragged keys, causal diagonal).
+  auto masked = [&](int j) {
+    const int64_t k0 = (int64_t)j * BK;
+    return k0 + BK > p.n_k || (CAUSAL && k0 + BK - 1 > qw);
+  };
+  constexpr int AHEAD = 2;
+  // dQ^T += K^T dS^T for tile j (column fragments of K: k = keys).
+  auto dq_mma = [&](int j) __attribute__((always_inline)) {
+    const T* ks = reinterpret_cast<const T*>(stage(j));
+    constexpr int NSTEP = NPC;
+    Frag<T> ka[2][AHEAD + 1];
+    auto fetch = [&](int step) __attribute__((always_inline)) {
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+        ka[dt][step % (AHEAD + 1)] = lds_col_frag<T>(ks, RSB / 2, 16 * step, 32 * dt, lane);
+    };
+#pragma unroll
+    for (int step = 0; step < AHEAD; ++step) fetch(step);
+#pragma unroll
+    for (int step = 0; step < NSTEP; ++step) {
+      if (step + AHEAD < NSTEP) fetch(step + AHEAD);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) acc[dt] = mma(ka[dt][step % (AHEAD + 1)], dsf[step], acc[dt]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // S^T = K Q^T + s_init and dP^T = V dO^T + dp_init for tile j (row fragments).
+  auto sdp = [&](int j) __attribute__((always_inline)) {
+    const T* ks = reinterpret_cast<const T*>(stage(j));
+    const T* vs = reinterpret_cast<const T*>(stage(j) + TILEB);
+    constexpr int NSTEP = KC * NKT;
+    Frag<T> fa[AHEAD + 1], fb[AHEAD + 1];
+    auto fetch = [&](int step) __attribute__((always_inline)) {
+      const int kc = step / NKT, kt = step % NKT;
+      fa[step % (AHEAD + 1)] = lds_frag<T>(ks + (32 * kt + krow) * (RSB / 2) + 16 * kc + 8 * h);
+      fb[step % (AHEAD + 1)] = lds_frag<T>(vs + (32 * kt + krow) * (RSB / 2) + 16 * kc + 8 * h);
+    };
+#pragma unroll
+    for (int step = 0; step < AHEAD; ++step) fetch(step);
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[kt][r] = s_init;
+        dp[kt][r] = dp_init;
+      }
+#pragma unroll
+    for (int step = 0; step < NSTEP; ++step) {
+      if (step + AHEAD < NSTEP) fetch(step + AHEAD);
+      const int kc = step / NKT, kt = step % NKT;
+      s[kt] = mma(fa[step % (AHEAD + 1)], qf[kc], s[kt]);
+      dp[kt] = mma(fb[step % (AHEAD + 1)], gf[kc], dp[kt]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // P = 2^(c S), dS = P dP for tile j into the dS^T operands.
+  auto pds = [&](auto mask_tag, int j) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const int64_t k0 = (int64_t)j * BK;
+    int lim = BK;
+    if constexpr (MASK) {
+      // key k0 + x is valid iff x < key_lim and, causal, x <= query - k0.
+      lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+      if (CAUSAL) {
+        const int64_t qr = query - k0 + 1;
+        if (qr < lim) lim = qr > 0 ? (int)qr : 0;
+      }
+    }
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float pr = fast_exp2(s[kt][r] * cl2);
+        if (MASK && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
+        dp[kt][r] = pr * dp[kt][r];
+      }
+#pragma unroll
+    for (int pc = 0; pc < NPC; ++pc) {
+      float td[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) td[e] = dp[pc >> 1][8 * (pc & 1) + e];
+      dsf[pc] = to_frag<T>(td);
+      keep_here(dsf[pc]);  // the conversions belong to this phase
+    }
+  };
+
+  for (int j = 0; j < n_tiles; ++j) {
+    // ---- MFMA phase
+    if (j >= 1 && active(j - 1)) dq_mma(j - 1);
+    if (active(j)) sdp(j);
+    if (grp == 1) wait_copies(j + 2 < n_tiles);
+    barrier();
+    // ---- VALU phase
+    if (active(j)) {
+      if (masked(j)) pds(BoolC<true>{}, j);
+      else pds(BoolC<false>{}, j);
+    }
+    if (grp == 1) {
+      issue(j + 3);
+    } else {
+      issue(j + 2);
+      wait_copies(j + 2 < n_tiles);
+    }
+    barrier();
+  }
+  if (n_tiles > 0 && active(n_tiles - 1)) dq_mma(n_tiles - 1);
+  if (grp == 0) barrier();  // group 1's start delay, balanced
+
+  if (valid) {
+    T* dqg = static_cast<T*>(p.dq) + ((size_t)bh * p.n_q + query) * D;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        typename FragT<T>::half v4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v4[e] = (T)(acc[dt][4 * a4 + e] * p.scale);
+        *reinterpret_cast<typename FragT<T>::half*>(dqg + 32 * dt + 8 * a4 + 4 * h) = v4;
+      }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 
 // Tile choices.  dK/dV: QS query sub-tiles of 32 per stage; dQ: QT query
@@ -867,6 +1134,11 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
                           dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
     }
     if (e != hipSuccess || !p.dq) return e;
+  }
+  if constexpr (sizeof(T) == 2 && D == 64 && __is_same(T, TO) && MEA_T64_DQ_PP) {
+    p.n_qtiles = (int)((p.n_q + qpp::BQG - 1) / qpp::BQG);
+    return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_pp_kernel<T, CAUSAL>),
+                           dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(qpp::NW * 64), args, 0, stream);
   }
   const int dq_lds = 2 * 2 * S::BK * (D + 16 / (int)sizeof(T)) * (int)sizeof(T);
   return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, S::QT, S::BK, S::Q_OCC, CAUSAL>),
