@@ -335,6 +335,9 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 // row-fragment reads of K and the transposing reads of V free of bank
 // conflicts.
 // ---------------------------------------------------------------------------
+#ifndef MEA_FWD_PP_W0
+#define MEA_FWD_PP_W0 2
+#endif
 namespace pp {
 constexpr int D = 64, QT = 2, BK = 64, NW = 8, BQ = NW * QT * 32, NSTAGE = 3;
 constexpr int ROWB = D * 2;          // bytes per LDS row (unpadded)
@@ -348,6 +351,10 @@ template <typename T, typename TO, bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   using namespace pp;
   constexpr int KC = D / 16, NKT = BK / 32, NPC = BK / 16, NDT = D / 32;
+  // 16-key chunks of query sub-tile 0 whose weights are computed in the MFMA
+  // phase (interleaved with the PV MFMAs); the rest go to the softmax phase.
+  constexpr int W0 = MEA_FWD_PP_W0;
+  static_assert(W0 >= 0 && W0 <= NPC, "weight chunks");
   static_assert(sizeof(T) == 2, "16-bit inputs only");
 
   // Three stages each of K and V: tile j of K lives in kst[j % 3], of V in
@@ -504,12 +511,12 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
       for (int r = 0; r < 16; ++r)
         if (32 * kt + permuted_row(r, h) >= lim) s[kt][t][r] = -INFINITY;
   };
-  auto weights = [&](auto t_tag, f32x16 (&s)[NKT][QT], Frag<T> (&pfo)[QT][NPC], float neg)
+  auto weights = [&](auto t_tag, f32x16 (&s)[NKT][QT], Frag<T> (&pfo)[QT][NPC], float neg, int pc0 = 0)
                      __attribute__((always_inline)) {
     constexpr int t = decltype(t_tag)::value;
     float sum0 = 0.0f, sum1 = 0.0f;
 #pragma unroll
-    for (int pc = 0; pc < NPC; ++pc) {
+    for (int pc = pc0; pc < NPC; ++pc) {
       float e8[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg));
@@ -573,16 +580,23 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
     for (int i = 0; i < NSTEP; ++i) {
       const int dt = i / NPC, pcv = i % NPC;
       if (i + 1 < NSTEP) vf[(i + 1) & 1] = vfrag(i + 1);
-      const int pcs = i >> 1, half = i & 1;
+      // Step i does half of chunk pcs of the weights; with W0 < NPC chunks
+      // here, the steps are spread evenly over the PV MFMAs.
+      constexpr int WSTEPS = 2 * W0;
+      const int wi = (i * WSTEPS) / NSTEP;
+      const bool has_w = WSTEPS > 0 && (i * WSTEPS) % NSTEP < WSTEPS;
+      const int pcs = wi >> 1, half = wi & 1;
       acc[0][dt] = mma(vf[i & 1], pf_old[0][pcv], acc[0][dt]);
-      float e4[4];
+      if (has_w) {
+        float e4[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        e4[e] = fast_exp2(fmaf(s[pcs >> 1][0][8 * (pcs & 1) + 4 * half + e], cl2, neg));
-      packed[2 * half] = pack2<T>(e4[0], e4[1]);
-      packed[2 * half + 1] = pack2<T>(e4[2], e4[3]);
+        for (int e = 0; e < 4; ++e)
+          e4[e] = fast_exp2(fmaf(s[pcs >> 1][0][8 * (pcs & 1) + 4 * half + e], cl2, neg));
+        packed[2 * half] = pack2<T>(e4[0], e4[1]);
+        packed[2 * half + 1] = pack2<T>(e4[2], e4[3]);
+      }
       acc[1][dt] = mma(vf[i & 1], pf_old[1][pcv], acc[1][dt]);
-      if (half) {
+      if (has_w && half) {
         pf_new[0][pcs] = __builtin_bit_cast(Frag<T>, packed);
         if (pcs & 1) sum1 = frag_sum(pf_new[0][pcs], nullptr, sum1);
         else sum0 = frag_sum(pf_new[0][pcs], nullptr, sum0);
@@ -664,13 +678,15 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
     constexpr bool MASK = decltype(mask_tag)::value;
     scores(kcur, s);
     if constexpr (MASK) mask_sub(j, IntC<0>{}, s);
-    finish_sub(IntC<0>{}, s, pf_new, pv_weights0(vprev, pf_old, pf_new, s, -m_ref[0]));
+    const float tsum0 = pv_weights0(vprev, pf_old, pf_new, s, -m_ref[0]);
+    if constexpr (W0 == NPC) finish_sub(IntC<0>{}, s, pf_new, tsum0);
     // Only group 1 has copies in flight (two per wave per tile); the wait is
     // a no-op for group 0.
     if (j + 2 < n_tiles) wait_global_loads_upto<4>();
     else if (j + 1 < n_tiles) wait_global_loads_upto<2>();
     else wait_global_loads();
     barrier();
+    if constexpr (W0 < NPC) finish_sub(IntC<0>{}, s, pf_new, tsum0 + weights(IntC<0>{}, s, pf_new, -m_ref[0], W0));
     if constexpr (MASK) mask_sub(j, IntC<1>{}, s);
     finish_sub(IntC<1>{}, s, pf_new, weights(IntC<1>{}, s, pf_new, -m_ref[1]));
     if (grp == 1) issue(j);
