@@ -378,42 +378,49 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // chunk 7), unit 18 the initial values (lanes 0..15 s_init, 16..31 dp_init;
   // the padded arrays hold every row of the tile).  Query rows past n_q repeat
   // the last row (finite values; their weights are 0).
-  auto unit_row = [&](int u) { return (64 * (u % 9) + lane) / 9; };
-  auto unit_col = [&](int u) {
-    const int ch = (64 * (u % 9) + lane) % 9;
-    return 8 * (ch < 8 ? ch : 7);
+  constexpr int ROWB = D * (int)sizeof(T);
+  const int n_full = n_iters > 0 ? (int)((p.n_q - q_begin) / BQ) : 0;  // tiles with no row past n_q
+  auto unit_off = [&](int u) {
+    const int slot = 64 * (u % 9) + lane;
+    const int ch = slot % 9;
+    return (unsigned)((slot / 9) * ROWB + 16 * (ch < 8 ? ch : 7));
   };
-  auto copy_unit = [&](int i, int u, int row, int col) __attribute__((always_inline)) {
+  auto copy_unit = [&](int i, int u, unsigned off) __attribute__((always_inline)) {
     const int64_t q0 = q_begin + (int64_t)i * BQ;
     unsigned char* st = stage(i);
     if (u < UNITS - 1) {
       const int which = u >= 9, v9 = u - 9 * which;
-      int64_t q = q0 + row;
-      if (q > p.n_q - 1) q = p.n_q - 1;
-      const T* src = (which ? dog : qg) + q * D + col;
-      copy_to_lds16(src, __builtin_amdgcn_readfirstlane(lds_addr(st + which * TILEB + 1024 * v9)));
+      const T* g = which ? dog : qg;
+      const unsigned lds = __builtin_amdgcn_readfirstlane(lds_addr(st + which * TILEB + 1024 * v9));
+      if (i < n_full) {
+        copy_to_lds16_sb(g + q0 * D, off, lds);
+      } else {
+        int64_t q = q0 + off / ROWB;
+        if (q > p.n_q - 1) q = p.n_q - 1;
+        copy_to_lds16(reinterpret_cast<const unsigned char*>(g + q * D) + off % ROWB, lds);
+      }
     } else {
       const unsigned base = __builtin_amdgcn_readfirstlane(lds_addr(st + 2 * TILEB));
       if (lane < 32) copy_to_lds16((lane < 16 ? sinitg : dpinitg) + q0 + 4 * (lane & 15), base);
     }
   };
   // Each wave's share of the copies of a tile: units wave + 8k (three for
-  // waves 0..2, two for the others), with the lane's row and column of each
-  // unit computed once.
+  // waves 0..2, two for the others), with the lane's byte offset within the
+  // tile of each unit computed once (a tile that ends past n_q takes the
+  // clamped path).
   constexpr int MAXU = (UNITS + NW - 1) / NW;
   const int n_units = (UNITS - wave + NW - 1) / NW;
-  int urow[MAXU], ucol[MAXU];
+  unsigned uoff[MAXU];
 #pragma unroll
   for (int k = 0; k < MAXU; ++k) {
     const int u = wave + NW * k;
-    urow[k] = u < UNITS - 1 ? unit_row(u) : 0;
-    ucol[k] = u < UNITS - 1 ? unit_col(u) : 0;
+    uoff[k] = u < UNITS - 1 ? unit_off(u) : 0u;
   }
   auto issue = [&](int i) __attribute__((always_inline)) {
     if (i < n_iters) {
 #pragma unroll
       for (int k = 0; k < MAXU; ++k)
-        if (wave + NW * k < UNITS) copy_unit(i, wave + NW * k, urow[k], ucol[k]);
+        if (wave + NW * k < UNITS) copy_unit(i, wave + NW * k, uoff[k]);
     }
   };
   // Wait until this wave's copies of older tiles have landed; those of the
@@ -440,7 +447,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // Prologue: all waves copy tile 0; group 1 then issues its shares of tiles
   // 1 and 2, group 0 its share of tile 1, and group 1 starts one phase behind.
   if (n_iters > 0)
-    for (int u = wave; u < UNITS; u += NW) copy_unit(0, u, unit_row(u), unit_col(u));
+    for (int u = wave; u < UNITS; u += NW) copy_unit(0, u, u < UNITS - 1 ? unit_off(u) : 0u);
   wait_global_loads();
   __syncthreads();
   if (grp == 1) {
@@ -887,34 +894,43 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
 
   // Copy unit u (0 <= u < UNITS) of key tile j: units 0..8 are the K tile,
   // 9..17 the V tile (lane slot s = 64 (u % 9) + lane is row s / 9, 16-byte
-  // chunk s % 9; chunk 8 is the row pad and gets a copy of chunk 7).  Rows past
-  // n_k repeat the last key (finite values; masked).
-  auto unit_row = [&](int u) { return (64 * (u % 9) + lane) / 9; };
-  auto unit_col = [&](int u) {
-    const int ch = (64 * (u % 9) + lane) % 9;
-    return 8 * (ch < 8 ? ch : 7);
+  // chunk s % 9; chunk 8 is the row pad and gets a copy of chunk 7).  The
+  // lane's byte offset within a tile is computed once per unit; a tile that
+  // ends past n_k takes the clamped path, whose rows past n_k repeat the last
+  // key (finite values; masked).
+  constexpr int ROWB = D * (int)sizeof(T);
+  const int n_full = (int)(p.n_k / BK);  // tiles with no key past n_k
+  auto unit_off = [&](int u) {
+    const int slot = 64 * (u % 9) + lane;
+    const int ch = slot % 9;
+    return (unsigned)((slot / 9) * ROWB + 16 * (ch < 8 ? ch : 7));
   };
-  auto copy_unit = [&](int j, int u, int row, int col) __attribute__((always_inline)) {
+  auto copy_unit = [&](int j, int u, unsigned off) __attribute__((always_inline)) {
     const int which = u >= 9, v9 = u - 9 * which;
-    int64_t key = (int64_t)j * BK + row;
-    if (key > p.n_k - 1) key = p.n_k - 1;
-    const T* src = (which ? vg : kg) + key * D + col;
-    copy_to_lds16(src, __builtin_amdgcn_readfirstlane(lds_addr(stage(j) + which * TILEB + 1024 * v9)));
+    const T* g = which ? vg : kg;
+    const unsigned lds = __builtin_amdgcn_readfirstlane(lds_addr(stage(j) + which * TILEB + 1024 * v9));
+    const int64_t k0 = (int64_t)j * BK;
+    if (j < n_full) {
+      copy_to_lds16_sb(g + k0 * D, off, lds);
+    } else {
+      int64_t key = k0 + off / ROWB;
+      if (key > p.n_k - 1) key = p.n_k - 1;
+      copy_to_lds16(reinterpret_cast<const unsigned char*>(g + key * D) + off % ROWB, lds);
+    }
   };
   constexpr int MAXU = (UNITS + NW - 1) / NW;
   const int n_units = (UNITS - wave + NW - 1) / NW;
-  int urow[MAXU], ucol[MAXU];
+  unsigned uoff[MAXU];
 #pragma unroll
   for (int k = 0; k < MAXU; ++k) {
     const int u = wave + NW * k;
-    urow[k] = u < UNITS ? unit_row(u) : 0;
-    ucol[k] = u < UNITS ? unit_col(u) : 0;
+    uoff[k] = u < UNITS ? unit_off(u) : 0u;
   }
   auto issue = [&](int j) __attribute__((always_inline)) {
     if (j < n_tiles) {
 #pragma unroll
       for (int k = 0; k < MAXU; ++k)
-        if (wave + NW * k < UNITS) copy_unit(j, wave + NW * k, urow[k], ucol[k]);
+        if (wave + NW * k < UNITS) copy_unit(j, wave + NW * k, uoff[k]);
     }
   };
   auto wait_copies = [&](bool recent) __attribute__((always_inline)) {
@@ -935,7 +951,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   // tile j - 2; both wait for tile j before the barrier that precedes group
   // 0's MFMA phase of tile j.
   if (n_tiles > 0)
-    for (int u = wave; u < UNITS; u += NW) copy_unit(0, u, unit_row(u), unit_col(u));
+    for (int u = wave; u < UNITS; u += NW) copy_unit(0, u, unit_off(u));
   wait_global_loads();
   __syncthreads();
   if (grp == 1) {

@@ -160,6 +160,21 @@ __device__ __forceinline__ void copy_to_lds16(const void* src, unsigned lds_base
                : "v"(src), "s"(lds_base)
                : "memory", "m0");
 }
+// The same copy with a wave-uniform base address in SGPRs and a per-lane
+// 32-bit byte offset (lane l reads base + voff_l): a tile's copies then cost
+// no vector instructions beyond the offsets computed once.
+__device__ __forceinline__ void copy_to_lds16_sb(const void* base, unsigned voff, unsigned lds_base) {
+  // readfirstlane returns int: widen each half as unsigned (a sign-extended
+  // low half would corrupt the high half).
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const unsigned hi = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<unsigned>(b >> 32)));
+  const unsigned lo = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<unsigned>(b)));
+  const uint64_t sb = (static_cast<uint64_t>(hi) << 32) | static_cast<uint64_t>(lo);
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sb), "s"(lds_base)
+               : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
 // Convert eight float32 values to a fragment of T (round to nearest even).

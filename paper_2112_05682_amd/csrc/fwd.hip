@@ -645,18 +645,19 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   // Group 1 issues two waves of copies ahead, as if from softmax phases -2
   // and -1, and starts one phase behind group 0.  Its wave w copies units
   // w - 4 and w (rows 8u .. 8u + 7) of each tile; the lane's source offsets
-  // within a tile are computed once.
+  // within a tile (bytes) are computed once.
   const int urow0 = 8 * (wave - 4) + (lane >> 3), urow1 = urow0 + 32;
-  const int uk0 = urow0 * D + 8 * ((lane & 7) ^ swz_k(urow0));
-  const int uk1 = urow1 * D + 8 * ((lane & 7) ^ swz_k(urow1));
-  const int uv0 = urow0 * D + 8 * ((lane & 7) ^ swz_v(urow0));
-  const int uv1 = urow1 * D + 8 * ((lane & 7) ^ swz_v(urow1));
-  auto copy_tile = [&](const T* g, int j, unsigned char* stage, int off0, int off1) __attribute__((always_inline)) {
+  constexpr unsigned E = sizeof(T);
+  const unsigned uk0 = E * (urow0 * D + 8 * ((lane & 7) ^ swz_k(urow0)));
+  const unsigned uk1 = E * (urow1 * D + 8 * ((lane & 7) ^ swz_k(urow1)));
+  const unsigned uv0 = E * (urow0 * D + 8 * ((lane & 7) ^ swz_v(urow0)));
+  const unsigned uv1 = E * (urow1 * D + 8 * ((lane & 7) ^ swz_v(urow1)));
+  auto copy_tile = [&](const T* g, int j, unsigned char* stage, unsigned off0, unsigned off1) __attribute__((always_inline)) {
     const int64_t k0 = kb + (int64_t)j * BK;
     const unsigned base = __builtin_amdgcn_readfirstlane(lds_addr(stage) + (wave - 4) * 1024);
     if (k0 + BK <= p.n_k) {
-      copy_to_lds16(g + k0 * D + off0, base);
-      copy_to_lds16(g + k0 * D + off1, base + 4096);
+      copy_to_lds16_sb(g + k0 * D, off0, base);
+      copy_to_lds16_sb(g + k0 * D, off1, base + 4096);
     } else {
       load_tile(g, k0, stage, g == vg, wave - 4, 4);
     }
