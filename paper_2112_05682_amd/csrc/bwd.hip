@@ -535,6 +535,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   for (int i = 0; i < n_iters; ++i) {
     const int64_t q0 = q_begin + (int64_t)i * BQ;
     // ---- MFMA phase
+    mfma_phase_priority();
     if (i >= 1 && active(i - 1)) dvdk(i - 1);
     if (active(i)) sdp(i);
     // Group 1: tile i + 1 must land before this barrier (its share of tile
@@ -542,6 +543,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
     if (grp == 1) wait_copies(i + 2 < n_iters);
     barrier();
     // ---- VALU phase
+    valu_phase_priority();
     if (active(i)) {
       const bool need_mask = CAUSAL && q0 < kw + 31;
       const int key_rel = (int)(key - q0);  // key minus the tile's first query
@@ -1056,11 +1058,13 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
 
   for (int j = 0; j < n_tiles; ++j) {
     // ---- MFMA phase
+    mfma_phase_priority();
     if (j >= 1 && active(j - 1)) dq_mma(j - 1);
     if (active(j)) sdp(j);
     if (grp == 1) wait_copies(j + 2 < n_tiles);
     barrier();
     // ---- VALU phase
+    valu_phase_priority();
     if (active(j)) {
       if (masked(j)) pds(BoolC<true>{}, j);
       else pds(BoolC<false>{}, j);

@@ -140,6 +140,20 @@ __device__ __forceinline__ void keep_here(const V& v) {
   asm volatile("" ::"v"(v));
 }
 
+// Wave issue priority for the phase-split kernels: the wave in its MFMA phase
+// is raised above the wave in its softmax phase on the same SIMD, so that the
+// arbiter, which otherwise favours the older wave, issues each MFMA as soon as
+// the matrix pipe can take it and the softmax wave fills the remaining slots.
+#ifndef MEA_PP_PRIO
+#define MEA_PP_PRIO 1
+#endif
+__device__ __forceinline__ void mfma_phase_priority() {
+  if (MEA_PP_PRIO) __builtin_amdgcn_s_setprio(MEA_PP_PRIO);
+}
+__device__ __forceinline__ void valu_phase_priority() {
+  if (MEA_PP_PRIO) __builtin_amdgcn_s_setprio(0);
+}
+
 // LDS byte address of a pointer into shared memory (the low 32 bits of its
 // generic address).
 __device__ __forceinline__ unsigned lds_addr(const void* p) {

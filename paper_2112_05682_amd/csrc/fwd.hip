@@ -677,6 +677,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
     const unsigned char* kcur = kstage(j);
     const unsigned char* vprev = vstage(j + NSTAGE - 1);
     constexpr bool MASK = decltype(mask_tag)::value;
+    mfma_phase_priority();
     scores(kcur, s);
     if constexpr (MASK) mask_sub(j, IntC<0>{}, s);
     const float tsum0 = pv_weights0(vprev, pf_old, pf_new, s, -m_ref[0]);
@@ -687,6 +688,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
     else if (j + 1 < n_tiles) wait_global_loads_upto<2>();
     else wait_global_loads();
     barrier();
+    valu_phase_priority();
     if constexpr (W0 < NPC) finish_sub(IntC<0>{}, s, pf_new, tsum0 + weights(IntC<0>{}, s, pf_new, -m_ref[0], W0));
     if constexpr (MASK) mask_sub(j, IntC<1>{}, s);
     finish_sub(IntC<1>{}, s, pf_new, weights(IntC<1>{}, s, pf_new, -m_ref[1]));
