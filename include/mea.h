@@ -84,10 +84,11 @@ typedef struct {
  * Section 4 rescales and adds.  Returns MEA_OK or a validation error. */
 mea_status mea_attention_fwd_workspace_size(const mea_problem* p, size_t* bytes);
 
-/* Bytes of device workspace mea_attention_bwd needs for `p`: two per-row
- * float32 arrays of B*H*ceil(n_q/64)*64 entries each, holding -lse/scale and
- * -D_i with D_i = sum_t dO_it O_it (Section 5.2's recompute needs only these
- * and the inputs), O(n) like the lse. */
+/* Bytes of device workspace mea_attention_bwd needs for `p`: per padded row
+ * (B*H*ceil(n_q/64)*64 rows) the values -lse/scale and -D_i with
+ * D_i = sum_t dO_it O_it (Section 5.2's recompute needs only these and the
+ * inputs), O(n) like the lse: 16 bytes per row for 16-bit inputs and outputs
+ * at d = 64 (each value as three bf16 parts), else two float32 values. */
 mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes);
 
 /* Forward (Sections 2-4): o = softmax(scale * q k^T) v, computed tile by

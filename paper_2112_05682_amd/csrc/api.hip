@@ -98,15 +98,20 @@ FwdPlan plan_fwd(const mea_problem* p) {
 
 int64_t bwd_row_pad(int64_t n_q) { return (n_q + mea::kBwdRowPad - 1) / mea::kBwdRowPad * mea::kBwdRowPad; }
 
-// Bytes of one per-row backward array, rounded to 256.
-size_t bwd_row_array_bytes(const mea_problem* p) {
-  const size_t b = (size_t)p->batch * (size_t)p->heads * (size_t)bwd_row_pad(p->n_q) * 4;
+// Bytes of one per-row backward array of `elem` bytes per row, rounded to 256.
+size_t bwd_row_array_bytes(const mea_problem* p, size_t elem) {
+  const size_t b = (size_t)p->batch * (size_t)p->heads * (size_t)bwd_row_pad(p->n_q) * elem;
   return (b + 255) / 256 * 256;
 }
 
+bool bwd_records(const mea_problem* p) {
+  return mea::bwd_uses_row_records((int)p->dtype, (int)p->d, p->dtype != MEA_F32 && p->out_f32 != 0);
+}
+
 size_t bwd_workspace(const mea_problem* p) {
-  // s_init and dp_init, [B*H, n_q_pad] float32 each, 256-byte aligned.
-  return 2 * bwd_row_array_bytes(p) + 256;
+  // One 16-byte record per padded row (two-group kernels), or s_init and
+  // dp_init as [B*H, n_q_pad] float32 arrays; 256-byte aligned.
+  return (bwd_records(p) ? bwd_row_array_bytes(p, 16) : 2 * bwd_row_array_bytes(p, 4)) + 256;
 }
 
 float* align256(void* base, size_t off) {
@@ -213,8 +218,12 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   bp.dk = dk;
   bp.dv = dv;
   bp.n_q_pad = bwd_row_pad(p->n_q);
-  bp.s_init = align256(workspace, 0);
-  bp.dp_init = bp.s_init + bwd_row_array_bytes(p) / 4;
+  if (bwd_records(p)) {
+    bp.row_rec = reinterpret_cast<uint4*>(align256(workspace, 0));
+  } else {
+    bp.s_init = align256(workspace, 0);
+    bp.dp_init = bp.s_init + bwd_row_array_bytes(p, 4) / 4;
+  }
   bp.n_q = p->n_q;
   bp.n_k = p->n_k;
   bp.bh = (int)(p->batch * p->heads);

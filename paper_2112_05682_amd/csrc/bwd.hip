@@ -16,13 +16,9 @@
 #include "device.hpp"
 #include "kernels.hpp"
 
-// 16-bit d = 64 dK/dV with 16-bit outputs: 1 selects the two-group kernel,
-// 0 the 4-wave kernel; AHEAD is its LDS prefetch distance in steps.
-#ifndef MEA_T64_DKDV_PP
-#define MEA_T64_DKDV_PP 1
-#endif
-#ifndef MEA_T64_DQ_PP
-#define MEA_T64_DQ_PP 1
+// LDS fetch distances, in steps, of the two-group dQ and dK/dV kernels.
+#ifndef MEA_T64_DQ_AHEAD
+#define MEA_T64_DQ_AHEAD 2
 #endif
 #ifndef MEA_T64_DKDV_AHEAD
 #define MEA_T64_DKDV_AHEAD 2
@@ -31,10 +27,22 @@
 namespace mea {
 
 template <bool B> struct BoolC { static constexpr bool value = B; };
+template <int I> struct IntC { static constexpr int value = I; };
 
 // ------------------------------------------------------------------- pre
-// D_i = dO_i . O_i and the accumulator initial values of every (padded) row.
-template <typename TO, int D>
+// x as hi + mid + lo, three bf16 values (round to nearest each): the two
+// differences are exact in float32, so the parts carry 24 significant bits
+// and (hi + mid) + lo gives x back in float32.
+__device__ __forceinline__ void split3_bf16(float x, __bf16& hi, __bf16& mid, __bf16& lo) {
+  hi = (__bf16)x;
+  const float r1 = x - (float)hi;
+  mid = (__bf16)r1;
+  lo = (__bf16)(r1 - (float)mid);
+}
+
+// D_i = dO_i . O_i and the accumulator initial values of every (padded) row,
+// as records (REC) or as two float32 arrays.
+template <typename TO, int D, bool REC>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
   using T = TO;  // o and do share the output dtype
   constexpr int E = sizeof(T);
@@ -57,8 +65,21 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
 #pragma unroll
   for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, TPR);
   if (prow < rows && part == 0) {
-    p.s_init[prow] = real ? -p.lse[row] / p.scale : -INFINITY;
-    p.dp_init[prow] = real ? -acc : 0.0f;
+    const float lse = real ? p.lse[row] : 0.0f;
+    if constexpr (REC) {
+      // A row with no finite lse (padding) gets weights 2^(c (S - 2^100)) = 0.
+      const bool live = real && __builtin_isfinite(lse);
+      const float s0 = live ? -lse / p.scale : -0x1p100f;
+      const float d0 = live ? -acc : 0.0f;
+      __bf16 r[8];
+      split3_bf16(s0, r[0], r[1], r[2]);
+      split3_bf16(d0, r[4], r[5], r[6]);
+      r[3] = r[7] = (__bf16)0.0f;
+      p.row_rec[prow] = __builtin_bit_cast(uint4, r);
+    } else {
+      p.s_init[prow] = real ? -lse / p.scale : -INFINITY;
+      p.dp_init[prow] = real ? -acc : 0.0f;
+    }
   }
 }
 
@@ -309,10 +330,10 @@ namespace kvpp {
 constexpr int D = 64, NW = 8, BKG = NW * 32, BQ = 64, QS = BQ / 32, NSTAGE = 4;
 constexpr int RSB = 144;                      // bytes per LDS row (128 + 16 pad)
 constexpr int TILEB = BQ * RSB;               // one Q or dO tile: 9 KiB
-constexpr int INITB = 2 * BQ * 4;             // s_init and dp_init of the tile
-constexpr int STAGEB = 2 * TILEB + INITB;     // 18944 bytes
+constexpr int RECB = BQ * 16;                 // the tile's per-row records
+constexpr int STAGEB = 2 * TILEB + RECB;      // 19456 bytes
 constexpr int UNITS = 2 * TILEB / 1024 + 1;   // 1 KiB copies per stage (18 + 1)
-static_assert(TILEB % 1024 == 0 && INITB == 512, "stage layout");
+static_assert(TILEB % 1024 == 0 && RECB == 1024, "stage layout");
 }  // namespace kvpp
 
 template <typename T, bool CAUSAL>
@@ -337,8 +358,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
 
   const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
   const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
-  const float* __restrict__ sinitg = p.s_init + (size_t)bh * p.n_q_pad;
-  const float* __restrict__ dpinitg = p.dp_init + (size_t)bh * p.n_q_pad;
+  const uint4* __restrict__ recg = p.row_rec + (size_t)bh * p.n_q_pad;
   const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
   const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
 
@@ -375,9 +395,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // Copy unit u (0 <= u < UNITS) of query tile i into its stage: units 0..8
   // are the Q tile, 9..17 the dO tile (lane slot s = 64 (u % 9) + lane is row
   // s / 9, 16-byte chunk s % 9; chunk 8 is the row pad and gets a copy of
-  // chunk 7), unit 18 the initial values (lanes 0..15 s_init, 16..31 dp_init;
-  // the padded arrays hold every row of the tile).  Query rows past n_q repeat
-  // the last row (finite values; their weights are 0).
+  // chunk 7), unit 18 the per-row records (lane l: row l; the padded record
+  // array holds every row of the tile).  Query rows past n_q repeat the last
+  // row (finite values; their weights are 0).
   constexpr int ROWB = D * (int)sizeof(T);
   const int n_full = n_iters > 0 ? (int)((p.n_q - q_begin) / BQ) : 0;  // tiles with no row past n_q
   auto unit_off = [&](int u) {
@@ -400,8 +420,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
         copy_to_lds16(reinterpret_cast<const unsigned char*>(g + q * D) + off % ROWB, lds);
       }
     } else {
-      const unsigned base = __builtin_amdgcn_readfirstlane(lds_addr(st + 2 * TILEB));
-      if (lane < 32) copy_to_lds16((lane < 16 ? sinitg : dpinitg) + q0 + 4 * (lane & 15), base);
+      copy_to_lds16(recg + q0 + lane, __builtin_amdgcn_readfirstlane(lds_addr(st + 2 * TILEB)));
     }
   };
   // Each wave's share of the copies of a tile: units wave + 8k (three for
@@ -462,89 +481,113 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   const float cl2 = p.scale_log2;
   f32x16 s[QS], dp[QS];
   Frag<T> pa[NQC], da[NQC];
-  // Whether any query of tile i sees any key of this wave (causal).
-  auto active = [&](int i) { return !CAUSAL || q_begin + (int64_t)i * BQ + BQ - 1 >= kw; };
   // The MFMA phase issues each LDS fragment read AHEAD steps (two MFMAs each)
   // before its MFMAs (scheduling fences between steps), so that a wave alone
   // on the matrix pipe does not wait for LDS latency.  The causal variant keeps
   // a shorter distance for its larger register footprint.
   constexpr int AHEAD = CAUSAL ? 2 : MEA_T64_DKDV_AHEAD;
-  // dV += P^T dO and dK += dS^T Q for tile i (column fragments: k = queries).
-  auto dvdk = [&](int i) __attribute__((always_inline)) {
-    const unsigned char* st = stage(i);
-    const T* qs_t = reinterpret_cast<const T*>(st);
-    const T* dos_t = reinterpret_cast<const T*>(st + TILEB);
-    constexpr int NSTEP = NQC * NDT;
-    Frag<T> bo[AHEAD + 1], bq[AHEAD + 1];
-    auto fetch = [&](int step) __attribute__((always_inline)) {
-      const int qc = step / NDT, dt = step % NDT;
-      bo[step % (AHEAD + 1)] = lds_col_frag<T>(dos_t, RSB / 2, 16 * qc, 32 * dt, lane);
-      bq[step % (AHEAD + 1)] = lds_col_frag<T>(qs_t, RSB / 2, 16 * qc, 32 * dt, lane);
-    };
-#pragma unroll
-    for (int step = 0; step < AHEAD; ++step) fetch(step);
-#pragma unroll
-    for (int step = 0; step < NSTEP; ++step) {
-      if (step + AHEAD < NSTEP) fetch(step + AHEAD);
-      const int qc = step / NDT, dt = step % NDT;
-      dv[dt] = mma(pa[qc], bo[step % (AHEAD + 1)], dv[dt]);
-      dk[dt] = mma(da[qc], bq[step % (AHEAD + 1)], dk[dt]);
-      __builtin_amdgcn_sched_barrier(0);
+  // One fetch ring serves the whole MFMA phase.  Steps 0 .. NS1 - 1 are
+  // dV += P^T dO and dK += dS^T Q of the previous tile (column fragments of dO
+  // and Q: k = queries); steps NS1 .. NS1 + NS2 - 1 are S = Q K^T + s_init and
+  // dP = dO V^T + dp_init of this tile (row fragments of Q and dO).  A step's
+  // two fragments are read AHEAD steps before its MFMAs: across the move from
+  // dV/dK to S/dP, and, for the first AHEAD steps, at the end of the preceding
+  // softmax phase, so that the phase never starts on LDS latency.
+  constexpr int NS1 = NQC * NDT, NS2 = KC * QS, NS = NS1 + NS2;
+  Frag<T> rx[AHEAD + 1], ry[AHEAD + 1];
+  auto fetch = [&](int i_dv, int i_sd, int g) __attribute__((always_inline)) {
+    const int slot = g % (AHEAD + 1);
+    if (g < NS1) {
+      const unsigned char* st = stage(i_dv);
+      const int qc = g / NDT, dt = g % NDT;
+      rx[slot] = lds_col_frag<T>(reinterpret_cast<const T*>(st + TILEB), RSB / 2, 16 * qc, 32 * dt, lane);
+      ry[slot] = lds_col_frag<T>(reinterpret_cast<const T*>(st), RSB / 2, 16 * qc, 32 * dt, lane);
+    } else {
+      const unsigned char* st = stage(i_sd);
+      const int kc = (g - NS1) / QS, qs = (g - NS1) % QS;
+      const int off = (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h;
+      rx[slot] = lds_frag<T>(reinterpret_cast<const T*>(st) + off);
+      ry[slot] = lds_frag<T>(reinterpret_cast<const T*>(st + TILEB) + off);
     }
   };
-  // S = Q K^T + s_init and dP = dO V^T + dp_init for tile i (row fragments).
-  auto sdp = [&](int i) __attribute__((always_inline)) {
-    const unsigned char* st = stage(i);
-    const T* qs_t = reinterpret_cast<const T*>(st);
-    const T* dos_t = reinterpret_cast<const T*>(st + TILEB);
-    const float* sinit_s = reinterpret_cast<const float*>(st + 2 * TILEB);
-    const float* dpinit_s = sinit_s + BQ;
-    constexpr int NSTEP = KC * QS;
-    Frag<T> fa[AHEAD + 1], fg[AHEAD + 1];
-    auto fetch = [&](int step) __attribute__((always_inline)) {
-      const int kc = step / QS, qs = step % QS;
-      fa[step % (AHEAD + 1)] = lds_frag<T>(qs_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
-      fg[step % (AHEAD + 1)] = lds_frag<T>(dos_t + (32 * qs + qrow) * (RSB / 2) + 16 * kc + 8 * h);
-    };
+  // S and dP start from the per-row values of tile i: one bf16 MFMA each per
+  // query sub-tile, A = the rows' records (lane c: query 32 qs + perm32(c),
+  // the same record in both lane halves), B = ones picking the three s parts
+  // (bsel_s) or the three d parts (bsel_d) in the first lane half and zeros in
+  // the second, C = 0.  The records are read at the start of the MFMA phase.
+  bf16x8 rec[QS];
+  bf16x8 bsel_s, bsel_d;
 #pragma unroll
-    for (int step = 0; step < AHEAD; ++step) fetch(step);
+  for (int e = 0; e < 8; ++e) {
+    bsel_s[e] = (__bf16)(h == 0 && e < 3 ? 1.0f : 0.0f);
+    bsel_d[e] = (__bf16)(h == 0 && e >= 4 && e < 7 ? 1.0f : 0.0f);
+  }
+  auto read_rec = [&](int i) __attribute__((always_inline)) {
 #pragma unroll
     for (int qs = 0; qs < QS; ++qs)
+      rec[qs] = *reinterpret_cast<const bf16x8*>(stage(i) + 2 * TILEB + 16 * (32 * qs + qrow));
+  };
+  auto init_sdp = [&]() __attribute__((always_inline)) {
+    const f32x16 zero = {};
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = 32 * qs + 16 * (j >> 1) + 8 * h + 4 * (j & 1);
-        const f32x4 a = *reinterpret_cast<const f32x4*>(sinit_s + row);
-        const f32x4 b = *reinterpret_cast<const f32x4*>(dpinit_s + row);
+    for (int qs = 0; qs < QS; ++qs) {
+      s[qs] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rec[qs], bsel_s, zero, 0, 0, 0);
+      dp[qs] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rec[qs], bsel_d, zero, 0, 0, 0);
+    }
+  };
+  // Steps [G0, G1) with dV/dK of tile i_dv and S/dP of tile i_sd; the ring
+  // already holds steps G0 .. G0 + AHEAD - 1.  S and dP are initialised just
+  // before their first step.
+  auto run = [&](auto g0_tag, auto g1_tag, int i_dv, int i_sd) __attribute__((always_inline)) {
+    constexpr int G0 = decltype(g0_tag)::value, G1 = decltype(g1_tag)::value;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          s[qs][4 * j + e] = a[e];
-          dp[qs][4 * j + e] = b[e];
-        }
+    for (int g = G0; g < G1; ++g) {
+      if (g + AHEAD < G1) fetch(i_dv, i_sd, g + AHEAD);
+      if (g == NS1) init_sdp();
+      const int slot = g % (AHEAD + 1);
+      if (g < NS1) {
+        const int qc = g / NDT, dt = g % NDT;
+        dv[dt] = mma(pa[qc], rx[slot], dv[dt]);
+        dk[dt] = mma(da[qc], ry[slot], dk[dt]);
+      } else {
+        const int kc = (g - NS1) / QS, qs = (g - NS1) % QS;
+        s[qs] = mma(rx[slot], kf[kc], s[qs]);
+        dp[qs] = mma(ry[slot], vf[kc], dp[qs]);
       }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int step = 0; step < NSTEP; ++step) {
-      if (step + AHEAD < NSTEP) fetch(step + AHEAD);
-      const int kc = step / QS, qs = step % QS;
-      s[qs] = mma(fa[step % (AHEAD + 1)], kf[kc], s[qs]);
-      dp[qs] = mma(fg[step % (AHEAD + 1)], vf[kc], dp[qs]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  // dV/dK of tile i_dv alone (the ring was filled at the end of the softmax
+  // phase of tile i_dv).
+  auto dvdk = [&](int i_dv) __attribute__((always_inline)) { run(IntC<0>{}, IntC<NS1>{}, i_dv, i_dv); };
 
-  for (int i = 0; i < n_iters; ++i) {
+  // One iteration per query tile.  MODE 0: the tile is not active for this
+  // wave (causal: all its queries precede the wave's keys), only the copies
+  // and barriers run; MODE 1: the wave's first active tile (S/dP only); MODE 2:
+  // dV/dK of the previous tile and S/dP of this one.  A tile active for a wave
+  // stays active for its later tiles (the queries only grow), so the modes
+  // come in this order and each loop below runs one of them.
+  auto iteration = [&](auto mode_tag, int i) __attribute__((always_inline)) {
+    constexpr int MODE = decltype(mode_tag)::value;
     const int64_t q0 = q_begin + (int64_t)i * BQ;
-    // ---- MFMA phase
+    // ---- MFMA phase (S and dP are free: the last softmax phase converted them)
     mfma_phase_priority();
-    if (i >= 1 && active(i - 1)) dvdk(i - 1);
-    if (active(i)) sdp(i);
+    if constexpr (MODE == 1) {
+      read_rec(i);
+#pragma unroll
+      for (int g = NS1; g < NS1 + AHEAD; ++g) fetch(i, i, g);
+      run(IntC<NS1>{}, IntC<NS>{}, i, i);
+    } else if constexpr (MODE == 2) {
+      read_rec(i);
+      run(IntC<0>{}, IntC<NS>{}, i - 1, i);
+    }
     // Group 1: tile i + 1 must land before this barrier (its share of tile
     // i + 2 may still run).
     if (grp == 1) wait_copies(i + 2 < n_iters);
     barrier();
     // ---- VALU phase
     valu_phase_priority();
-    if (active(i)) {
+    if constexpr (MODE != 0) {
       const bool need_mask = CAUSAL && q0 < kw + 31;
       const int key_rel = (int)(key - q0);  // key minus the tile's first query
 #pragma unroll
@@ -569,6 +612,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
         keep_here(pa[qc]);  // the conversions belong to this phase
         keep_here(da[qc]);
       }
+      // The first fragments of dV/dK of this tile, for the next MFMA phase.
+#pragma unroll
+      for (int g = 0; g < AHEAD; ++g) fetch(i, i, g);
     }
     if (grp == 1) {
       issue(i + 3);
@@ -578,9 +624,20 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
       wait_copies(i + 2 < n_iters);
     }
     barrier();
+  };
+  // The wave's first active tile: the first i with q_begin + 64 i + 63 >= kw.
+  int i_first = 0;
+  if (CAUSAL) {
+    const int64_t t = kw - q_begin - (BQ - 1);
+    i_first = t > 0 ? (int)((t + BQ - 1) / BQ) : 0;
+    if (i_first > n_iters) i_first = n_iters;
   }
+  int i = 0;
+  for (; i < i_first; ++i) iteration(IntC<0>{}, i);
+  if (i < n_iters) iteration(IntC<1>{}, i++);
+  for (; i < n_iters; ++i) iteration(IntC<2>{}, i);
   // dV/dK of the last tile.
-  if (n_iters > 0 && active(n_iters - 1)) dvdk(n_iters - 1);
+  if (i_first < n_iters) dvdk(n_iters - 1);
   // Group 0 issued one barrier fewer (group 1's start delay): balance it so
   // that no wave leaves while the other group still waits at a barrier.
   if (grp == 0) barrier();
@@ -878,8 +935,13 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
       }
     }
   }
-  const float s_init = valid ? p.s_init[(size_t)bh * p.n_q_pad + query] : -INFINITY;
-  const float dp_init = valid ? p.dp_init[(size_t)bh * p.n_q_pad + query] : 0.0f;
+  // The query's initial values from its record (three bf16 parts each).
+  float s_init = -INFINITY, dp_init = 0.0f;
+  if (valid) {
+    const bf16x8 r = __builtin_bit_cast(bf16x8, p.row_rec[(size_t)bh * p.n_q_pad + query]);
+    s_init = ((float)r[0] + (float)r[1]) + (float)r[2];
+    dp_init = ((float)r[4] + (float)r[5]) + (float)r[6];
+  }
   wait_global_loads();
 
   f32x16 acc[NDT];
@@ -975,7 +1037,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
     const int64_t k0 = (int64_t)j * BK;
     return k0 + BK > p.n_k || (CAUSAL && k0 + BK - 1 > qw);
   };
-  constexpr int AHEAD = 2;
+  constexpr int AHEAD = CAUSAL ? 2 : MEA_T64_DQ_AHEAD;
   // dQ^T += K^T dS^T for tile j (column fragments of K: k = keys).
   auto dq_mma = [&](int j) __attribute__((always_inline)) {
     const T* ks = reinterpret_cast<const T*>(stage(j));
@@ -1139,13 +1201,14 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   void* args[] = {&p};
   const int64_t rows = (int64_t)p.bh * p.n_q_pad;
   constexpr int RPB = 256 / (D * (int)sizeof(TO) / 16);
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, D>),
+  constexpr bool PP = sizeof(T) == 2 && D == 64 && __is_same(T, TO);
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, D, PP>),
                                  dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
   if (e != hipSuccess) return e;
   p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
   p.n_qtiles = (int)((p.n_q + 128 * S::QT - 1) / (128 * S::QT));
   if (p.dk) {
-    if constexpr (sizeof(T) == 2 && D == 64 && __is_same(T, TO) && MEA_T64_DKDV_PP) {
+    if constexpr (PP) {
       p.n_ktiles = (int)((p.n_k + kvpp::BKG - 1) / kvpp::BKG);
       e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_pp_kernel<T, CAUSAL>),
                           dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(kvpp::NW * 64), args, 0, stream);
@@ -1155,7 +1218,7 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
     }
     if (e != hipSuccess || !p.dq) return e;
   }
-  if constexpr (sizeof(T) == 2 && D == 64 && __is_same(T, TO) && MEA_T64_DQ_PP) {
+  if constexpr (PP) {
     p.n_qtiles = (int)((p.n_q + qpp::BQG - 1) / qpp::BQG);
     return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_pp_kernel<T, CAUSAL>),
                            dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(qpp::NW * 64), args, 0, stream);

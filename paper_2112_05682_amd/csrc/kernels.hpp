@@ -38,12 +38,18 @@ struct BwdParams {
   void* dk;
   void* dv;
   // Per-row initial values of the score and dP accumulators, written by the
-  // preprocess kernel, [B*H, n_q_pad] float32: s_init = -lse / scale (so that
-  // P = 2^(c * (S + s_init)), c = scale * log2 e) and dp_init = -D with
-  // D_i = dO_i . O_i (so that dS = P * (dP + dp_init)).  Rows n_q .. n_q_pad - 1
-  // hold -inf and 0: they contribute nothing.
+  // preprocess kernel: s_init = -lse / scale (so that P = 2^(c * (S + s_init)),
+  // c = scale * log2 e) and dp_init = -D with D_i = dO_i . O_i (so that
+  // dS = P * (dP + dp_init)).  Rows n_q .. n_q_pad - 1 contribute nothing.
+  // The two-group kernels (16-bit inputs and outputs, d = 64) take them as
+  // one 16-byte record per row, eight bf16 values {s_hi, s_mid, s_lo, 0,
+  // d_hi, d_mid, d_lo, 0} whose three parts sum to s_init and dp_init in
+  // float32 (padding rows: s = -2^100, d = 0), so that one bf16 MFMA against
+  // a constant operand puts them into the accumulators; the other kernels
+  // take [B*H, n_q_pad] float32 arrays (padding rows -inf and 0).
   float* s_init;
   float* dp_init;
+  uint4* row_rec;
   int64_t n_q_pad;  // n_q rounded up to kBwdRowPad
   int64_t n_q;
   int64_t n_k;
@@ -57,6 +63,10 @@ struct BwdParams {
 // Row padding of the backward's per-row arrays (a multiple of every query
 // tile the backward kernels stage).
 constexpr int kBwdRowPad = 64;
+
+// Whether the backward of a problem runs the two-group kernels, which take
+// the per-row values as records (dtype: 0 float32, 1 fp16, 2 bf16).
+inline bool bwd_uses_row_records(int dtype, int d, bool out_f32) { return dtype != 0 && d == 64 && !out_f32; }
 
 // Tile shapes per (element type, head dimension); shared by the host plan
 // and the kernel instantiations.
