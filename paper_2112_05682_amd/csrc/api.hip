@@ -68,7 +68,33 @@ void fwd_tiles(int dtype, int64_t d, int* bq, int* bk) {
 // Grid plan.  The chip has 256 CUs; when the query tiles alone give too few
 // workgroups, the keys are split so that each split's summary is combined
 // afterwards (Section 4 combine).
+// Decode plan: one wave per key range; ranges of at least 4 key tiles, about
+// 2048 workgroups in all (8 per CU), at most 1024 ranges per (batch, head).
+FwdPlan plan_decode(const mea_problem* p) {
+  FwdPlan pl;
+  pl.bq = 64;
+  pl.bk = mea::fwd_decode_tile((int)p->d);
+  pl.n_qtiles = 1;
+  const int64_t bh = p->batch * p->heads;
+  const int64_t n_keys = p->causal && p->n_k > p->n_q ? p->n_q : p->n_k;
+  const int64_t k_tiles = (n_keys + pl.bk - 1) / pl.bk;
+  int64_t splits = (2048 + bh - 1) / bh;
+  if (splits > k_tiles / 4) splits = k_tiles / 4;
+  if (splits > 1024) splits = 1024;
+  if (splits < 1) splits = 1;
+  const int64_t tiles_per_split = (k_tiles + splits - 1) / splits;
+  pl.keys_per_split = tiles_per_split * pl.bk;
+  pl.n_splits = (int)((n_keys + pl.keys_per_split - 1) / pl.keys_per_split);
+  pl.workspace = 0;
+  if (pl.n_splits > 1) {
+    const size_t rows = (size_t)pl.n_splits * (size_t)bh * (size_t)p->n_q;
+    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256;
+  }
+  return pl;
+}
+
 FwdPlan plan_fwd(const mea_problem* p) {
+  if (mea::fwd_uses_decode((int)p->dtype, p->n_q)) return plan_decode(p);
   FwdPlan pl;
   fwd_tiles(p->dtype, p->d, &pl.bq, &pl.bk);
   const int64_t bh = p->batch * p->heads;

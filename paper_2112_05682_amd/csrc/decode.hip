@@ -1,0 +1,298 @@
+// Decode-shaped forward: a small group of queries (n_q <= 64 per batch and
+// head) against a long key sequence.  This is the paper's single-query
+// algorithm (Section 2, stabilised by the running maximum of Section 3)
+// generalised to a query group, with the keys split into ranges whose
+// summaries are combined afterwards (Section 4): each workgroup is one wave
+// that streams one key range of one (batch, head) through LDS and keeps the
+// running numerator, denominator and maximum of every query of the group.
+//
+// The work is bound by HBM (K and V are read once: 4 d bytes per key for
+// 16-bit inputs against 4 d n_q flops), so the kernel is shaped for bytes in
+// flight rather than for matrix throughput: one wave per workgroup, a
+// two-stage LDS ring of asynchronous copies per wave, and enough workgroups
+// per CU (the ring is 36 KiB) to keep about 64 KiB of copies in flight per
+// CU.  The scores and the weighted values still go through MFMA with the
+// query group padded to 32 or 64 columns: at n_q <= 64 the padded matrix work
+// stays below the HBM time.
+#include "device.hpp"
+#include "kernels.hpp"
+
+namespace mea {
+
+namespace dec {
+// Tile geometry for head dimension D: BK keys per tile, LDS rows of D
+// features plus one 16-byte pad slot (row and transposing reads then touch
+// distinct banks), the copies of a tile as NCOPY 1 KiB wave copies (the slots
+// past the tile's rows are a dead tail inside the tile's LDS space).
+template <int D>
+struct Cfg {
+  static constexpr int BK = D == 64 ? 64 : 32;
+  static constexpr int SPR = D / 8 + 1;  // 16-byte slots per LDS row
+  static constexpr int RSB = 16 * SPR;   // bytes per LDS row
+  static constexpr int NSLOT = BK * SPR;
+  static constexpr int NCOPY = (NSLOT + 63) / 64;
+  static constexpr int TILEB = NCOPY * 1024;
+  static constexpr int NSTAGE = 2;
+  static constexpr int STAGEB = 2 * TILEB;  // K tile, V tile
+  static_assert(BK * RSB <= TILEB, "rows fit the tile");
+};
+}  // namespace dec
+
+// Top-left causal (key j visible to query i iff j <= i): only the first n_q
+// keys can be visible to a group of n_q queries.
+__host__ __device__ inline int64_t decode_keys(int64_t n_q, int64_t n_k, bool causal) {
+  return causal && n_k > n_q ? n_q : n_k;
+}
+
+// One wave: queries 0 .. 32 QT - 1 of (batch, head) bh against keys
+// [split * keys_per_split, ...).  Scores in the orientation S^T = K Q^T (lane =
+// query, registers = keys, K rows read in the perm32 order so that the
+// weights convert in place into the B operand of O^T += V^T P^T).
+template <typename T, typename TO, int D, int QT, bool CAUSAL>
+__global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
+  using C = dec::Cfg<D>;
+  constexpr int BK = C::BK, NKT = BK / 32, KC = D / 16, NDT = D / 32, NPC = BK / 16;
+  constexpr int RS = C::RSB / 2;  // LDS row stride in elements
+  constexpr int ROWB = D * 2;     // global row bytes
+  __shared__ __align__(16) unsigned char smem[C::NSTAGE * C::STAGEB];
+
+  const int lane = threadIdx.x;
+  const int h = lane >> 5, c = lane & 31;
+  const int split = blockIdx.x % p.n_splits;
+  const int bh = blockIdx.x / p.n_splits;
+
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+
+  const int64_t n_keys = decode_keys(p.n_q, p.n_k, CAUSAL);
+  const int64_t kb = (int64_t)split * p.keys_per_split;
+  int64_t ke = kb + p.keys_per_split;
+  if (ke > n_keys) ke = n_keys;
+  const int n_tiles = kb < ke ? (int)((ke - kb + BK - 1) / BK) : 0;
+
+  // Q^T as B operands: lane (h, c) holds query 32 t + c, features 16 kc + 8 h ..
+  Frag<T> qf[QT][KC];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const int64_t query = 32 * t + c;
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      if (query < p.n_q) {
+        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[t][kc][e] = (T)0.0f;
+      }
+    }
+  }
+
+  // Copy u of a tile moves lane slots 64 u + lane: row slot / SPR, 16-byte
+  // chunk slot % SPR (the pad slot gets a copy of the last chunk); slots past
+  // the tile's rows repeat its last slot.  Byte offsets within a tile row
+  // block are computed once.
+  unsigned uoff[C::NCOPY];
+#pragma unroll
+  for (int u = 0; u < C::NCOPY; ++u) {
+    int slot = 64 * u + lane;
+    if (slot >= C::NSLOT) slot = C::NSLOT - 1;
+    const int row = slot / C::SPR, ch = slot % C::SPR;
+    uoff[u] = (unsigned)(row * ROWB + 16 * (ch < C::SPR - 1 ? ch : C::SPR - 2));
+  }
+  auto copy_tile = [&](int j) __attribute__((always_inline)) {
+    const int64_t k0 = kb + (int64_t)j * BK;
+    unsigned char* st = smem + (j % C::NSTAGE) * C::STAGEB;
+    const unsigned kl = lds_addr(st), vl = lds_addr(st + C::TILEB);
+    if (k0 + BK <= ke) {
+#pragma unroll
+      for (int u = 0; u < C::NCOPY; ++u) {
+        copy_to_lds16_sb(kg + k0 * D, uoff[u], __builtin_amdgcn_readfirstlane(kl + 1024 * u));
+        copy_to_lds16_sb(vg + k0 * D, uoff[u], __builtin_amdgcn_readfirstlane(vl + 1024 * u));
+      }
+    } else {
+      // Ragged last tile: rows past the range repeat its last key (finite
+      // values, masked below).
+#pragma unroll
+      for (int u = 0; u < C::NCOPY; ++u) {
+        int64_t key = k0 + uoff[u] / ROWB;
+        if (key > ke - 1) key = ke - 1;
+        const unsigned col = uoff[u] % ROWB;
+        copy_to_lds16(reinterpret_cast<const unsigned char*>(kg + key * D) + col,
+                      __builtin_amdgcn_readfirstlane(kl + 1024 * u));
+        copy_to_lds16(reinterpret_cast<const unsigned char*>(vg + key * D) + col,
+                      __builtin_amdgcn_readfirstlane(vl + 1024 * u));
+      }
+    }
+  };
+
+  const float cl2 = p.scale_log2;
+  const int krow = perm32(c);
+  float m_run[QT], l_run[QT];
+  f32x16 acc[QT][NDT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.0f;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[t][dt][r] = 0.0f;
+  }
+
+  if (n_tiles > 0) copy_tile(0);
+  if (n_tiles > 1) copy_tile(1);
+  for (int j = 0; j < n_tiles; ++j) {
+    // Tile j has landed once at most the copies of tile j + 1 are in flight.
+    if (j + 1 < n_tiles) wait_global_loads_upto<2 * C::NCOPY>();
+    else wait_global_loads();
+    const unsigned char* st = smem + (j % C::NSTAGE) * C::STAGEB;
+    const T* ks = reinterpret_cast<const T*>(st);
+    const T* vs = reinterpret_cast<const T*>(st + C::TILEB);
+    const int64_t k0 = kb + (int64_t)j * BK;
+
+    // S^T = K Q^T for the tile (one K fragment serves every query sub-tile).
+    f32x16 s[QT][NKT];
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[t][kt][r] = 0.0f;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        const Frag<T> kf = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) s[t][kt] = mma(kf, qf[t][kc], s[t][kt]);
+      }
+
+    // Mask keys past the range (ragged tile) and, causal, keys after the query.
+    if (CAUSAL || k0 + BK > ke) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        int64_t lim = ke - k0;  // keys k0 + x with x < lim are in range
+        if (CAUSAL && 32 * t + c + 1 - k0 < lim) lim = 32 * t + c + 1 - k0;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (32 * kt + permuted_row(r, h) >= lim) s[t][kt][r] = -INFINITY;
+      }
+    }
+
+    // Online softmax per query (lane): running maximum in units of c S.
+    Frag<T> pf[QT][NPC];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][kt][r]);
+      mx = xhalf_max(mx) * cl2;
+      const float m_new = fmaxf(m_run[t], mx);
+      // No visible key yet: reference 0 (every weight is 2^-inf = 0).
+      const float mref = m_new == -INFINITY ? 0.0f : m_new;
+      const float alpha = fast_exp2(m_run[t] - mref);
+      m_run[t] = m_new;
+      l_run[t] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[t][dt][r] *= alpha;
+#pragma unroll
+      for (int pc = 0; pc < NPC; ++pc) {
+        float w8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w8[e] = fast_exp2(fmaf(s[t][pc >> 1][8 * (pc & 1) + e], cl2, -mref));
+        pf[t][pc] = to_frag<T>(w8);
+        l_run[t] = frag_sum(pf[t][pc], nullptr, l_run[t]);  // the rounded weights the numerator uses
+      }
+    }
+
+    // O^T += V^T P^T (one V fragment serves every query sub-tile).
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int pc = 0; pc < NPC; ++pc) {
+        const Frag<T> vf = lds_col_frag<T>(vs, RS, 16 * pc, 32 * dt, lane);
+#pragma unroll
+        for (int t = 0; t < QT; ++t) acc[t][dt] = mma(vf, pf[t][pc], acc[t][dt]);
+      }
+
+    // The stage is free once its reads have returned; refill it with tile j + 2.
+    if (j + 2 < n_tiles) {
+      wait_lds_reads();
+      copy_tile(j + 2);
+    }
+  }
+
+  // Epilogue: the two lane halves hold disjoint keys of the same query.
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    const float l_tot = xhalf_sum(l_run[t]);
+    const int64_t row = 32 * t + c;
+    if (row >= p.n_q) continue;
+    if (p.n_splits == 1) {
+      const float inv = 1.0f / l_tot;
+      TO* og = static_cast<TO*>(p.o) + ((size_t)bh * p.n_q + row) * D;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          typename FragT<TO>::half v4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
+          *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
+        }
+      if (h == 0 && p.lse) p.lse[(size_t)bh * p.n_q + row] = (m_run[t] + __log2f(l_tot)) * 0.6931471805599453f;
+    } else {
+      const size_t prow = ((size_t)split * p.bh + bh) * p.n_q + row;
+      float* po = p.part_o + prow * D;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          f32x4 v4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v4[e] = acc[t][dt][4 * a4 + e];
+          *reinterpret_cast<f32x4*>(po + 32 * dt + 8 * a4 + 4 * h) = v4;
+        }
+      if (h == 0) {
+        p.part_m[prow] = m_run[t];  // log2 units (scaled), -inf if the range has no visible key
+        p.part_l[prow] = l_tot;
+      }
+    }
+  }
+}
+
+template <typename T, typename TO, int D>
+static hipError_t launch_decode_dt(const FwdParams& p, bool causal, hipStream_t stream) {
+  FwdParams pc = p;
+  void* args[] = {&pc};
+  const dim3 grid((unsigned)((int64_t)p.bh * p.n_splits)), block(64);
+  if (p.n_q <= 32) {
+    auto k = causal ? attn_decode_kernel<T, TO, D, 1, true> : attn_decode_kernel<T, TO, D, 1, false>;
+    return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, args, 0, stream);
+  }
+  auto k = causal ? attn_decode_kernel<T, TO, D, 2, true> : attn_decode_kernel<T, TO, D, 2, false>;
+  return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, args, 0, stream);
+}
+
+template <typename T, int D>
+static hipError_t launch_decode_out(const FwdParams& p, bool causal, bool out_f32, hipStream_t stream) {
+  return out_f32 ? launch_decode_dt<T, float, D>(p, causal, stream) : launch_decode_dt<T, T, D>(p, causal, stream);
+}
+
+hipError_t launch_decode(const FwdParams& p, int dtype, int d, bool causal, bool out_f32, hipStream_t stream) {
+  switch (dtype * 1000 + d) {
+    case 1 * 1000 + 64: return launch_decode_out<_Float16, 64>(p, causal, out_f32, stream);
+    case 1 * 1000 + 128: return launch_decode_out<_Float16, 128>(p, causal, out_f32, stream);
+    case 2 * 1000 + 64: return launch_decode_out<__bf16, 64>(p, causal, out_f32, stream);
+    case 2 * 1000 + 128: return launch_decode_out<__bf16, 128>(p, causal, out_f32, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace mea

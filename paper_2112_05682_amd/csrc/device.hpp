@@ -128,9 +128,13 @@ __device__ __forceinline__ void wait_global_loads() { __builtin_amdgcn_s_waitcnt
 // (they complete in issue order).
 template <int N>
 __device__ __forceinline__ void wait_global_loads_upto() {
-  static_assert(N >= 0 && N < 16, "vmcnt immediate");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+  static_assert(N >= 0 && N < 64, "vmcnt immediate");
+  // vmcnt bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left unconstrained.
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
+// Wait until every LDS read of this wave has returned (lgkmcnt(0), vmcnt and
+// expcnt unconstrained): the LDS space they read may then be overwritten.
+__device__ __forceinline__ void wait_lds_reads() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // Materialise v in registers at this point: an empty statement that takes v
 // as input, so that the computation of v cannot be sunk past what follows

@@ -844,8 +844,28 @@ static hipError_t launch_fwd_out(const FwdParams& p, bool causal, bool out_f32, 
   return out_f32 ? launch_fwd_dt<T, float, D>(p, causal, stream) : launch_fwd_dt<T, T, D>(p, causal, stream);
 }
 
+template <typename TO, int D>
+static hipError_t launch_combine(const FwdParams& p, hipStream_t stream) {
+  FwdParams pc = p;
+  void* args[] = {&pc};
+  const int64_t threads = (int64_t)p.bh * p.n_q * (D / 4);
+  return hipLaunchKernel(reinterpret_cast<const void*>(attn_combine_kernel<TO, D>),
+                         dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, stream);
+}
+
 hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, bool out_f32,
                       hipStream_t stream) {
+  if (fwd_uses_decode(dtype, p.n_q)) {
+    const hipError_t e = launch_decode(p, dtype, d, causal, out_f32, stream);
+    if (e != hipSuccess || p.n_splits == 1) return e;
+    const bool f32 = out_f32;
+    if (dtype == 1) {
+      if (d == 64) return f32 ? launch_combine<float, 64>(p, stream) : launch_combine<_Float16, 64>(p, stream);
+      return f32 ? launch_combine<float, 128>(p, stream) : launch_combine<_Float16, 128>(p, stream);
+    }
+    if (d == 64) return f32 ? launch_combine<float, 64>(p, stream) : launch_combine<__bf16, 64>(p, stream);
+    return f32 ? launch_combine<float, 128>(p, stream) : launch_combine<__bf16, 128>(p, stream);
+  }
   switch (dtype * 1000 + d) {
     case 0 * 1000 + 64: return launch_fwd_dt<float, float, 64>(p, causal, stream);
     case 0 * 1000 + 128: return launch_fwd_dt<float, float, 128>(p, causal, stream);

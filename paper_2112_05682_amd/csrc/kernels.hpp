@@ -93,6 +93,11 @@ template <> struct FwdShape<float, 128> { static constexpr int QT = 1, BK = 32, 
 
 // dtype codes follow mea_dtype: 0 = f32, 1 = f16, 2 = bf16.
 // out_f32: o (and, in the backward, do) are float32 instead of the input dtype.
+// Decode-shaped forward: 16-bit inputs and at most 64 queries per (batch,
+// head) run the key-streaming decode kernel (key tile fwd_decode_tile(d)).
+inline bool fwd_uses_decode(int dtype, int64_t n_q) { return dtype != 0 && n_q <= 64; }
+inline int fwd_decode_tile(int d) { return d == 64 ? 64 : 32; }
+hipError_t launch_decode(const FwdParams& p, int dtype, int d, bool causal, bool out_f32, hipStream_t stream);
 hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, bool out_f32,
                       hipStream_t stream);
 hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, bool out_f32,

@@ -52,6 +52,12 @@ WORKLOADS = {
                  causal=True, std=0.5),
         Workload("longkv_bf16_b1h1_nq16384_nk1048576_d64", 1, 1, 16384, 1 << 20, 64, "bf16",
                  backward=False),
+        # Decode-shaped: one query per (batch, head) against a long key
+        # sequence (the paper's single-query setting, Section 2), and a group
+        # of 16 queries.
+        Workload("decode_bf16_b8h16_nq1_nk65536_d64", 8, 16, 1, 65536, 64, "bf16", backward=False),
+        Workload("decode_bf16_b8h16_nq16_nk65536_d64", 8, 16, 16, 65536, 64, "bf16",
+                 backward=False),
     )
 }
 
