@@ -62,6 +62,41 @@ def load_traffic(kernel: str):
     return ent.get("hbm_bytes_per_launch")
 
 
+DECODE_WORKLOAD = "decode_bf16_b8h16_nq1_nk65536_d64"
+
+
+def bench_decode(w, dev, calls: int = 50, warmup: int = 5):
+    """Decode-shaped forward (one query per batch and head against n_k keys):
+    HBM-bound, so its roofline is the 8 TB/s HBM peak.  Algorithmic bytes per
+    call: K and V once (4 n_k d per (batch, head) for 16-bit inputs), Q and O
+    (4 n_q d) and the lse (4 n_q); the time includes the combine of the key
+    ranges.  HIP events on torch's current stream, the stream the kernels run on."""
+    import torch
+
+    from paper_2112_05682_amd import attention_fwd
+    from paper_2112_05682_amd.inputs import workload_inputs
+
+    x = {k_: t.to(dev) for k_, t in workload_inputs(w, with_grad=False).items()}
+    for _ in range(warmup):
+        attention_fwd(x["q"], x["k"], x["v"], causal=w.causal)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(calls):
+        attention_fwd(x["q"], x["k"], x["v"], causal=w.causal)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / calls
+    bh = w.batch * w.heads
+    nbytes = bh * (4 * w.n_k * w.d + 4 * w.n_q * w.d + 4 * w.n_q)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    del x
+    return {"workload": w.name, "kernel": "attn_decode_kernel", "bound": "hbm", "calls": calls,
+            "ms": round(ms, 4), "algorithmic_bytes": nbytes, "achieved": round(gbs, 1),
+            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "traffic": load_traffic("attn_decode_kernel"), "includes": "combine of the key ranges"}
+
+
 def cpu_baseline(w):
     """Time the float64 oracle (forward + backward) on whole (batch, head)
     slices of the workload (heads are independent, so a slice is exact)."""
@@ -100,6 +135,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device copy (HBM counter calibration)")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the decode-shaped forward measurement")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -190,6 +227,8 @@ def main() -> int:
     lse_bytes = w.batch * w.heads * w.n_q * 4
     n2_bytes = w.batch * w.heads * w.n_q * w.n_k * 4
 
+    decode = None if args.no_decode else bench_decode(WORKLOADS[DECODE_WORKLOAD], dev)
+
     if args.copy_calibration:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -231,6 +270,8 @@ def main() -> int:
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic},
     }
+    if decode is not None:
+        out["decode"] = decode
     if not args.no_cpu_baseline:
         cb = cpu_baseline(w)
         out["cpu_baseline"] = {kk: (round(vv, 6) if isinstance(vv, float) else vv)
