@@ -1030,8 +1030,6 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   const float cl2 = p.scale_log2;
   f32x16 s[NKT], dp[NKT];
   Frag<T> dsf[NPC];
-  // Whether any key of tile j is visible to any query of this wave (causal).
-  auto active = [&](int j) { return !CAUSAL || (int64_t)j * BK <= qw + 31; };
   // Whether tile j needs the elementwise mask (ragged keys, causal diagonal).
   auto masked = [&](int j) {
     const int64_t k0 = (int64_t)j * BK;
@@ -1118,16 +1116,23 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
     }
   };
 
-  for (int j = 0; j < n_tiles; ++j) {
+  // One iteration per key tile.  MODE 1: the first tile (S/dP only); MODE 2:
+  // dQ of the previous tile and S/dP of this one; MODE 3: dQ of the previous
+  // tile only (this one is past the wave's last query, causal); MODE 0:
+  // copies and barriers only.  A tile past the wave's last query stays so for
+  // the later tiles (the keys only grow), so the modes come in this order and
+  // each loop below runs one of them.
+  auto iteration = [&](auto mode_tag, int j) __attribute__((always_inline)) {
+    constexpr int MODE = decltype(mode_tag)::value;
     // ---- MFMA phase
     mfma_phase_priority();
-    if (j >= 1 && active(j - 1)) dq_mma(j - 1);
-    if (active(j)) sdp(j);
+    if constexpr (MODE == 2 || MODE == 3) dq_mma(j - 1);
+    if constexpr (MODE == 1 || MODE == 2) sdp(j);
     if (grp == 1) wait_copies(j + 2 < n_tiles);
     barrier();
     // ---- VALU phase
     valu_phase_priority();
-    if (active(j)) {
+    if constexpr (MODE == 1 || MODE == 2) {
       if (masked(j)) pds(BoolC<true>{}, j);
       else pds(BoolC<false>{}, j);
     }
@@ -1138,8 +1143,19 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
       wait_copies(j + 2 < n_tiles);
     }
     barrier();
+  };
+  // Tiles 0 .. j_end - 1 hold keys visible to the wave.
+  int j_end = n_tiles;
+  if (CAUSAL) {
+    const int64_t last = (qw + 31) / BK + 1;
+    if (last < j_end) j_end = (int)last;
   }
-  if (n_tiles > 0 && active(n_tiles - 1)) dq_mma(n_tiles - 1);
+  int j = 0;
+  if (j < j_end) iteration(IntC<1>{}, j++);
+  for (; j < j_end; ++j) iteration(IntC<2>{}, j);
+  if (j < n_tiles) iteration(IntC<3>{}, j++);
+  for (; j < n_tiles; ++j) iteration(IntC<0>{}, j);
+  if (j_end == n_tiles && n_tiles > 0) dq_mma(n_tiles - 1);
   if (grp == 0) barrier();  // group 1's start delay, balanced
 
   if (valid) {
