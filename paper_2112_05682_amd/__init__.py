@@ -8,6 +8,8 @@ is the thin Python binding.
 """
 from .attention import (MemoryEfficientAttention, attention, attention_bwd, attention_fwd,
                         bwd_workspace_bytes, fwd_workspace_bytes)
+from .nn import MultiheadAttention, TransformerBlock, TransformerLM
 
 __all__ = ["attention", "attention_fwd", "attention_bwd", "MemoryEfficientAttention",
-           "fwd_workspace_bytes", "bwd_workspace_bytes"]
+           "fwd_workspace_bytes", "bwd_workspace_bytes", "MultiheadAttention", "TransformerBlock",
+           "TransformerLM"]
