@@ -88,7 +88,8 @@ FwdPlan plan_decode(const mea_problem* p) {
   pl.workspace = 0;
   if (pl.n_splits > 1) {
     const size_t rows = (size_t)pl.n_splits * (size_t)bh * (size_t)p->n_q;
-    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256;
+    const size_t stage = mea::combine_stage_floats(pl.n_splits, bh * p->n_q, p->d);
+    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256 + (stage ? stage * 4 + 256 : 0);
   }
   return pl;
 }
@@ -117,7 +118,8 @@ FwdPlan plan_fwd(const mea_problem* p) {
   pl.workspace = 0;
   if (pl.n_splits > 1) {
     const size_t rows = (size_t)pl.n_splits * (size_t)bh * (size_t)p->n_q;
-    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256;
+    const size_t stage = mea::combine_stage_floats(pl.n_splits, bh * p->n_q, p->d);
+    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256 + (stage ? stage * 4 + 256 : 0);
   }
   return pl;
 }
@@ -209,6 +211,13 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
     fp.part_o = align256(workspace, 0);
     fp.part_m = fp.part_o + rows * (size_t)p->d;
     fp.part_l = fp.part_m + rows;
+    const int64_t rows1 = (int64_t)fp.bh * p->n_q;
+    if (mea::combine_stage_floats(pl.n_splits, rows1, p->d) > 0) {
+      const size_t r2 = (size_t)((pl.n_splits + mea::kCombineGroup - 1) / mea::kCombineGroup) * (size_t)rows1;
+      fp.part2_o = align256(fp.part_l + rows, 0);
+      fp.part2_m = fp.part2_o + r2 * (size_t)p->d;
+      fp.part2_l = fp.part2_m + r2;
+    }
   }
   const int64_t grid = (int64_t)fp.n_qtiles * fp.bh * fp.n_splits;
   if (grid >= ((int64_t)1 << 31)) return MEA_ERR_INVALID_ARG;

@@ -795,7 +795,82 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
   if (f0 == 0 && p.lse) p.lse[row] = (m_g + __log2f(l)) * kLn2;
 }
 
+// One stage of the combine: each output range g summarises input ranges
+// g G .. g G + G - 1 (fewer at the end) of the same row: maximum m_g, and the
+// numerator and denominator rescaled by 2^(m_s - m_g) and added -- the same
+// algebra as the final combine, without the division.  One thread per
+// (row, output range, 4 features); the G inputs are read together.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_stage_kernel(const float* __restrict__ po,
+                                                                 const float* __restrict__ pm,
+                                                                 const float* __restrict__ pl, int s_in,
+                                                                 float* __restrict__ qo, float* __restrict__ qm,
+                                                                 float* __restrict__ ql, int s_out, int64_t rows) {
+  constexpr int G4 = D / 4;
+  constexpr int G = kCombineGroup;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= rows * s_out * G4) return;
+  const int64_t row = gid / ((int64_t)s_out * G4);
+  const int rem = (int)(gid % ((int64_t)s_out * G4));
+  const int g = rem / G4, f0 = 4 * (rem % G4);
+  const int s0 = g * G;
+  const int n = s_in - s0 < G ? s_in - s0 : G;
+  float ms[G];
+#pragma unroll
+  for (int i = 0; i < G; ++i) ms[i] = i < n ? pm[(size_t)(s0 + i) * rows + row] : -INFINITY;
+  float m_g = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < G; ++i) m_g = fmaxf(m_g, ms[i]);
+  float l = 0.0f;
+  f32x4 o = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    if (i < n) {
+      const size_t prow = (size_t)(s0 + i) * rows + row;
+      const float wgt = ms[i] == -INFINITY ? 0.0f : fast_exp2(ms[i] - m_g);
+      l += wgt * pl[prow];
+      o += wgt * *reinterpret_cast<const f32x4*>(po + prow * D + f0);
+    }
+  }
+  const size_t orow = (size_t)g * rows + row;
+  *reinterpret_cast<f32x4*>(qo + orow * D + f0) = o;
+  if (f0 == 0) {
+    qm[orow] = m_g;
+    ql[orow] = l;
+  }
+}
+
 // ---------------------------------------------------------------- launchers
+
+// Combine of the key ranges' summaries into o and lse: stages of
+// kCombineGroup ranges while more remain, alternating between the two
+// partial buffers, then the final combine.
+template <typename TO, int D>
+static hipError_t launch_combine(const FwdParams& p, hipStream_t stream) {
+  FwdParams pf = p;
+  const int64_t rows = (int64_t)p.bh * p.n_q;
+  bool in_first = true;
+  while (pf.n_splits > kCombineGroup) {
+    const int s_out = (pf.n_splits + kCombineGroup - 1) / kCombineGroup;
+    float* qo = in_first ? p.part2_o : p.part_o;
+    float* qm = in_first ? p.part2_m : p.part_m;
+    float* ql = in_first ? p.part2_l : p.part_l;
+    const int64_t threads = rows * s_out * (D / 4);
+    hipLaunchKernelGGL(attn_combine_stage_kernel<D>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                       stream, pf.part_o, pf.part_m, pf.part_l, pf.n_splits, qo, qm, ql, s_out, rows);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    pf.part_o = qo;
+    pf.part_m = qm;
+    pf.part_l = ql;
+    pf.n_splits = s_out;
+    in_first = !in_first;
+  }
+  void* args[] = {&pf};
+  const int64_t threads = rows * (D / 4);
+  return hipLaunchKernel(reinterpret_cast<const void*>(attn_combine_kernel<TO, D>),
+                         dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, stream);
+}
 
 template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
 static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
@@ -807,10 +882,7 @@ static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid),
                                  dim3(Cfg::NT), args, Cfg::LDS_BYTES, stream);
   if (e != hipSuccess || p.n_splits == 1) return e;
-  auto comb = attn_combine_kernel<TO, D>;
-  const int64_t threads = (int64_t)p.bh * p.n_q * (D / 4);
-  return hipLaunchKernel(reinterpret_cast<const void*>(comb), dim3((unsigned)((threads + 255) / 256)),
-                         dim3(256), args, 0, stream);
+  return launch_combine<TO, D>(p, stream);
 }
 
 template <typename T, typename TO, bool CAUSAL>
@@ -822,10 +894,7 @@ static hipError_t launch_fwd_pp(const FwdParams& p, hipStream_t stream) {
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid),
                                  dim3(pp::NW * 64), args, 0, stream);
   if (e != hipSuccess || p.n_splits == 1) return e;
-  auto comb = attn_combine_kernel<TO, pp::D>;
-  const int64_t threads = (int64_t)p.bh * p.n_q * (pp::D / 4);
-  return hipLaunchKernel(reinterpret_cast<const void*>(comb), dim3((unsigned)((threads + 255) / 256)),
-                         dim3(256), args, 0, stream);
+  return launch_combine<TO, pp::D>(p, stream);
 }
 
 template <typename T, typename TO, int D>
@@ -842,15 +911,6 @@ static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t str
 template <typename T, int D>
 static hipError_t launch_fwd_out(const FwdParams& p, bool causal, bool out_f32, hipStream_t stream) {
   return out_f32 ? launch_fwd_dt<T, float, D>(p, causal, stream) : launch_fwd_dt<T, T, D>(p, causal, stream);
-}
-
-template <typename TO, int D>
-static hipError_t launch_combine(const FwdParams& p, hipStream_t stream) {
-  FwdParams pc = p;
-  void* args[] = {&pc};
-  const int64_t threads = (int64_t)p.bh * p.n_q * (D / 4);
-  return hipLaunchKernel(reinterpret_cast<const void*>(attn_combine_kernel<TO, D>),
-                         dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, stream);
 }
 
 hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, bool out_f32,

@@ -16,6 +16,11 @@ struct FwdParams {
   float* part_o;  // split partials [S, B*H, n_q, D] (n_splits > 1)
   float* part_m;  // [S, B*H, n_q]
   float* part_l;  // [S, B*H, n_q]
+  // Second partial buffer for the staged combine (n_splits > kCombineGroup):
+  // ceil(S / kCombineGroup) splits in the same layout.
+  float* part2_o;
+  float* part2_m;
+  float* part2_l;
   int64_t n_q;
   int64_t n_k;
   int64_t keys_per_split;  // multiple of the key tile
@@ -25,6 +30,18 @@ struct FwdParams {
   float scale;       // score scale
   float scale_log2;  // scale * log2(e)
 };
+
+// The summaries of more than kCombineGroup key ranges are combined in stages
+// of kCombineGroup ranges each (Section 4's combine applied as a tree), so
+// that the work stays parallel when there are few rows and many ranges.
+constexpr int kCombineGroup = 16;
+
+// Floats of the second partial buffer (0 when the combine is one stage).
+inline size_t combine_stage_floats(int64_t n_splits, int64_t rows, int64_t d) {
+  if (n_splits <= kCombineGroup) return 0;
+  const int64_t s1 = (n_splits + kCombineGroup - 1) / kCombineGroup;
+  return (size_t)s1 * (size_t)rows * (size_t)(d + 2);
+}
 
 // Arguments of the backward kernels.
 struct BwdParams {

@@ -112,3 +112,12 @@ def test_decode_full_size_sampled(name):
         print("  slice", (b, h), "rel_err O %.3g LSE %.3g" % (eo, el), flush=True)
         assert eo <= TOL[w.dtype] and el <= TOL[w.dtype], (b, h, eo, el)
     assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+
+
+def test_decode_staged_combine_long_keys():
+    # 2^22 keys for one (batch, head): 1024 key ranges, combined in three
+    # stages of 16 ranges and a final combine (Section 4's combine as a tree).
+    B, H, nq, nk, d = 1, 1, 2, 1 << 22, 64
+    ws = _lib.fwd_workspace_size(_lib.problem(B, H, nq, nk, d, 2, False, d ** -0.5))
+    assert ws > 1024 * nq * (d + 2) * 4  # room for the ranges and the stage buffer
+    check(B, H, nq, nk, d, "bf16")
