@@ -15,9 +15,12 @@
  * (the checkpointing of Section 5.2) from the saved per-row log-sum-exp.
  *
  * Conventions shared by every entry point:
- *   - Layout: contiguous row-major [batch, heads, n, d], feature index
- *     innermost; q, o, do, dq are [B, H, n_q, d]; k, v, dk, dv are
- *     [B, H, n_k, d]; lse is [B, H, n_q] float32.
+ *   - Layout: q, o, do, dq are [B, H, n_q, d]; k, v, dk, dv are
+ *     [B, H, n_k, d]; by default contiguous row-major with the feature index
+ *     innermost, or with the batch, head and row strides given per tensor in
+ *     mea_problem.strides (features always contiguous), which covers the
+ *     paper's [n, heads, d] layout and views into a packed QKV projection;
+ *     lse is always contiguous [B, H, n_q] float32.
  *   - Pointers: q, k, v, o, do, dq, dk, dv, lse and workspace are DEVICE
  *     pointers, 16-byte aligned.  The mea_problem pointer is a HOST pointer.
  *   - Ownership: the caller allocates every buffer, including the workspace.
@@ -61,6 +64,22 @@ typedef enum {
 
 typedef enum { MEA_F32 = 0, MEA_F16 = 1, MEA_BF16 = 2 } mea_dtype;
 
+/* Element strides of one [B, H, n, d] tensor: element (b, h, i, f) is at
+ * b * batch + h * head + i * row + f.  Every stride is a multiple of 16 bytes
+ * (8 elements for 16-bit types, 4 for float32) and row is in [d, 2^24); batch
+ * and head may be 0 for inputs (one head's keys shared by several query
+ * heads), not for outputs.  The library does not check that the rows of an
+ * output are disjoint beyond that. */
+typedef struct {
+  int64_t batch, head, row;
+} mea_tensor_strides;
+
+/* Strides of every tensor of a call (the backward's tensors unused by a call
+ * are ignored, and the forward reads only q, k, v, o). */
+typedef struct {
+  mea_tensor_strides q, k, v, o, d_o, dq, dk, dv;
+} mea_strides;
+
 /* Problem description (host memory, read during the call only). */
 typedef struct {
   int64_t batch;  /* B >= 1 */
@@ -74,6 +93,8 @@ typedef struct {
   int32_t out_f32; /* 0: o and do in `dtype`; 1: o and do in float32 (the
                       paper's experiments use 16-bit inputs with a float32
                       output, Section 5.1); ignored when dtype is MEA_F32 */
+  const mea_strides* strides; /* HOST pointer or NULL (every tensor contiguous
+                                 [B, H, n, d]); read during the call only */
 } mea_problem;
 
 /* Bytes of device workspace mea_attention_fwd needs for `p` (written to

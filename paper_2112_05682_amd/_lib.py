@@ -29,6 +29,18 @@ EXPORTS = (
 )
 
 
+class MeaTensorStrides(ctypes.Structure):
+    """Mirror of ``mea_tensor_strides`` (elements)."""
+
+    _fields_ = [("batch", ctypes.c_int64), ("head", ctypes.c_int64), ("row", ctypes.c_int64)]
+
+
+class MeaStrides(ctypes.Structure):
+    """Mirror of ``mea_strides``."""
+
+    _fields_ = [(name, MeaTensorStrides) for name in ("q", "k", "v", "o", "d_o", "dq", "dk", "dv")]
+
+
 class MeaProblem(ctypes.Structure):
     """Mirror of ``mea_problem``."""
 
@@ -42,6 +54,7 @@ class MeaProblem(ctypes.Structure):
         ("causal", ctypes.c_int32),
         ("scale", ctypes.c_float),
         ("out_f32", ctypes.c_int32),
+        ("strides", ctypes.POINTER(MeaStrides)),
     ]
 
 
@@ -88,9 +101,22 @@ def check(name: str, status: int) -> None:
         raise MeaError(name, status, status_string(status))
 
 
-def problem(batch, heads, n_q, n_k, d, dtype, causal, scale, out_f32=False) -> MeaProblem:
-    return MeaProblem(int(batch), int(heads), int(n_q), int(n_k), int(d), int(dtype),
-                      int(bool(causal)), float(scale), int(bool(out_f32)))
+def problem(batch, heads, n_q, n_k, d, dtype, causal, scale, out_f32=False,
+            strides: dict | None = None) -> MeaProblem:
+    """``strides`` maps tensor names (q, k, v, o, d_o, dq, dk, dv) to
+    (batch, head, row) element strides; missing names and None mean contiguous
+    [B, H, n, d]."""
+    p = MeaProblem(int(batch), int(heads), int(n_q), int(n_k), int(d), int(dtype),
+                   int(bool(causal)), float(scale), int(bool(out_f32)), None)
+    if strides:
+        st = MeaStrides()
+        for name, n in (("q", n_q), ("k", n_k), ("v", n_k), ("o", n_q), ("d_o", n_q),
+                        ("dq", n_q), ("dk", n_k), ("dv", n_k)):
+            bs, hs, rs = strides.get(name) or (int(heads) * int(n) * int(d), int(n) * int(d), int(d))
+            setattr(st, name, MeaTensorStrides(int(bs), int(hs), int(rs)))
+        p._strides_keepalive = st  # the struct must outlive the calls that read it
+        p.strides = ctypes.pointer(st)
+    return p
 
 
 def fwd_workspace_size(p: MeaProblem) -> int:

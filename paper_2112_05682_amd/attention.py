@@ -2,7 +2,10 @@
 through torch, and the current HIP stream.  Every step of the computation runs
 in the HIP kernels of ``libmea.so``; nothing here computes attention.
 
-Tensors are ``[B, H, n, d]``, contiguous, on one GPU; q, k, v and the
+Tensors are ``[B, H, n, d]`` on one GPU with contiguous features; their batch,
+head and row strides are passed to the kernels, so views such as the paper's
+``[n, heads, d]`` layout (a transpose of ``[B, n, H, d]``) or slices of a
+packed QKV projection are read and written in place.  q, k, v and the
 gradients share one dtype (float32, float16 or bfloat16), o and do share it or
 are float32 (16-bit inputs with a float32 output, as in the paper's
 experiments); d must be 64 or 128.
@@ -19,7 +22,10 @@ _DTYPE_CODE = {torch.float32: _lib.MEA_F32, torch.float16: _lib.MEA_F16,
                torch.bfloat16: _lib.MEA_BF16}
 
 
-def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: bool = False):
+def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: bool = False,
+             tensors: dict | None = None):
+    """``tensors`` maps ABI tensor names (q, k, v, o, d_o, dq, dk, dv) to the
+    tensors of a call, whose strides are passed when any is not contiguous."""
     if q.dim() != 4 or k.dim() != 4:
         raise ValueError("q and k must be [B, H, n, d]")
     B, H, n_q, d = q.shape
@@ -28,8 +34,11 @@ def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: boo
         raise TypeError("unsupported dtype %s" % q.dtype)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
+    strides = None
+    if tensors and any(not t.is_contiguous() for t in tensors.values() if t is not None):
+        strides = {name: tuple(t.stride()[:3]) for name, t in tensors.items() if t is not None}
     return _lib.problem(B, H, n_q, n_k, d, _DTYPE_CODE[q.dtype], causal, scale,
-                        out_f32 and q.dtype != torch.float32)
+                        out_f32 and q.dtype != torch.float32, strides)
 
 
 def _check_tensors(names, tensors, dtype, device):
@@ -40,8 +49,15 @@ def _check_tensors(names, tensors, dtype, device):
             raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
         if t.dtype != dtype:
             raise TypeError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
-        if not t.is_contiguous():
-            raise ValueError("%s must be contiguous" % name)
+        if name == "lse":
+            if not t.is_contiguous():
+                raise ValueError("lse must be contiguous")
+            continue
+        if t.dim() != 4 or t.stride(3) != 1:
+            raise ValueError("%s must be [B, H, n, d] with contiguous features" % name)
+        unit = 16 // t.element_size()
+        if t.data_ptr() % 16 or any(st_ % unit for st_ in t.stride()[:3]):
+            raise ValueError("%s: data pointer and strides must be multiples of 16 bytes" % name)
 
 
 def _stream(device) -> int:
@@ -68,9 +84,12 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: boo
     out_dtype = q.dtype if out_dtype is None else out_dtype
     if out_dtype not in (q.dtype, torch.float32):
         raise TypeError("out_dtype must be q's dtype or float32")
-    p = _problem(q, k, causal, scale, out_dtype == torch.float32)
     o = torch.empty(q.shape, dtype=out_dtype, device=q.device) if out is None else out
     _check_tensors(("out",), (o,), out_dtype, q.device)
+    if o.shape != q.shape:
+        raise ValueError("out must have q's shape")
+    p = _problem(q, k, causal, scale, out_dtype == torch.float32,
+                 {"q": q, "k": k, "v": v, "o": o})
     lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if need_lse else None
     ws_bytes = _lib.fwd_workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device) if ws_bytes else None
@@ -82,9 +101,10 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: boo
 
 
 def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None = None,
-                  need_dq: bool = True, need_dkdv: bool = True):
+                  need_dq: bool = True, need_dkdv: bool = True, out=None):
     """Returns ``(dq, dk, dv)`` for the upstream gradient ``do``; a gradient that
-    is not needed is returned as None and its kernel is not run."""
+    is not needed is returned as None and its kernel is not run.  ``out`` may
+    give the (dq, dk, dv) tensors to write (any may be None: allocated)."""
     _check_tensors(("q", "k", "v"), (q, k, v), q.dtype, q.device)
     if o.dtype not in (q.dtype, torch.float32):
         raise TypeError("o must have q's dtype or float32")
@@ -94,10 +114,20 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
         raise ValueError("o, do must match q and lse must be [B, H, n_q]")
     if not (need_dq or need_dkdv):
         raise ValueError("nothing to compute")
-    p = _problem(q, k, causal, scale, o.dtype == torch.float32)
-    dq = torch.empty_like(q) if need_dq else None
-    dk = torch.empty_like(k) if need_dkdv else None
-    dv = torch.empty_like(v) if need_dkdv else None
+    given = out if out is not None else (None, None, None)
+    dq = (given[0] if given[0] is not None else torch.empty(q.shape, dtype=q.dtype, device=q.device)) \
+        if need_dq else None
+    dk = (given[1] if given[1] is not None else torch.empty(k.shape, dtype=k.dtype, device=k.device)) \
+        if need_dkdv else None
+    dv = (given[2] if given[2] is not None else torch.empty(v.shape, dtype=v.dtype, device=v.device)) \
+        if need_dkdv else None
+    outs = [(n_, t) for n_, t in (("dq", dq), ("dk", dk), ("dv", dv)) if t is not None]
+    _check_tensors([n_ for n_, _ in outs], [t for _, t in outs], q.dtype, q.device)
+    for n_, t in outs:
+        if t.shape != (q.shape if n_ == "dq" else k.shape):
+            raise ValueError("%s has the wrong shape" % n_)
+    p = _problem(q, k, causal, scale, o.dtype == torch.float32,
+                 {"q": q, "k": k, "v": v, "o": o, "d_o": do, "dq": dq, "dk": dk, "dv": dv})
     ws_bytes = _lib.bwd_workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     _lib.check("mea_attention_bwd", _lib.bwd(
@@ -114,7 +144,7 @@ class MemoryEfficientAttention(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, q, k, v, causal=False, scale=None, out_dtype=None):
-        q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
+        q, k, v = (_feature_contiguous(t) for t in (q, k, v))
         o, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out_dtype=out_dtype)
         ctx.save_for_backward(q, k, v, o, lse)
         ctx.causal = causal
@@ -124,9 +154,56 @@ class MemoryEfficientAttention(torch.autograd.Function):
     @staticmethod
     def backward(ctx, do):
         q, k, v, o, lse = ctx.saved_tensors
-        dq, dk, dv = attention_bwd(q, k, v, o, lse, do.to(o.dtype).contiguous(), ctx.causal,
+        dq, dk, dv = attention_bwd(q, k, v, o, lse, _feature_contiguous(do.to(o.dtype)), ctx.causal,
                                    ctx.scale)
         return dq, dk, dv, None, None, None
+
+
+def _feature_contiguous(t: torch.Tensor) -> torch.Tensor:
+    """t itself when the kernels can read it in place (contiguous features,
+    16-byte aligned pointer and strides), else a contiguous copy."""
+    unit = 16 // t.element_size()
+    if t.dim() == 4 and t.stride(3) == 1 and t.data_ptr() % 16 == 0 and \
+            all(st_ % unit == 0 for st_ in t.stride()[:3]):
+        return t
+    return t.contiguous()
+
+
+class PackedQKVAttention(torch.autograd.Function):
+    """Self-attention on the output of one fused QKV projection, ``qkv`` of
+    shape ``[B, n, 3, H, d]``: q, k and v are read as strided views of it, the
+    output is ``[B, n, H, d]`` (so ``reshape(B, n, H * d)`` is free) and the
+    gradient is written as one packed ``[B, n, 3, H, d]`` tensor -- neither
+    direction copies or transposes.  Saves qkv, o and the O(n) lse."""
+
+    @staticmethod
+    def forward(ctx, qkv, causal=False, scale=None):
+        if qkv.dim() != 5 or qkv.shape[2] != 3:
+            raise ValueError("qkv must be [B, n, 3, H, d]")
+        qkv = qkv if qkv.is_contiguous() else qkv.contiguous()
+        B, n, _, H, d = qkv.shape
+        q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))  # [B, H, n, d] views
+        o = torch.empty(B, n, H, d, dtype=qkv.dtype, device=qkv.device)
+        _, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out=o.transpose(1, 2))
+        ctx.save_for_backward(qkv, o, lse)
+        ctx.causal, ctx.scale = causal, scale
+        return o
+
+    @staticmethod
+    def backward(ctx, do):
+        qkv, o, lse = ctx.saved_tensors
+        q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))
+        dqkv = torch.empty_like(qkv)
+        dq, dk, dv = (dqkv[:, :, i].transpose(1, 2) for i in range(3))
+        do_ = _feature_contiguous(do.to(o.dtype).transpose(1, 2))
+        attention_bwd(q, k, v, o.transpose(1, 2), lse, do_, ctx.causal, ctx.scale, out=(dq, dk, dv))
+        return dqkv, None, None
+
+
+def attention_packed(qkv, causal: bool = False, scale: float | None = None):
+    """Exact softmax self-attention of a packed ``[B, n, 3, H, d]`` projection,
+    differentiable, O(n) extra memory; returns ``[B, n, H, d]``."""
+    return PackedQKVAttention.apply(qkv, causal, scale)
 
 
 def attention(q, k, v, causal: bool = False, scale: float | None = None,

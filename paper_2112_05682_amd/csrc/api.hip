@@ -41,6 +41,28 @@ mea_status check_problem(const mea_problem* p) {
   return MEA_OK;
 }
 
+// Strides of a tensor of n rows: given, or contiguous [B, H, n, d].
+mea::TensorStrides strides_of(const mea_problem* p, const mea_tensor_strides* given, int64_t n) {
+  if (given) return {given->batch, given->head, given->row};
+  return {p->heads * n * p->d, n * p->d, p->d};
+}
+
+// Validation of one tensor's strides (see mea.h).
+bool strides_ok(const mea_problem* p, const mea::TensorStrides& s, int64_t n, bool output, size_t elem) {
+  const int64_t align = 16 / (int64_t)elem;
+  if (s.b < 0 || s.h < 0 || s.r < p->d || s.r >= ((int64_t)1 << 24)) return false;
+  if (output && (s.b == 0 || s.h == 0)) return false;
+  if (s.b % align || s.h % align || s.r % align) return false;
+  int64_t a, b, c, tot;
+  if (!mul_ok(p->batch - 1, s.b, &a) || !mul_ok(p->heads - 1, s.h, &b) || !mul_ok(n - 1, s.r, &c)) return false;
+  if (__builtin_add_overflow(a, b, &tot) || __builtin_add_overflow(tot, c, &tot) ||
+      __builtin_add_overflow(tot, p->d, &tot))
+    return false;
+  return true;
+}
+
+size_t elem_size(int32_t dtype) { return dtype == MEA_F32 ? 4 : 2; }
+
 bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 bool dev_ptr_ok(const void* ptr) { return ptr != nullptr && aligned16(ptr); }
 
@@ -206,6 +228,18 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
   fp.n_splits = pl.n_splits;
   fp.scale = p->scale;
   fp.scale_log2 = p->scale * kLog2e;
+  fp.heads = (int)p->heads;
+  {
+    const mea_strides* st_ = p->strides;
+    const size_t e = elem_size(p->dtype), eo = p->out_f32 && p->dtype != MEA_F32 ? 4 : e;
+    fp.sq = strides_of(p, st_ ? &st_->q : nullptr, p->n_q);
+    fp.sk = strides_of(p, st_ ? &st_->k : nullptr, p->n_k);
+    fp.sv = strides_of(p, st_ ? &st_->v : nullptr, p->n_k);
+    fp.so = strides_of(p, st_ ? &st_->o : nullptr, p->n_q);
+    if (!strides_ok(p, fp.sq, p->n_q, false, e) || !strides_ok(p, fp.sk, p->n_k, false, e) ||
+        !strides_ok(p, fp.sv, p->n_k, false, e) || !strides_ok(p, fp.so, p->n_q, true, eo))
+      return MEA_ERR_INVALID_ARG;
+  }
   if (pl.n_splits > 1) {
     const size_t rows = (size_t)pl.n_splits * (size_t)fp.bh * (size_t)p->n_q;
     fp.part_o = align256(workspace, 0);
@@ -264,6 +298,24 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   bp.bh = (int)(p->batch * p->heads);
   bp.scale = p->scale;
   bp.scale_log2 = p->scale * kLog2e;
+  bp.heads = (int)p->heads;
+  {
+    const mea_strides* st_ = p->strides;
+    const size_t e = elem_size(p->dtype), eo = p->out_f32 && p->dtype != MEA_F32 ? 4 : e;
+    bp.sq = strides_of(p, st_ ? &st_->q : nullptr, p->n_q);
+    bp.sk = strides_of(p, st_ ? &st_->k : nullptr, p->n_k);
+    bp.sv = strides_of(p, st_ ? &st_->v : nullptr, p->n_k);
+    bp.so = strides_of(p, st_ ? &st_->o : nullptr, p->n_q);
+    bp.sdo = strides_of(p, st_ ? &st_->d_o : nullptr, p->n_q);
+    bp.sdq = strides_of(p, st_ ? &st_->dq : nullptr, p->n_q);
+    bp.sdk = strides_of(p, st_ ? &st_->dk : nullptr, p->n_k);
+    bp.sdv = strides_of(p, st_ ? &st_->dv : nullptr, p->n_k);
+    if (!strides_ok(p, bp.sq, p->n_q, false, e) || !strides_ok(p, bp.sk, p->n_k, false, e) ||
+        !strides_ok(p, bp.sv, p->n_k, false, e) || !strides_ok(p, bp.so, p->n_q, false, eo) ||
+        !strides_ok(p, bp.sdo, p->n_q, false, eo) || (dq && !strides_ok(p, bp.sdq, p->n_q, true, e)) ||
+        (dk && (!strides_ok(p, bp.sdk, p->n_k, true, e) || !strides_ok(p, bp.sdv, p->n_k, true, e))))
+      return MEA_ERR_INVALID_ARG;
+  }
   const hipError_t e = mea::launch_bwd(bp, p->dtype, (int)p->d, p->causal != 0, p->out_f32 != 0, stream);
   if (e == hipErrorNotSupported) return MEA_ERR_UNSUPPORTED;
   return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;

@@ -57,8 +57,10 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
   float acc = 0.0f;
   if (real) {
     typedef T vec16 __attribute__((ext_vector_type(16 / E)));
-    const vec16 o = *reinterpret_cast<const vec16*>(static_cast<const T*>(p.o) + row * D + part * (16 / E));
-    const vec16 g = *reinterpret_cast<const vec16*>(static_cast<const T*>(p.d_o) + row * D + part * (16 / E));
+    const T* orow = static_cast<const T*>(p.o) + head_base(p.so, (int)bh, p.heads) + i * p.so.r;
+    const T* grow = static_cast<const T*>(p.d_o) + head_base(p.sdo, (int)bh, p.heads) + i * p.sdo.r;
+    const vec16 o = *reinterpret_cast<const vec16*>(orow + part * (16 / E));
+    const vec16 g = *reinterpret_cast<const vec16*>(grow + part * (16 / E));
 #pragma unroll
     for (int e = 0; e < 16 / E; ++e) acc = fmaf((float)o[e], (float)g[e], acc);
   }
@@ -122,20 +124,20 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   const int64_t kw = k0 + 32 * wave;
   const int64_t key = kw + c;
 
-  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + head_base(p.sq, bh, p.heads);
+  const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + head_base(p.sdo, bh, p.heads);
   const float* __restrict__ sinitg = p.s_init + (size_t)bh * p.n_q_pad;
   const float* __restrict__ dpinitg = p.dp_init + (size_t)bh * p.n_q_pad;
-  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
-  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   // K^T and V^T as B operands: lane (h, key c) holds row `key`, k = 16kc + 8h + s.
   Frag<T> kf[KC], vf[KC];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
     if (key < p.n_k) {
-      kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * D + 16 * kc + 8 * h);
-      vf[kc] = *reinterpret_cast<const Frag<T>*>(vg + key * D + 16 * kc + 8 * h);
+      kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * p.sk.r + 16 * kc + 8 * h);
+      vf[kc] = *reinterpret_cast<const Frag<T>*>(vg + key * p.sv.r + 16 * kc + 8 * h);
     } else {
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
@@ -172,11 +174,11 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
         const int rem = chunk % (Cfg::BQ * Cfg::CPR);
         const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
         const int64_t q = q0 + row;
-        const int64_t off = q * D + col * (16 / Cfg::E);
+        const int64_t coff = col * (16 / Cfg::E);
         if (q >= p.n_q)
           stage[i] = u32x4{0u, 0u, 0u, 0u};
         else
-          stage[i] = which ? ld_chunk_as<T, TO>(dog + off) : ld16(qg + off);
+          stage[i] = which ? ld_chunk_as<T, TO>(dog + q * p.sdo.r + coff) : ld16(qg + q * p.sq.r + coff);
       }
     }
     if (tid < 2 * Cfg::BQ) {
@@ -301,16 +303,16 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   }
 
   // Accumulators: lane (h, feature c), register r <-> key kw + c_row(r, h).
-  T* dkg = static_cast<T*>(p.dk) + (size_t)bh * p.n_k * D;
-  T* dvg = static_cast<T*>(p.dv) + (size_t)bh * p.n_k * D;
+  T* dkg = static_cast<T*>(p.dk) + head_base(p.sdk, bh, p.heads);
+  T* dvg = static_cast<T*>(p.dv) + head_base(p.sdv, bh, p.heads);
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int64_t kr = kw + c_row(r, h);
       if (kr < p.n_k) {
-        dkg[kr * D + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
-        dvg[kr * D + 32 * dt + c] = (T)dv[dt][r];
+        dkg[kr * p.sdk.r + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
+        dvg[kr * p.sdv.r + 32 * dt + c] = (T)dv[dt][r];
       }
     }
 }
@@ -356,18 +358,18 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   const int64_t kw = k0 + 32 * wave;
   const int64_t key = kw + c;
 
-  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + head_base(p.sq, bh, p.heads);
+  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + head_base(p.sdo, bh, p.heads);
   const uint4* __restrict__ recg = p.row_rec + (size_t)bh * p.n_q_pad;
-  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
-  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   Frag<T> kf[KC], vf[KC];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
     if (key < p.n_k) {
-      kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * D + 16 * kc + 8 * h);
-      vf[kc] = *reinterpret_cast<const Frag<T>*>(vg + key * D + 16 * kc + 8 * h);
+      kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * p.sk.r + 16 * kc + 8 * h);
+      vf[kc] = *reinterpret_cast<const Frag<T>*>(vg + key * p.sv.r + 16 * kc + 8 * h);
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -398,12 +400,16 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // chunk 7), unit 18 the per-row records (lane l: row l; the padded record
   // array holds every row of the tile).  Query rows past n_q repeat the last
   // row (finite values; their weights are 0).
-  constexpr int ROWB = D * (int)sizeof(T);
   const int n_full = n_iters > 0 ? (int)((p.n_q - q_begin) / BQ) : 0;  // tiles with no row past n_q
+  auto unit_row = [&](int u) { return (64 * (u % 9) + lane) / 9; };
+  auto unit_col = [&](int u) {
+    const int ch = (64 * (u % 9) + lane) % 9;
+    return (unsigned)(16 * (ch < 8 ? ch : 7));
+  };
+  // Byte offset within a tile (row strides < 2^24 elements, checked on the host).
   auto unit_off = [&](int u) {
-    const int slot = 64 * (u % 9) + lane;
-    const int ch = slot % 9;
-    return (unsigned)((slot / 9) * ROWB + 16 * (ch < 8 ? ch : 7));
+    const unsigned rsb = (unsigned)sizeof(T) * (unsigned)(u >= 9 ? p.sdo.r : p.sq.r);
+    return (unsigned)unit_row(u) * rsb + unit_col(u);
   };
   auto copy_unit = [&](int i, int u, unsigned off) __attribute__((always_inline)) {
     const int64_t q0 = q_begin + (int64_t)i * BQ;
@@ -411,13 +417,14 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
     if (u < UNITS - 1) {
       const int which = u >= 9, v9 = u - 9 * which;
       const T* g = which ? dog : qg;
+      const int64_t rs = which ? p.sdo.r : p.sq.r;
       const unsigned lds = __builtin_amdgcn_readfirstlane(lds_addr(st + which * TILEB + 1024 * v9));
       if (i < n_full) {
-        copy_to_lds16_sb(g + q0 * D, off, lds);
+        copy_to_lds16_sb(g + q0 * rs, off, lds);
       } else {
-        int64_t q = q0 + off / ROWB;
+        int64_t q = q0 + unit_row(u);
         if (q > p.n_q - 1) q = p.n_q - 1;
-        copy_to_lds16(reinterpret_cast<const unsigned char*>(g + q * D) + off % ROWB, lds);
+        copy_to_lds16(reinterpret_cast<const unsigned char*>(g + q * rs) + unit_col(u), lds);
       }
     } else {
       copy_to_lds16(recg + q0 + lane, __builtin_amdgcn_readfirstlane(lds_addr(st + 2 * TILEB)));
@@ -642,16 +649,16 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // that no wave leaves while the other group still waits at a barrier.
   if (grp == 0) barrier();
 
-  T* dkg = static_cast<T*>(p.dk) + (size_t)bh * p.n_k * D;
-  T* dvg = static_cast<T*>(p.dv) + (size_t)bh * p.n_k * D;
+  T* dkg = static_cast<T*>(p.dk) + head_base(p.sdk, bh, p.heads);
+  T* dvg = static_cast<T*>(p.dv) + head_base(p.sdv, bh, p.heads);
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int64_t kr = kw + c_row(r, h);
       if (kr < p.n_k) {
-        dkg[kr * D + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
-        dvg[kr * D + 32 * dt + c] = (T)dv[dt][r];
+        dkg[kr * p.sdk.r + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
+        dvg[kr * p.sdv.r + 32 * dt + c] = (T)dv[dt][r];
       }
     }
 }
@@ -687,10 +694,10 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   const int64_t q0 = (int64_t)qtile * BQ;
   const int64_t qw = q0 + 32 * QT * wave;  // first query of this wave
 
-  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
-  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + head_base(p.sq, bh, p.heads);
+  const TO* __restrict__ dog = static_cast<const TO*>(p.d_o) + head_base(p.sdo, bh, p.heads);
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   // Q^T and dO^T as B operands: lane (h, query c of sub-tile t), k = 16kc + 8h + s.
   // Initial values of the S^T and dP^T accumulators of each query: -lse/scale
@@ -704,8 +711,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       if (valid) {
-        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
-        gf[t][kc] = ld_frag_as<T, TO>(dog + query * D + 16 * kc + 8 * h);
+        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + query * p.sq.r + 16 * kc + 8 * h);
+        gf[t][kc] = ld_frag_as<T, TO>(dog + query * p.sdo.r + 16 * kc + 8 * h);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -740,7 +747,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
       const int rem = chunk % (BK * CPR);
       const int row = rem / CPR, col = rem % CPR;
       const int64_t kr = k0 + row;
-      const T* src = (which ? vg : kg) + kr * D + col * (16 / E);
+      const T* src = (which ? vg + kr * p.sv.r : kg + kr * p.sk.r) + col * (16 / E);
       stage[i] = kr < p.n_k ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
     }
   };
@@ -863,7 +870,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   for (int t = 0; t < QT; ++t) {
     const int64_t query = qw + 32 * t + c;
     if (query >= p.n_q) continue;
-    T* dqg = static_cast<T*>(p.dq) + ((size_t)bh * p.n_q + query) * D;
+    T* dqg = static_cast<T*>(p.dq) + head_base(p.sdq, bh, p.heads) + query * p.sdq.r;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -914,10 +921,10 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   const int64_t qw = q0 + 32 * wave;  // first query of this wave
   const int64_t query = qw + c;
 
-  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
-  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + head_base(p.sq, bh, p.heads);
+  const T* __restrict__ dog = static_cast<const T*>(p.d_o) + head_base(p.sdo, bh, p.heads);
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   // Q^T and dO^T as B operands: lane (h, query c), k = 16 kc + 8 h + s.
   Frag<T> qf[KC], gf[KC];
@@ -925,8 +932,8 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
     if (valid) {
-      qf[kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
-      gf[kc] = *reinterpret_cast<const Frag<T>*>(dog + query * D + 16 * kc + 8 * h);
+      qf[kc] = *reinterpret_cast<const Frag<T>*>(qg + query * p.sq.r + 16 * kc + 8 * h);
+      gf[kc] = *reinterpret_cast<const Frag<T>*>(dog + query * p.sdo.r + 16 * kc + 8 * h);
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -962,24 +969,29 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   // lane's byte offset within a tile is computed once per unit; a tile that
   // ends past n_k takes the clamped path, whose rows past n_k repeat the last
   // key (finite values; masked).
-  constexpr int ROWB = D * (int)sizeof(T);
   const int n_full = (int)(p.n_k / BK);  // tiles with no key past n_k
+  auto unit_row = [&](int u) { return (64 * (u % 9) + lane) / 9; };
+  auto unit_col = [&](int u) {
+    const int ch = (64 * (u % 9) + lane) % 9;
+    return (unsigned)(16 * (ch < 8 ? ch : 7));
+  };
+  // Byte offset within a tile (row strides < 2^24 elements, checked on the host).
   auto unit_off = [&](int u) {
-    const int slot = 64 * (u % 9) + lane;
-    const int ch = slot % 9;
-    return (unsigned)((slot / 9) * ROWB + 16 * (ch < 8 ? ch : 7));
+    const unsigned rsb = (unsigned)sizeof(T) * (unsigned)(u >= 9 ? p.sv.r : p.sk.r);
+    return (unsigned)unit_row(u) * rsb + unit_col(u);
   };
   auto copy_unit = [&](int j, int u, unsigned off) __attribute__((always_inline)) {
     const int which = u >= 9, v9 = u - 9 * which;
     const T* g = which ? vg : kg;
+    const int64_t rs = which ? p.sv.r : p.sk.r;
     const unsigned lds = __builtin_amdgcn_readfirstlane(lds_addr(stage(j) + which * TILEB + 1024 * v9));
     const int64_t k0 = (int64_t)j * BK;
     if (j < n_full) {
-      copy_to_lds16_sb(g + k0 * D, off, lds);
+      copy_to_lds16_sb(g + k0 * rs, off, lds);
     } else {
-      int64_t key = k0 + off / ROWB;
+      int64_t key = k0 + unit_row(u);
       if (key > p.n_k - 1) key = p.n_k - 1;
-      copy_to_lds16(reinterpret_cast<const unsigned char*>(g + key * D) + off % ROWB, lds);
+      copy_to_lds16(reinterpret_cast<const unsigned char*>(g + key * rs) + unit_col(u), lds);
     }
   };
   constexpr int MAXU = (UNITS + NW - 1) / NW;
@@ -1159,7 +1171,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   if (grp == 0) barrier();  // group 1's start delay, balanced
 
   if (valid) {
-    T* dqg = static_cast<T*>(p.dq) + ((size_t)bh * p.n_q + query) * D;
+    T* dqg = static_cast<T*>(p.dq) + head_base(p.sdq, bh, p.heads) + query * p.sdq.r;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll

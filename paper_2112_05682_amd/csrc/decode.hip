@@ -53,7 +53,6 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
   using C = dec::Cfg<D>;
   constexpr int BK = C::BK, NKT = BK / 32, KC = D / 16, NDT = D / 32, NPC = BK / 16;
   constexpr int RS = C::RSB / 2;  // LDS row stride in elements
-  constexpr int ROWB = D * 2;     // global row bytes
   __shared__ __align__(16) unsigned char smem[C::NSTAGE * C::STAGEB];
 
   const int lane = threadIdx.x;
@@ -61,9 +60,9 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
   const int split = blockIdx.x % p.n_splits;
   const int bh = blockIdx.x / p.n_splits;
 
-  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
-  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + head_base(p.sq, bh, p.heads);
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   const int64_t n_keys = decode_keys(p.n_q, p.n_k, CAUSAL);
   const int64_t kb = (int64_t)split * p.keys_per_split;
@@ -79,7 +78,7 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       if (query < p.n_q) {
-        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + query * D + 16 * kc + 8 * h);
+        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + query * p.sq.r + 16 * kc + 8 * h);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) qf[t][kc][e] = (T)0.0f;
@@ -89,15 +88,20 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
 
   // Copy u of a tile moves lane slots 64 u + lane: row slot / SPR, 16-byte
   // chunk slot % SPR (the pad slot gets a copy of the last chunk); slots past
-  // the tile's rows repeat its last slot.  Byte offsets within a tile row
-  // block are computed once.
-  unsigned uoff[C::NCOPY];
+  // the tile's rows repeat its last slot.  The row and the byte column of
+  // each copy are computed once, and the byte offsets within a tile of K and
+  // of V (row strides < 2^24 elements, checked on the host).
+  int urow[C::NCOPY];
+  unsigned ucol[C::NCOPY], ukoff[C::NCOPY], uvoff[C::NCOPY];
 #pragma unroll
   for (int u = 0; u < C::NCOPY; ++u) {
     int slot = 64 * u + lane;
     if (slot >= C::NSLOT) slot = C::NSLOT - 1;
-    const int row = slot / C::SPR, ch = slot % C::SPR;
-    uoff[u] = (unsigned)(row * ROWB + 16 * (ch < C::SPR - 1 ? ch : C::SPR - 2));
+    const int ch = slot % C::SPR;
+    urow[u] = slot / C::SPR;
+    ucol[u] = (unsigned)(16 * (ch < C::SPR - 1 ? ch : C::SPR - 2));
+    ukoff[u] = (unsigned)urow[u] * (unsigned)(2 * p.sk.r) + ucol[u];
+    uvoff[u] = (unsigned)urow[u] * (unsigned)(2 * p.sv.r) + ucol[u];
   }
   auto copy_tile = [&](int j) __attribute__((always_inline)) {
     const int64_t k0 = kb + (int64_t)j * BK;
@@ -106,20 +110,19 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
     if (k0 + BK <= ke) {
 #pragma unroll
       for (int u = 0; u < C::NCOPY; ++u) {
-        copy_to_lds16_sb(kg + k0 * D, uoff[u], __builtin_amdgcn_readfirstlane(kl + 1024 * u));
-        copy_to_lds16_sb(vg + k0 * D, uoff[u], __builtin_amdgcn_readfirstlane(vl + 1024 * u));
+        copy_to_lds16_sb(kg + k0 * p.sk.r, ukoff[u], __builtin_amdgcn_readfirstlane(kl + 1024 * u));
+        copy_to_lds16_sb(vg + k0 * p.sv.r, uvoff[u], __builtin_amdgcn_readfirstlane(vl + 1024 * u));
       }
     } else {
       // Ragged last tile: rows past the range repeat its last key (finite
       // values, masked below).
 #pragma unroll
       for (int u = 0; u < C::NCOPY; ++u) {
-        int64_t key = k0 + uoff[u] / ROWB;
+        int64_t key = k0 + urow[u];
         if (key > ke - 1) key = ke - 1;
-        const unsigned col = uoff[u] % ROWB;
-        copy_to_lds16(reinterpret_cast<const unsigned char*>(kg + key * D) + col,
+        copy_to_lds16(reinterpret_cast<const unsigned char*>(kg + key * p.sk.r) + ucol[u],
                       __builtin_amdgcn_readfirstlane(kl + 1024 * u));
-        copy_to_lds16(reinterpret_cast<const unsigned char*>(vg + key * D) + col,
+        copy_to_lds16(reinterpret_cast<const unsigned char*>(vg + key * p.sv.r) + ucol[u],
                       __builtin_amdgcn_readfirstlane(vl + 1024 * u));
       }
     }
@@ -236,7 +239,7 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
     if (row >= p.n_q) continue;
     if (p.n_splits == 1) {
       const float inv = 1.0f / l_tot;
-      TO* og = static_cast<TO*>(p.o) + ((size_t)bh * p.n_q + row) * D;
+      TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll

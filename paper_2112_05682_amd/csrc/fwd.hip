@@ -78,9 +78,9 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   const int64_t q0 = (int64_t)qtile * Cfg::BQ;
   const int64_t qw = q0 + (int64_t)wave * QT * 32;  // first query of this wave
 
-  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
-  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + head_base(p.sq, bh, p.heads);
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   const int64_t kb = (int64_t)split * p.keys_per_split;
   int64_t ke = kb + p.keys_per_split;
@@ -96,7 +96,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       if (row < p.n_q) {
-        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + row * D + 16 * kc + 8 * h);
+        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + row * p.sq.r + 16 * kc + 8 * h);
       } else {
 #pragma unroll
         for (int s = 0; s < 8; ++s) qf[t][kc][s] = (T)0.0f;
@@ -132,7 +132,8 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
       const int rem = chunk % (BK * Cfg::CPR);
       const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
       const int64_t key = k0 + row;
-      const T* src = (which ? vg : kg) + key * D + col * (16 / Cfg::E);
+      const T* src = which ? vg + key * p.sv.r : kg + key * p.sk.r;
+      src += col * (16 / Cfg::E);
       stage[i] = key < p.n_k ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
     }
   };
@@ -288,7 +289,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
     if (row >= p.n_q) continue;
     if (p.n_splits == 1) {
       const float inv = 1.0f / l_tot;
-      TO* og = static_cast<TO*>(p.o) + ((size_t)bh * p.n_q + row) * D;
+      TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -376,9 +377,9 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   const int64_t q0 = (int64_t)qtile * BQ;
   const int64_t qw = q0 + (int64_t)wave * QT * 32;
 
-  const T* __restrict__ qg = static_cast<const T*>(p.q) + (size_t)bh * p.n_q * D;
-  const T* __restrict__ kg = static_cast<const T*>(p.k) + (size_t)bh * p.n_k * D;
-  const T* __restrict__ vg = static_cast<const T*>(p.v) + (size_t)bh * p.n_k * D;
+  const T* __restrict__ qg = static_cast<const T*>(p.q) + head_base(p.sq, bh, p.heads);
+  const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
+  const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   const int64_t kb = (int64_t)split * p.keys_per_split;
   int64_t ke = kb + p.keys_per_split;
@@ -402,7 +403,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       if (row < p.n_q) {
-        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + row * D + 16 * kc + 8 * h);
+        qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + row * p.sq.r + 16 * kc + 8 * h);
       } else {
 #pragma unroll
         for (int e = 0; e < 8; ++e) qf[t][kc][e] = (T)0.0f;
@@ -435,13 +436,14 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   // (finite data; those keys are masked).
   auto load_tile = [&](const T* g, int64_t k0, unsigned char* stage, bool is_v, int part, int nparts)
                        __attribute__((always_inline)) {
+    const int64_t rs = is_v ? p.sv.r : p.sk.r;
     for (int ii = part; ii < BK / 8; ii += nparts) {
       const int row = 8 * ii + (lane >> 3);
       const int x = lane & 7;
       const int lchunk = x ^ (is_v ? swz_v(row) : swz_k(row));
       int64_t key = k0 + row;
       if (key > p.n_k - 1) key = p.n_k - 1;
-      const T* src = g + key * D + lchunk * 8;
+      const T* src = g + key * rs + lchunk * 8;
       copy_to_lds16(src, __builtin_amdgcn_readfirstlane(lds_addr(stage) + ii * 1024));
     }
   };
@@ -648,23 +650,26 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   // within a tile (bytes) are computed once.
   const int urow0 = 8 * (wave - 4) + (lane >> 3), urow1 = urow0 + 32;
   constexpr unsigned E = sizeof(T);
-  const unsigned uk0 = E * (urow0 * D + 8 * ((lane & 7) ^ swz_k(urow0)));
-  const unsigned uk1 = E * (urow1 * D + 8 * ((lane & 7) ^ swz_k(urow1)));
-  const unsigned uv0 = E * (urow0 * D + 8 * ((lane & 7) ^ swz_v(urow0)));
-  const unsigned uv1 = E * (urow1 * D + 8 * ((lane & 7) ^ swz_v(urow1)));
-  auto copy_tile = [&](const T* g, int j, unsigned char* stage, unsigned off0, unsigned off1) __attribute__((always_inline)) {
+  const unsigned rk = (unsigned)p.sk.r, rv = (unsigned)p.sv.r;  // row strides (< 2^24, checked on the host)
+  const unsigned uk0 = E * (urow0 * rk + 8 * ((lane & 7) ^ swz_k(urow0)));
+  const unsigned uk1 = E * (urow1 * rk + 8 * ((lane & 7) ^ swz_k(urow1)));
+  const unsigned uv0 = E * (urow0 * rv + 8 * ((lane & 7) ^ swz_v(urow0)));
+  const unsigned uv1 = E * (urow1 * rv + 8 * ((lane & 7) ^ swz_v(urow1)));
+  auto copy_tile = [&](bool is_v, int j, unsigned char* stage, unsigned off0, unsigned off1) __attribute__((always_inline)) {
     const int64_t k0 = kb + (int64_t)j * BK;
     const unsigned base = __builtin_amdgcn_readfirstlane(lds_addr(stage) + (wave - 4) * 1024);
+    const T* g = is_v ? vg : kg;
     if (k0 + BK <= p.n_k) {
-      copy_to_lds16_sb(g + k0 * D, off0, base);
-      copy_to_lds16_sb(g + k0 * D, off1, base + 4096);
+      const T* tile = g + k0 * (is_v ? p.sv.r : p.sk.r);
+      copy_to_lds16_sb(tile, off0, base);
+      copy_to_lds16_sb(tile, off1, base + 4096);
     } else {
-      load_tile(g, k0, stage, g == vg, wave - 4, 4);
+      load_tile(g, k0, stage, is_v, wave - 4, 4);
     }
   };
   auto issue = [&](int j) __attribute__((always_inline)) {
-    if (j + 3 < n_tiles) copy_tile(kg, j + 3, kstage(j + 3), uk0, uk1);
-    if (j + 2 < n_tiles) copy_tile(vg, j + 2, vstage(j + 2), uv0, uv1);
+    if (j + 3 < n_tiles) copy_tile(false, j + 3, kstage(j + 3), uk0, uk1);
+    if (j + 2 < n_tiles) copy_tile(true, j + 2, vstage(j + 2), uv0, uv1);
   };
   if (grp == 1) {
     issue(-2);
@@ -732,7 +737,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
     if (row >= p.n_q) continue;
     if (p.n_splits == 1) {
       const float inv = 1.0f / l_tot;
-      TO* og = static_cast<TO*>(p.o) + ((size_t)bh * p.n_q + row) * D;
+      TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -791,7 +796,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
   typename FragT<TO>::half out;
 #pragma unroll
   for (int e = 0; e < 4; ++e) out[e] = (TO)(o[e] * inv);
-  *reinterpret_cast<typename FragT<TO>::half*>(static_cast<TO*>(p.o) + row * D + f0) = out;
+  const int bh = (int)(row / p.n_q);
+  TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + (row - (int64_t)bh * p.n_q) * p.so.r;
+  *reinterpret_cast<typename FragT<TO>::half*>(og + f0) = out;
   if (f0 == 0 && p.lse) p.lse[row] = (m_g + __log2f(l)) * kLn2;
 }
 

@@ -6,6 +6,15 @@
 
 namespace mea {
 
+// Element strides of one [B, H, n, d] tensor (batch, head, row); features
+// are contiguous.  Row 0 of (batch, head) bh starts at head_base(s, bh, H).
+struct TensorStrides {
+  int64_t b, h, r;
+};
+__host__ __device__ inline int64_t head_base(const TensorStrides& s, int bh, int heads) {
+  return (int64_t)(bh / heads) * s.b + (int64_t)(bh % heads) * s.h;
+}
+
 // Arguments of the forward kernels (passed by value).
 struct FwdParams {
   const void* q;
@@ -29,6 +38,8 @@ struct FwdParams {
   int n_splits;
   float scale;       // score scale
   float scale_log2;  // scale * log2(e)
+  int heads;         // H (bh = b * H + h)
+  TensorStrides sq, sk, sv, so;
 };
 
 // The summaries of more than kCombineGroup key ranges are combined in stages
@@ -75,6 +86,8 @@ struct BwdParams {
   int n_ktiles;  // key tiles of the dK/dV kernel
   float scale;
   float scale_log2;
+  int heads;  // H (bh = b * H + h)
+  TensorStrides sq, sk, sv, so, sdo, sdq, sdk, sdv;
 };
 
 // Row padding of the backward's per-row arrays (a multiple of every query

@@ -12,16 +12,17 @@ from __future__ import annotations
 import torch
 from torch import nn
 
-from .attention import attention
+from .attention import attention_packed
 
 
 class MultiheadAttention(nn.Module):
     """Self-attention over ``x`` of shape ``[B, n, embed_dim]``.
 
-    One fused input projection gives Q, K and V, which are split into
-    ``num_heads`` heads of ``embed_dim // num_heads`` features, laid out as the
-    kernels' contiguous ``[B, H, n, d]``; the heads' outputs are concatenated
-    and projected back.  ``causal`` masks key j for query i when j > i.
+    One fused input projection gives Q, K and V as a packed
+    ``[B, n, 3, H, d]`` tensor that the kernels read in place (strided views,
+    ``num_heads`` heads of ``embed_dim // num_heads`` features); the output
+    ``[B, n, H, d]`` is the heads' concatenation, projected back.  ``causal``
+    masks key j for query i when j > i.
     """
 
     def __init__(self, embed_dim: int, num_heads: int, causal: bool = False, bias: bool = True,
@@ -41,10 +42,9 @@ class MultiheadAttention(nn.Module):
         B, n, E = x.shape
         if E != self.embed_dim:
             raise ValueError("expected embed_dim %d, got %d" % (self.embed_dim, E))
-        qkv = self.qkv(x).view(B, n, 3, self.num_heads, self.head_dim).permute(2, 0, 3, 1, 4)
-        q, k, v = (t.contiguous() for t in qkv.unbind(0))
-        o = attention(q, k, v, causal=self.causal)  # [B, H, n, d]
-        return self.out(o.transpose(1, 2).reshape(B, n, E))
+        qkv = self.qkv(x).view(B, n, 3, self.num_heads, self.head_dim)
+        o = attention_packed(qkv, causal=self.causal)  # [B, n, H, d], no copies either way
+        return self.out(o.reshape(B, n, E))
 
 
 class TransformerBlock(nn.Module):

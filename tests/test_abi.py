@@ -149,16 +149,59 @@ def test_problem_struct_layout_matches_the_header(tmp_path):
     src = tmp_path / "layout.c"
     src.write_text(
         '#include <stddef.h>\n#include <stdio.h>\n#include "mea.h"\n'
-        'int main(void) { printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", sizeof(mea_problem), '
+        'int main(void) { printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", '
+        'sizeof(mea_problem), '
         'offsetof(mea_problem, batch), offsetof(mea_problem, heads), offsetof(mea_problem, n_q), '
         'offsetof(mea_problem, n_k), offsetof(mea_problem, d), offsetof(mea_problem, dtype), '
         'offsetof(mea_problem, causal), offsetof(mea_problem, scale), '
-        'offsetof(mea_problem, out_f32)); return 0; }\n')
+        'offsetof(mea_problem, out_f32), offsetof(mea_problem, strides), '
+        'sizeof(mea_strides), offsetof(mea_strides, d_o), offsetof(mea_strides, dv)); return 0; }\n')
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROOT, "include"),
                     "-I/opt/rocm/include", str(src), "-o", str(exe)], check=True)
     got = [int(t) for t in subprocess.run([str(exe)], check=True, capture_output=True,
                                           text=True).stdout.split()]
-    M = _lib.MeaProblem
-    want = [ctypes.sizeof(M)] + [getattr(M, f).offset for f, _ in M._fields_]
+    M, S = _lib.MeaProblem, _lib.MeaStrides
+    want = [ctypes.sizeof(M)] + [getattr(M, f).offset for f, _ in M._fields_] + [
+        ctypes.sizeof(S), S.d_o.offset, S.dv.offset]
     assert got == want
+
+
+def _strided_prob(**over):
+    # bf16, B=2, H=4, n_q=100, n_k=300, d=64 in the [B, n, H, d] layout, with
+    # one tensor's strides replaced by `over`.
+    B, H, nq, nk, d = 2, 4, 100, 300, 64
+    st = {"q": (nq * H * d, d, H * d), "k": (nk * H * d, d, H * d), "v": (nk * H * d, d, H * d),
+          "o": (nq * H * d, d, H * d), "d_o": (nq * H * d, d, H * d), "dq": (nq * H * d, d, H * d),
+          "dk": (nk * H * d, d, H * d), "dv": (nk * H * d, d, H * d)}
+    st.update(over)
+    return _lib.problem(B, H, nq, nk, d, _lib.MEA_BF16, False, 0.125, strides=st)
+
+
+@pytest.mark.parametrize("bad", [
+    {"q": (100 * 256, 64, 32)},        # row stride below d
+    {"k": (300 * 256, 64, 1 << 24)},   # row stride beyond the 32-bit copy offsets
+    {"v": (300 * 256, 60, 256)},       # head stride not a multiple of 16 bytes
+    {"o": (100 * 256, 0, 256)},        # output rows shared by every head
+    {"q": (-1, 64, 256)},              # negative stride
+])
+def test_fwd_rejects_bad_strides(bad):
+    # Validation fails before anything is launched (the pointers are fake).
+    assert _lib.fwd(_strided_prob(**bad), FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == \
+        _lib.MEA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("bad", [{"dq": (100 * 256, 0, 256)}, {"dk": (300 * 256, 64, 8)},
+                                 {"d_o": (100 * 256, 64, 36)}])
+def test_bwd_rejects_bad_strides(bad):
+    p = _strided_prob(**bad)
+    assert _lib.bwd(p, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+
+
+def test_shared_key_heads_are_valid_input_strides():
+    # Head stride 0 for k and v (one key head for all query heads) is allowed
+    # for inputs; for dk and dv it would make heads overwrite each other.
+    ok = _strided_prob(k=(300 * 64, 0, 64), v=(300 * 64, 0, 64))
+    assert ok.strides.contents.k.head == 0
+    bad = _strided_prob(dk=(300 * 64, 0, 64))
+    assert _lib.bwd(bad, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
