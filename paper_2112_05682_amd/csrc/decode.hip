@@ -210,7 +210,7 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) w8[e] = fast_exp2(fmaf(s[t][pc >> 1][8 * (pc & 1) + e], cl2, -mref));
         pf[t][pc] = to_frag<T>(w8);
-        l_run[t] = frag_sum(pf[t][pc], nullptr, l_run[t]);  // the rounded weights the numerator uses
+        l_run[t] = tree_sum<8>(w8, l_run[t]);
       }
     }
 

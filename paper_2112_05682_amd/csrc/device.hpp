@@ -213,34 +213,21 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// acc + the sum of the eight weights of a P fragment.  For 16-bit types the
-// already-rounded fragment is summed with packed dot products against 1, so
-// the denominator adds exactly the weights the PV MFMA multiplies; float32
-// fragments are summed directly.
-__device__ __forceinline__ float frag_sum(const bf16x8& f, const float*, float acc) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const bf16x2 pr = {f[2 * i], f[2 * i + 1]};
-    acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
+// acc + the sum of n weights, added as a balanced tree so that the
+// dependency chain is log2(n) + 1 additions long.  The denominator adds the
+// float32 weights before they are rounded for the PV MFMA: the difference is
+// one rounding per weight, of random sign, far below the 16-bit rounding of
+// the products themselves.  (Packed dot products of the rounded fragment with
+// 1 would add exactly the rounded weights, but on gfx950 they cost several
+// times a VALU add while MFMAs are in flight.)
+template <int N>
+__device__ __forceinline__ float tree_sum(const float* x, float acc) {
+  static_assert(N == 4 || N == 8, "4 or 8 terms");
+  if constexpr (N == 4) {
+    return acc + ((x[0] + x[1]) + (x[2] + x[3]));
+  } else {
+    return acc + (((x[0] + x[1]) + (x[2] + x[3])) + ((x[4] + x[5]) + (x[6] + x[7])));
   }
-  return acc;
-}
-__device__ __forceinline__ float frag_sum(const f16x8& f, const float*, float acc) {
-  typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-  const f16x2 one = {(_Float16)1.0f, (_Float16)1.0f};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const f16x2 pr = {f[2 * i], f[2 * i + 1]};
-    acc = __builtin_amdgcn_fdot2(pr, one, acc, false);
-  }
-  return acc;
-}
-__device__ __forceinline__ float frag_sum(const f32x8&, const float* x, float acc) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) acc += x[i];
-  return acc;
 }
 
 // 16-byte global load / store helpers.

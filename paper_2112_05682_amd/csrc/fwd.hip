@@ -242,7 +242,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg));
         pf[t][pc] = to_frag<T>(e8);
-        l_run[t] = frag_sum(pf[t][pc], e8, l_run[t]);
+        l_run[t] = tree_sum<8>(e8, l_run[t]);
       }
     }
     // O^T += V^T P^T; each V^T fragment feeds every query sub-tile.
@@ -337,7 +337,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 // conflicts.
 // ---------------------------------------------------------------------------
 #ifndef MEA_FWD_PP_W0
-#define MEA_FWD_PP_W0 2
+#define MEA_FWD_PP_W0 3
 #endif
 namespace pp {
 constexpr int D = 64, QT = 2, BK = 64, NW = 8, BQ = NW * QT * 32, NSTAGE = 3;
@@ -523,8 +523,8 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg));
       pfo[t][pc] = to_frag<T>(e8);
-      if (pc & 1) sum1 = frag_sum(pfo[t][pc], e8, sum1);
-      else sum0 = frag_sum(pfo[t][pc], e8, sum0);
+      if (pc & 1) sum1 = tree_sum<8>(e8, sum1);
+      else sum0 = tree_sum<8>(e8, sum0);
     }
     return sum0 + sum1;
   };
@@ -596,13 +596,11 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
           e4[e] = fast_exp2(fmaf(s[pcs >> 1][0][8 * (pcs & 1) + 4 * half + e], cl2, neg));
         packed[2 * half] = pack2<T>(e4[0], e4[1]);
         packed[2 * half + 1] = pack2<T>(e4[2], e4[3]);
+        if (pcs & 1) sum1 = tree_sum<4>(e4, sum1);
+        else sum0 = tree_sum<4>(e4, sum0);
       }
       acc[1][dt] = mma(vf[i & 1], pf_old[1][pcv], acc[1][dt]);
-      if (has_w && half) {
-        pf_new[0][pcs] = __builtin_bit_cast(Frag<T>, packed);
-        if (pcs & 1) sum1 = frag_sum(pf_new[0][pcs], nullptr, sum1);
-        else sum0 = frag_sum(pf_new[0][pcs], nullptr, sum0);
-      }
+      if (has_w && half) pf_new[0][pcs] = __builtin_bit_cast(Frag<T>, packed);
       __builtin_amdgcn_sched_barrier(0);
     }
     return sum0 + sum1;
