@@ -23,6 +23,19 @@
 #ifndef MEA_T64_DKDV_AHEAD
 #define MEA_T64_DKDV_AHEAD 2
 #endif
+// 16-key chunks of a key tile's dS computed in the MFMA phase of the
+// two-group dQ kernel (the rest in its softmax phase).
+#ifndef MEA_T64_DQ_W
+#define MEA_T64_DQ_W 1
+#endif
+// Keys per lane whose softmax stages the dQ kernel issues together.
+#ifndef MEA_T64_DQ_G
+#define MEA_T64_DQ_G 16
+#endif
+// K/V stages of the two-group dQ kernel's LDS ring.
+#ifndef MEA_T64_DQ_NSTAGE
+#define MEA_T64_DQ_NSTAGE 4
+#endif
 
 namespace mea {
 
@@ -892,7 +905,10 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 // tile j.  VALU phase: P = 2^(c S), dS = P dP, rounded into the operands of
 // the next MFMA phase.  K and V stream through a four-stage LDS ring.
 namespace qpp {
-constexpr int D = 64, NW = 8, BQG = NW * 32, BK = 64, NKT = BK / 32, NSTAGE = 4;
+constexpr int D = 64, NW = 8, BQG = NW * 32, BK = 64, NKT = BK / 32, NSTAGE = MEA_T64_DQ_NSTAGE;
+// Copy lead, in tiles, of group 1 and group 0 (see the copy schedule below).
+constexpr int LEAD1 = NSTAGE - 1, LEAD0 = NSTAGE - 2;
+static_assert(NSTAGE >= 4 && NSTAGE <= 6, "K/V stages");
 constexpr int RSB = 144;                 // bytes per LDS row (128 + 16 pad)
 constexpr int TILEB = BK * RSB;          // one K or V tile: 9 KiB
 constexpr int STAGEB = 2 * TILEB;
@@ -1009,10 +1025,12 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
         if (wave + NW * k < UNITS) copy_unit(j, wave + NW * k, uoff[k]);
     }
   };
-  auto wait_copies = [&](bool recent) __attribute__((always_inline)) {
-    if (!recent) wait_global_loads();
-    else if (n_units == 3) wait_global_loads_upto<3>();
-    else wait_global_loads_upto<2>();
+  // Wait for this wave's copies of tile j + 1 while its copies of the tiles
+  // after it, up to tile `last` (the newest issued), may still run.
+  auto wait_copies = [&](int j, int last) __attribute__((always_inline)) {
+    if (last > n_tiles - 1) last = n_tiles - 1;
+    const int later = last - (j + 1);
+    wait_global_loads_rt<3 * (LEAD1 - 2)>(later > 0 ? later * n_units : 0);
   };
   auto barrier = [&]() {
     asm volatile("" ::: "memory");
@@ -1022,20 +1040,23 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
     asm volatile("" ::: "memory");
   };
 
-  // Copy schedule as in the two-group dK/dV kernel: group 1 issues its share
-  // of tile j in its VALU phase of tile j - 3, group 0 in its VALU phase of
-  // tile j - 2; both wait for tile j before the barrier that precedes group
-  // 0's MFMA phase of tile j.
+  // Copy schedule: group 1 issues its share of tile j in its VALU phase of
+  // tile j - LEAD1, group 0 in its VALU phase of tile j - LEAD0; both wait for
+  // tile j before the barrier that precedes group 0's MFMA phase of tile j.
+  // The last reader of tile j's stage is group 1's MFMA phase of tile j + 1
+  // (the dQ steps of tile j), two phases before the VALU phase of group 1 that
+  // overwrites it with tile j + NSTAGE and one before group 0's.
   if (n_tiles > 0)
     for (int u = wave; u < UNITS; u += NW) copy_unit(0, u, unit_off(u));
   wait_global_loads();
   __syncthreads();
   if (grp == 1) {
-    issue(1);
-    issue(2);
+#pragma unroll
+    for (int t = 1; t < LEAD1; ++t) issue(t);
     barrier();
   } else {
-    issue(1);
+#pragma unroll
+    for (int t = 1; t < LEAD0; ++t) issue(t);
   }
 
   const int krow = perm32(c);
@@ -1097,34 +1118,133 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // P = 2^(c S), dS = P dP for tile j into the dS^T operands.
-  auto pds = [&](auto mask_tag, int j) __attribute__((always_inline)) {
-    constexpr bool MASK = decltype(mask_tag)::value;
+  // Keys of tile j visible to the wave's queries, for the masked variants:
+  // key k0 + x is valid iff x < lim (ragged tail; causal: x <= query - k0).
+  auto key_lim = [&](int j) {
     const int64_t k0 = (int64_t)j * BK;
-    int lim = BK;
-    if constexpr (MASK) {
-      // key k0 + x is valid iff x < key_lim and, causal, x <= query - k0.
-      lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
-      if (CAUSAL) {
-        const int64_t qr = query - k0 + 1;
-        if (qr < lim) lim = qr > 0 ? (int)qr : 0;
+    int lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+    if (CAUSAL) {
+      const int64_t qr = query - k0 + 1;
+      if (qr < lim) lim = qr > 0 ? (int)qr : 0;
+    }
+    return lim;
+  };
+  // P = 2^(c S), dS = P dP for four keys of 16-key chunk pc (half hf of it),
+  // rounded and packed into two dwords of the chunk's dS^T operand.
+  auto pds_half = [&](auto mask_tag, int pc, int hf, int lim) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    const int kt = pc >> 1;
+    float ds[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 8 * (pc & 1) + 4 * hf + e;
+      float pr = fast_exp2(s[kt][r] * cl2);
+      if (MASK && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
+      ds[e] = pr * dp[kt][r];
+    }
+    return u32x2{pack2<T>(ds[0], ds[1]), pack2<T>(ds[2], ds[3])};
+  };
+  // Chunks pc0 .. NPC - 1 of tile j (the softmax phase's share), in groups of
+  // G keys per lane whose multiplies, exponentials, multiplies and conversions
+  // are issued as separate stages: G independent chains per stage hide the
+  // latency of each stage behind the issue of the next (the compiler would
+  // otherwise reuse a few temporaries and serialise short chains).
+  auto pds = [&](auto mask_tag, int pc0, int lim) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    constexpr int G = MEA_T64_DQ_G;
+    static_assert(G == 8 || G == 16, "8 or 16 keys per lane per group");
+#pragma unroll
+    for (int g0 = 8 * pc0; g0 < 8 * NPC; g0 += G) {
+      const int n = 8 * NPC - g0 < G ? 8 * NPC - g0 : G;
+      float x[G];
+#pragma unroll
+      for (int e = 0; e < n; ++e) x[e] = s[(g0 + e) >> 4][(g0 + e) & 15] * cl2;
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = 0; e < n; ++e) {
+        x[e] = fast_exp2(x[e]);
+        const int kt = (g0 + e) >> 4, r = (g0 + e) & 15;
+        if (MASK && 32 * kt + permuted_row(r, h) >= lim) x[e] = 0.0f;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = 0; e < n; ++e) x[e] *= dp[(g0 + e) >> 4][(g0 + e) & 15];
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c8 = 0; c8 < n; c8 += 8) {
+        dsf[(g0 + c8) >> 3] = to_frag<T>(x + c8);
+        keep_here(dsf[(g0 + c8) >> 3]);  // the conversions belong to this phase
       }
     }
+  };
+
+  // MFMA phase of key tile j with dQ of tile j - 1 (steady state).  Steps, two
+  // MFMAs each: 0..3 S^T/dP^T of keys 0..31 of tile j (k chunk = step), 4..7
+  // dQ^T += K^T dS^T of tile j - 1 (key chunk = step - 4), 8..11 S^T/dP^T of
+  // keys 32..63.  The first W 16-key chunks of tile j's dS (keys 0..31 are
+  // final after step 3) are computed here, four keys per lane at a time
+  // between the two MFMAs of a step, spread over steps 4..11; chunk pc is
+  // written only after dQ step 4 + pc has read the old chunk pc.  One LDS
+  // fetch ring runs through all twelve steps.
+  constexpr int W = MEA_T64_DQ_W;
+  static_assert(W >= 0 && W <= 2, "only chunks of keys 0..31 are final before the dQ steps");
+  auto mfma_phase = [&](auto mask_tag, int j) __attribute__((always_inline)) {
+    constexpr int NS = 12;
+    const T* ks = reinterpret_cast<const T*>(stage(j));
+    const T* vs = reinterpret_cast<const T*>(stage(j) + TILEB);
+    const T* kp = reinterpret_cast<const T*>(stage(j - 1));
+    Frag<T> rx[AHEAD + 1], ry[AHEAD + 1];
+    auto fetch = [&](int g) __attribute__((always_inline)) {
+      const int slot = g % (AHEAD + 1);
+      if (g >= 4 && g < 8) {
+        rx[slot] = lds_col_frag<T>(kp, RSB / 2, 16 * (g - 4), 0, lane);
+        ry[slot] = lds_col_frag<T>(kp, RSB / 2, 16 * (g - 4), 32, lane);
+      } else {
+        const int kt = g >= 8, kc = g - 8 * kt;
+        rx[slot] = lds_frag<T>(ks + (32 * kt + krow) * (RSB / 2) + 16 * kc + 8 * h);
+        ry[slot] = lds_frag<T>(vs + (32 * kt + krow) * (RSB / 2) + 16 * kc + 8 * h);
+      }
+    };
+    const int lim = decltype(mask_tag)::value ? key_lim(j) : BK;
+#pragma unroll
+    for (int g = 0; g < AHEAD; ++g) fetch(g);
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float pr = fast_exp2(s[kt][r] * cl2);
-        if (MASK && 32 * kt + permuted_row(r, h) >= lim) pr = 0.0f;
-        dp[kt][r] = pr * dp[kt][r];
+        s[kt][r] = s_init;
+        dp[kt][r] = dp_init;
       }
+    u32x2 first_half = {0u, 0u};
 #pragma unroll
-    for (int pc = 0; pc < NPC; ++pc) {
-      float td[8];
+    for (int g = 0; g < NS; ++g) {
+      if (g + AHEAD < NS) fetch(g + AHEAD);
+      const int slot = g % (AHEAD + 1);
+      // Half-chunk u of the dS work runs in step 4 + (4 u) / W.
+      int u = -1;
+      if constexpr (W > 0) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) td[e] = dp[pc >> 1][8 * (pc & 1) + e];
-      dsf[pc] = to_frag<T>(td);
-      keep_here(dsf[pc]);  // the conversions belong to this phase
+        for (int uu = 0; uu < 2 * W; ++uu)
+          if (g == 4 + (4 * uu) / W) u = uu;
+      }
+      if (g >= 4 && g < 8) {
+        acc[0] = mma(rx[slot], dsf[g - 4], acc[0]);
+      } else {
+        const int kt = g >= 8, kc = g - 8 * kt;
+        s[kt] = mma(rx[slot], qf[kc], s[kt]);
+      }
+      if (u >= 0) {
+        const u32x2 part = pds_half(mask_tag, u >> 1, u & 1, lim);
+        if ((u & 1) == 0) first_half = part;
+        else dsf[u >> 1] = __builtin_bit_cast(Frag<T>, u32x4{first_half[0], first_half[1], part[0], part[1]});
+      }
+      if (g >= 4 && g < 8) {
+        acc[1] = mma(ry[slot], dsf[g - 4], acc[1]);
+      } else {
+        const int kt = g >= 8, kc = g - 8 * kt;
+        dp[kt] = mma(ry[slot], gf[kc], dp[kt]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -1133,40 +1253,51 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   // tile only (this one is past the wave's last query, causal); MODE 0:
   // copies and barriers only.  A tile past the wave's last query stays so for
   // the later tiles (the keys only grow), so the modes come in this order and
-  // each loop below runs one of them.
-  auto iteration = [&](auto mode_tag, int j) __attribute__((always_inline)) {
+  // each loop below runs one of them; MODE 2 runs unmasked tiles, then masked
+  // ones (ragged tail, causal diagonal), which also come last.
+  auto iteration = [&](auto mode_tag, auto mask_tag, int j) __attribute__((always_inline)) {
     constexpr int MODE = decltype(mode_tag)::value;
+    constexpr bool MASK = decltype(mask_tag)::value;
     // ---- MFMA phase
     mfma_phase_priority();
-    if constexpr (MODE == 2 || MODE == 3) dq_mma(j - 1);
-    if constexpr (MODE == 1 || MODE == 2) sdp(j);
-    if (grp == 1) wait_copies(j + 2 < n_tiles);
+    if constexpr (MODE == 2) mfma_phase(mask_tag, j);
+    if constexpr (MODE == 3) dq_mma(j - 1);
+    if constexpr (MODE == 1) sdp(j);
+    if (grp == 1) wait_copies(j, j - 1 + LEAD1);
     barrier();
     // ---- VALU phase
     valu_phase_priority();
-    if constexpr (MODE == 1 || MODE == 2) {
-      if (masked(j)) pds(BoolC<true>{}, j);
-      else pds(BoolC<false>{}, j);
+    if constexpr (MODE == 1) {
+      if (masked(j)) pds(BoolC<true>{}, 0, key_lim(j));
+      else pds(BoolC<false>{}, 0, BK);
+    } else if constexpr (MODE == 2) {
+      pds(mask_tag, W, MASK ? key_lim(j) : BK);
     }
     if (grp == 1) {
-      issue(j + 3);
+      issue(j + LEAD1);
     } else {
-      issue(j + 2);
-      wait_copies(j + 2 < n_tiles);
+      issue(j + LEAD0);
+      wait_copies(j, j + LEAD0);
     }
     barrier();
   };
-  // Tiles 0 .. j_end - 1 hold keys visible to the wave.
+  // Tiles 0 .. j_end - 1 hold keys visible to the wave; tiles j_mask and
+  // later need the elementwise mask.
   int j_end = n_tiles;
+  int j_mask = n_full;
   if (CAUSAL) {
     const int64_t last = (qw + 31) / BK + 1;
     if (last < j_end) j_end = (int)last;
+    // tile j holds a key after query qw iff 64 j + 63 > qw
+    const int jc = qw < BK - 1 ? 0 : (int)((qw - (BK - 1)) / BK) + 1;
+    if (jc < j_mask) j_mask = jc;
   }
   int j = 0;
-  if (j < j_end) iteration(IntC<1>{}, j++);
-  for (; j < j_end; ++j) iteration(IntC<2>{}, j);
-  if (j < n_tiles) iteration(IntC<3>{}, j++);
-  for (; j < n_tiles; ++j) iteration(IntC<0>{}, j);
+  if (j < j_end) iteration(IntC<1>{}, BoolC<false>{}, j++);
+  for (; j < j_end && j < j_mask; ++j) iteration(IntC<2>{}, BoolC<false>{}, j);
+  for (; j < j_end; ++j) iteration(IntC<2>{}, BoolC<true>{}, j);
+  if (j < n_tiles) iteration(IntC<3>{}, BoolC<false>{}, j++);
+  for (; j < n_tiles; ++j) iteration(IntC<0>{}, BoolC<false>{}, j);
   if (j_end == n_tiles && n_tiles > 0) dq_mma(n_tiles - 1);
   if (grp == 0) barrier();  // group 1's start delay, balanced
 

@@ -132,6 +132,16 @@ __device__ __forceinline__ void wait_global_loads_upto() {
   // vmcnt bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left unconstrained.
   __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
+// The same with a wave-uniform runtime count n <= NMAX.
+template <int NMAX>
+__device__ __forceinline__ void wait_global_loads_rt(int n) {
+  if constexpr (NMAX <= 0) {
+    wait_global_loads();
+  } else {
+    if (n >= NMAX) wait_global_loads_upto<NMAX>();
+    else wait_global_loads_rt<NMAX - 1>(n);
+  }
+}
 // Wait until every LDS read of this wave has returned (lgkmcnt(0), vmcnt and
 // expcnt unconstrained): the LDS space they read may then be overwritten.
 __device__ __forceinline__ void wait_lds_reads() { __builtin_amdgcn_s_waitcnt(0xC07F); }
