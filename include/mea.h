@@ -32,6 +32,11 @@
  *     aligned at the top-left (key 0 is always visible, so no row is empty,
  *     also when n_q != n_k).  The paper defines no mask; this is the reading
  *     the library adopts.
+ *   - Key padding (`kv_len` != NULL): batch b sees only its keys
+ *     j < kv_len[b] (clamped to [0, n_k]), on top of the causal mask; the
+ *     keys from there to n_k are never weighted (their dk and dv rows are
+ *     written as zeros).  A query row with no visible key (kv_len[b] <= 0)
+ *     gets o = 0, lse = -inf and zero gradients.
  *   - Errors: arguments are validated before anything is launched; on a
  *     validation error nothing is enqueued and the status says why.  A
  *     launch failure reported by the HIP runtime returns MEA_ERR_HIP.  Errors
@@ -95,6 +100,9 @@ typedef struct {
                       output, Section 5.1); ignored when dtype is MEA_F32 */
   const mea_strides* strides; /* HOST pointer or NULL (every tensor contiguous
                                  [B, H, n, d]); read during the call only */
+  const int32_t* kv_len;      /* DEVICE pointer to int32 [B] (4-byte aligned):
+                                 valid keys per batch (key padding, see above),
+                                 read by the kernels; NULL = all n_k keys */
 } mea_problem;
 
 /* Bytes of device workspace mea_attention_fwd needs for `p` (written to

@@ -52,15 +52,16 @@ def _load():
         if not os.path.exists(_LIB):
             build(force=True)
         lib = ctypes.CDLL(_LIB)
-        full = [_i64, _i64, _i64, _i64, _i64, _dp, _dp, _dp, _dbl, _int]
+        full = [_i64, _i64, _i64, _i64, _i64, _dp, _dp, _dp, _dbl, _int, _lp]
         lib.mea_oracle_fwd.argtypes = full + [_dp, _dp]
         lib.mea_oracle_fwd_lazy.argtypes = full + [_dp, _dp]
         lib.mea_oracle_fwd_chunked.argtypes = full + [_i64, _i64, _dp, _dp]
-        lib.mea_oracle_bwd.argtypes = [_i64] * 5 + [_dp] * 4 + [_dbl, _int] + [_dp] * 3
+        lib.mea_oracle_bwd.argtypes = [_i64] * 5 + [_dp] * 4 + [_dbl, _int, _lp] + [_dp] * 3
         head = [_i64, _i64, _i64, _dp, _dp, _dp]
-        lib.mea_oracle_fwd_rows.argtypes = head + [_dbl, _int, _lp, _i64, _dp, _dp]
-        lib.mea_oracle_bwd_dq_rows.argtypes = head + [_dp, _dbl, _int, _lp, _i64, _dp]
-        lib.mea_oracle_bwd_dkdv_keys.argtypes = head + [_dp, _dbl, _int, _lp, _i64, _dp, _dp]
+        lib.mea_oracle_fwd_rows.argtypes = head + [_dbl, _int, _i64, _lp, _i64, _dp, _dp]
+        lib.mea_oracle_bwd_dq_rows.argtypes = head + [_dp, _dbl, _int, _i64, _lp, _i64, _dp]
+        lib.mea_oracle_bwd_dkdv_keys.argtypes = head + [_dp, _dbl, _int, _i64, _lp, _i64, _dp,
+                                                        _dp]
         for name in ("mea_oracle_fwd", "mea_oracle_fwd_lazy", "mea_oracle_fwd_chunked",
                      "mea_oracle_bwd", "mea_oracle_fwd_rows", "mea_oracle_bwd_dq_rows",
                      "mea_oracle_bwd_dkdv_keys", "mea_oracle_num_threads"):
@@ -92,6 +93,20 @@ def _dims(q, k, v):
     return B, H, nq, k.shape[2], d
 
 
+def _kv_len(kv_len, batch: int):
+    """Per-batch valid key lengths as a contiguous int64 array (None: all keys)."""
+    if kv_len is None:
+        return None
+    a = np.ascontiguousarray(np.asarray(kv_len, dtype=np.int64).reshape(-1))
+    if a.size != batch:
+        raise ValueError("kv_len must have one entry per batch")
+    return a
+
+
+def _lptr(a):
+    return a.ctypes.data_as(_lp) if a is not None else None
+
+
 def default_scale(d: int) -> float:
     """The 1/sqrt(d) query scaling of the paper's implementation (Section 4)."""
     return 1.0 / float(np.sqrt(d))
@@ -101,56 +116,65 @@ def num_threads() -> int:
     return int(_load().mea_oracle_num_threads())
 
 
-def fwd(q, k, v, scale=None, causal=False):
-    """Direct form.  Returns (o [B,H,n_q,d], lse [B,H,n_q]) in float64."""
+def fwd(q, k, v, scale=None, causal=False, kv_len=None):
+    """Direct form.  Returns (o [B,H,n_q,d], lse [B,H,n_q]) in float64.
+    ``kv_len``: optional per-batch valid key lengths (key padding)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, nq, nk, d = _dims(q, k, v)
     scale = default_scale(d) if scale is None else float(scale)
+    kl = _kv_len(kv_len, B)
     o = np.empty((B, H, nq, d))
     lse = np.empty((B, H, nq))
     _check(_load().mea_oracle_fwd(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), scale,
-                                  int(bool(causal)), _ptr(o), _ptr(lse)), "mea_oracle_fwd")
+                                  int(bool(causal)), _lptr(kl), _ptr(o), _ptr(lse)),
+           "mea_oracle_fwd")
     return o, lse
 
 
-def fwd_lazy(q, k, v, scale=None, causal=False):
+def fwd_lazy(q, k, v, scale=None, causal=False, kv_len=None):
     """Section 3 single-pass form.  Returns (o, lse)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, nq, nk, d = _dims(q, k, v)
     scale = default_scale(d) if scale is None else float(scale)
+    kl = _kv_len(kv_len, B)
     o = np.empty((B, H, nq, d))
     lse = np.empty((B, H, nq))
     _check(_load().mea_oracle_fwd_lazy(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), scale,
-                                       int(bool(causal)), _ptr(o), _ptr(lse)),
+                                       int(bool(causal)), _lptr(kl), _ptr(o), _ptr(lse)),
            "mea_oracle_fwd_lazy")
     return o, lse
 
 
-def fwd_chunked(q, k, v, scale=None, causal=False, query_chunk=1024, key_chunk=4096):
+def fwd_chunked(q, k, v, scale=None, causal=False, query_chunk=1024, key_chunk=4096,
+                kv_len=None):
     """Section 4 chunk-summary form.  Returns (o, lse)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
     B, H, nq, nk, d = _dims(q, k, v)
     scale = default_scale(d) if scale is None else float(scale)
+    kl = _kv_len(kv_len, B)
     o = np.empty((B, H, nq, d))
     lse = np.empty((B, H, nq))
     _check(_load().mea_oracle_fwd_chunked(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), scale,
-                                          int(bool(causal)), int(query_chunk), int(key_chunk),
-                                          _ptr(o), _ptr(lse)), "mea_oracle_fwd_chunked")
+                                          int(bool(causal)), _lptr(kl), int(query_chunk),
+                                          int(key_chunk), _ptr(o), _ptr(lse)),
+           "mea_oracle_fwd_chunked")
     return o, lse
 
 
-def bwd(q, k, v, dout, scale=None, causal=False):
+def bwd(q, k, v, dout, scale=None, causal=False, kv_len=None):
     """Hand-derived gradients.  Returns (dq, dk, dv) in float64."""
     q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
     B, H, nq, nk, d = _dims(q, k, v)
     if dout.shape != q.shape:
         raise ValueError("dout must have the shape of q")
     scale = default_scale(d) if scale is None else float(scale)
+    kl = _kv_len(kv_len, B)
     dq = np.empty_like(q)
     dk = np.empty_like(k)
     dv = np.empty_like(v)
     _check(_load().mea_oracle_bwd(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), _ptr(dout),
-                                  scale, int(bool(causal)), _ptr(dq), _ptr(dk), _ptr(dv)),
+                                  scale, int(bool(causal)), _lptr(kl), _ptr(dq), _ptr(dk),
+                                  _ptr(dv)),
            "mea_oracle_bwd")
     return dq, dk, dv
 
@@ -162,8 +186,13 @@ def _head(x):
     return x
 
 
-def fwd_rows(q, k, v, rows, scale=None, causal=False):
-    """Forward for selected query rows of one head (q, k, v are [n, d])."""
+def _n_valid(n_valid, n_k: int) -> int:
+    return n_k if n_valid is None else int(n_valid)
+
+
+def fwd_rows(q, k, v, rows, scale=None, causal=False, n_valid=None):
+    """Forward for selected query rows of one head (q, k, v are [n, d]);
+    ``n_valid``: keys visible at most (key padding), default all."""
     q, k, v = _head(q), _head(k), _head(v)
     rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
     d = q.shape[1]
@@ -171,13 +200,13 @@ def fwd_rows(q, k, v, rows, scale=None, causal=False):
     o = np.empty((rows.size, d))
     lse = np.empty(rows.size)
     _check(_load().mea_oracle_fwd_rows(q.shape[0], k.shape[0], d, _ptr(q), _ptr(k), _ptr(v),
-                                       scale, int(bool(causal)),
+                                       scale, int(bool(causal)), _n_valid(n_valid, k.shape[0]),
                                        rows.ctypes.data_as(_lp), rows.size, _ptr(o), _ptr(lse)),
            "mea_oracle_fwd_rows")
     return o, lse
 
 
-def bwd_dq_rows(q, k, v, dout, rows, scale=None, causal=False):
+def bwd_dq_rows(q, k, v, dout, rows, scale=None, causal=False, n_valid=None):
     """dQ for selected query rows of one head."""
     q, k, v, dout = _head(q), _head(k), _head(v), _head(dout)
     rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
@@ -186,12 +215,13 @@ def bwd_dq_rows(q, k, v, dout, rows, scale=None, causal=False):
     dq = np.empty((rows.size, d))
     _check(_load().mea_oracle_bwd_dq_rows(q.shape[0], k.shape[0], d, _ptr(q), _ptr(k), _ptr(v),
                                           _ptr(dout), scale, int(bool(causal)),
+                                          _n_valid(n_valid, k.shape[0]),
                                           rows.ctypes.data_as(_lp), rows.size, _ptr(dq)),
            "mea_oracle_bwd_dq_rows")
     return dq
 
 
-def bwd_dkdv_keys(q, k, v, dout, keys, scale=None, causal=False):
+def bwd_dkdv_keys(q, k, v, dout, keys, scale=None, causal=False, n_valid=None):
     """dK and dV for selected key rows of one head."""
     q, k, v, dout = _head(q), _head(k), _head(v), _head(dout)
     keys = np.ascontiguousarray(np.asarray(keys, dtype=np.int64))
@@ -201,6 +231,7 @@ def bwd_dkdv_keys(q, k, v, dout, keys, scale=None, causal=False):
     dv = np.empty((keys.size, d))
     _check(_load().mea_oracle_bwd_dkdv_keys(q.shape[0], k.shape[0], d, _ptr(q), _ptr(k),
                                             _ptr(v), _ptr(dout), scale, int(bool(causal)),
+                                            _n_valid(n_valid, k.shape[0]),
                                             keys.ctypes.data_as(_lp), keys.size, _ptr(dk),
                                             _ptr(dv)),
            "mea_oracle_bwd_dkdv_keys")

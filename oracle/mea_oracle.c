@@ -42,6 +42,10 @@
  *   - masking: `causal` means key j is visible to query i iff j <= i
  *     (aligned at the top-left, so key 0 is always visible and no row is
  *     empty, also when n_q != n_k);
+ *   - key padding: batch b sees only keys j < kv_len[b] (clamped to
+ *     [0, n_k]; a NULL kv_len means all n_k), on top of the causal mask; a
+ *     row that sees no key has o = 0, lse = -inf and zero gradients, and a
+ *     key no row sees has zero dK and dV (the sums over an empty set);
  *   - lse is the natural-log log-sum-exp of the scaled scores of a row;
  *   - layout: contiguous [B, H, n, d], feature index innermost.
  *
@@ -63,10 +67,20 @@
 #define ORACLE_EINVAL 1
 #define ORACLE_ENOMEM 2
 
-/* Number of keys visible to query row i. */
-static int64_t visible_keys(int64_t i, int64_t n_k, int causal) {
-  if (!causal) return n_k;
-  return (i + 1 < n_k) ? (i + 1) : n_k;
+/* Number of keys visible to query row i: a prefix of the keys, the first
+ * n_valid of them (key padding) and, causal, at most the first i + 1. */
+static int64_t visible_keys(int64_t i, int64_t n_k, int causal, int64_t n_valid) {
+  int64_t n = n_k;
+  if (causal && i + 1 < n) n = i + 1;
+  return n < n_valid ? n : n_valid;
+}
+
+/* Valid keys of (batch, head) slice bh: kv_len[b] clamped to [0, n_k]. */
+static int64_t slice_valid(const int64_t* kv_len, int64_t bh, int64_t heads,
+                           int64_t n_k) {
+  if (!kv_len) return n_k;
+  const int64_t l = kv_len[bh / heads];
+  return l < 0 ? 0 : (l > n_k ? n_k : l);
 }
 
 static double dot(const double* a, const double* b, int64_t d) {
@@ -131,9 +145,10 @@ static int thread_id(void) {
  * lse_rows is [n_rows] (either may be NULL). */
 int mea_oracle_fwd_rows(int64_t n_q, int64_t n_k, int64_t d, const double* q,
                         const double* k, const double* v, double scale,
-                        int causal, const int64_t* rows, int64_t n_rows,
-                        double* o_rows, double* lse_rows) {
-  if (!dims_ok(n_q, n_k, d) || n_rows < 0 || !q || !k || !v || !rows)
+                        int causal, int64_t n_valid, const int64_t* rows,
+                        int64_t n_rows, double* o_rows, double* lse_rows) {
+  if (!dims_ok(n_q, n_k, d) || n_rows < 0 || !q || !k || !v || !rows ||
+      n_valid < 0 || n_valid > n_k)
     return ORACLE_EINVAL;
   for (int64_t r = 0; r < n_rows; ++r)
     if (rows[r] < 0 || rows[r] >= n_q) return ORACLE_EINVAL;
@@ -146,8 +161,8 @@ int mea_oracle_fwd_rows(int64_t n_q, int64_t n_k, int64_t d, const double* q,
     double* out = s + n_k;
     const int64_t i = rows[r];
     double lse;
-    direct_row(q + i * d, k, v, visible_keys(i, n_k, causal), d, scale, s, out,
-               &lse);
+    direct_row(q + i * d, k, v, visible_keys(i, n_k, causal, n_valid), d, scale,
+               s, out, &lse);
     if (o_rows) memcpy(o_rows + r * d, out, sizeof(double) * (size_t)d);
     if (lse_rows) lse_rows[r] = lse;
   }
@@ -158,7 +173,8 @@ int mea_oracle_fwd_rows(int64_t n_q, int64_t n_k, int64_t d, const double* q,
 /* Full [B, H, n_q, d] forward, direct form. */
 int mea_oracle_fwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
                    int64_t d, const double* q, const double* k, const double* v,
-                   double scale, int causal, double* o, double* lse) {
+                   double scale, int causal, const int64_t* kv_len, double* o,
+                   double* lse) {
   if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || !o || !lse)
     return ORACLE_EINVAL;
   int64_t* rows = (int64_t*)malloc(sizeof(int64_t) * (size_t)n_q);
@@ -167,7 +183,8 @@ int mea_oracle_fwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
   int err = ORACLE_OK;
   for (int64_t bh = 0; bh < batch * heads && err == ORACLE_OK; ++bh) {
     err = mea_oracle_fwd_rows(n_q, n_k, d, q + bh * n_q * d, k + bh * n_k * d,
-                              v + bh * n_k * d, scale, causal, rows, n_q,
+                              v + bh * n_k * d, scale, causal,
+                              slice_valid(kv_len, bh, heads, n_k), rows, n_q,
                               o + bh * n_q * d, lse + bh * n_q);
   }
   free(rows);
@@ -196,6 +213,11 @@ static void lazy_row(const double* qi, const double* k, const double* v,
     sstar = sstar * old_factor + new_factor;
     mstar = mi;
   }
+  if (n_vis == 0) { /* no visible key: the empty sums give o = 0 */
+    for (int64_t t = 0; t < d; ++t) out[t] = 0.0;
+    *lse = -INFINITY;
+    return;
+  }
   for (int64_t t = 0; t < d; ++t) out[t] = vstar[t] / sstar;
   *lse = mstar + log(sstar);
 }
@@ -203,7 +225,8 @@ static void lazy_row(const double* qi, const double* k, const double* v,
 int mea_oracle_fwd_lazy(int64_t batch, int64_t heads, int64_t n_q,
                         int64_t n_k, int64_t d, const double* q,
                         const double* k, const double* v, double scale,
-                        int causal, double* o, double* lse) {
+                        int causal, const int64_t* kv_len, double* o,
+                        double* lse) {
   if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || !q || !k || !v ||
       !o || !lse)
     return ORACLE_EINVAL;
@@ -213,9 +236,10 @@ int mea_oracle_fwd_lazy(int64_t batch, int64_t heads, int64_t n_q,
     const double* qh = q + bh * n_q * d;
     const double* kh = k + bh * n_k * d;
     const double* vh = v + bh * n_k * d;
+    const int64_t n_valid = slice_valid(kv_len, bh, heads, n_k);
 #pragma omp parallel for schedule(dynamic, 8)
     for (int64_t i = 0; i < n_q; ++i)
-      lazy_row(qh + i * d, kh, vh, visible_keys(i, n_k, causal), d, scale,
+      lazy_row(qh + i * d, kh, vh, visible_keys(i, n_k, causal, n_valid), d, scale,
                scratch + thread_id() * d, o + (bh * n_q + i) * d,
                lse + bh * n_q + i);
   }
@@ -264,6 +288,11 @@ static void chunk_summaries(const double* qi, const double* k, const double* v,
 static void combine_summaries(int64_t n_chunks, int64_t d, double* values,
                               double* weights, const double* maxes,
                               double* out, double* lse) {
+  if (n_chunks == 0) { /* no visible key: the empty sums give o = 0 */
+    for (int64_t t = 0; t < d; ++t) out[t] = 0.0;
+    *lse = -INFINITY;
+    return;
+  }
   double global_max = -INFINITY;
   for (int64_t c = 0; c < n_chunks; ++c)
     if (maxes[c] > global_max) global_max = maxes[c];
@@ -285,8 +314,9 @@ static void combine_summaries(int64_t n_chunks, int64_t d, double* values,
 int mea_oracle_fwd_chunked(int64_t batch, int64_t heads, int64_t n_q,
                            int64_t n_k, int64_t d, const double* q,
                            const double* k, const double* v, double scale,
-                           int causal, int64_t query_chunk, int64_t key_chunk,
-                           double* o, double* lse) {
+                           int causal, const int64_t* kv_len,
+                           int64_t query_chunk, int64_t key_chunk, double* o,
+                           double* lse) {
   if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || query_chunk < 1 ||
       key_chunk < 1 || !q || !k || !v || !o || !lse)
     return ORACLE_EINVAL;
@@ -300,6 +330,7 @@ int mea_oracle_fwd_chunked(int64_t batch, int64_t heads, int64_t n_q,
     const double* qh = q + bh * n_q * d;
     const double* kh = k + bh * n_k * d;
     const double* vh = v + bh * n_k * d;
+    const int64_t n_valid = slice_valid(kv_len, bh, heads, n_k);
     /* Outer loop over query chunks; each chunk's rows go straight to o. */
     for (int64_t i0 = 0; i0 < n_q; i0 += query_chunk) {
       const int64_t i1 = (i0 + query_chunk < n_q) ? i0 + query_chunk : n_q;
@@ -309,7 +340,7 @@ int mea_oracle_fwd_chunked(int64_t batch, int64_t heads, int64_t n_q,
         double* weights = values + max_chunks * d;
         double* maxes = weights + max_chunks;
         double* s = maxes + max_chunks;
-        const int64_t n_vis = visible_keys(i, n_k, causal);
+        const int64_t n_vis = visible_keys(i, n_k, causal, n_valid);
         const int64_t n_chunks = (n_vis + key_chunk - 1) / key_chunk;
         chunk_summaries(qh + i * d, kh, vh, n_vis, d, scale, key_chunk, values,
                         weights, maxes, s);
@@ -353,10 +384,10 @@ static void row_stats(const double* qi, const double* doi, const double* k,
 int mea_oracle_bwd_dq_rows(int64_t n_q, int64_t n_k, int64_t d,
                            const double* q, const double* k, const double* v,
                            const double* dout, double scale, int causal,
-                           const int64_t* rows, int64_t n_rows,
-                           double* dq_rows) {
+                           int64_t n_valid, const int64_t* rows,
+                           int64_t n_rows, double* dq_rows) {
   if (!dims_ok(n_q, n_k, d) || n_rows < 0 || !q || !k || !v || !dout ||
-      !rows || !dq_rows)
+      !rows || !dq_rows || n_valid < 0 || n_valid > n_k)
     return ORACLE_EINVAL;
   for (int64_t r = 0; r < n_rows; ++r)
     if (rows[r] < 0 || rows[r] >= n_q) return ORACLE_EINVAL;
@@ -368,7 +399,7 @@ int mea_oracle_bwd_dq_rows(int64_t n_q, int64_t n_k, int64_t d,
     const int64_t i = rows[r];
     const double* qi = q + i * d;
     const double* doi = dout + i * d;
-    const int64_t n_vis = visible_keys(i, n_k, causal);
+    const int64_t n_vis = visible_keys(i, n_k, causal, n_valid);
     double m, l, D;
     row_stats(qi, doi, k, v, n_vis, d, scale, s, &m, &l, &D);
     double* dqi = dq_rows + r * d;
@@ -391,9 +422,10 @@ int mea_oracle_bwd_dq_rows(int64_t n_q, int64_t n_k, int64_t d,
 int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
                              const double* q, const double* k, const double* v,
                              const double* dout, double scale, int causal,
-                             const int64_t* keys, int64_t n_keys,
-                             double* dk_rows, double* dv_rows) {
-  if (!dims_ok(n_q, n_k, d) || n_keys < 0 || !q || !k || !v || !dout || !keys)
+                             int64_t n_valid, const int64_t* keys,
+                             int64_t n_keys, double* dk_rows, double* dv_rows) {
+  if (!dims_ok(n_q, n_k, d) || n_keys < 0 || !q || !k || !v || !dout ||
+      !keys || n_valid < 0 || n_valid > n_k)
     return ORACLE_EINVAL;
   for (int64_t r = 0; r < n_keys; ++r)
     if (keys[r] < 0 || keys[r] >= n_k) return ORACLE_EINVAL;
@@ -416,8 +448,9 @@ int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
   /* Pass 1: per-query softmax statistics. */
 #pragma omp parallel for schedule(dynamic, 8)
   for (int64_t i = 0; i < n_q; ++i)
-    row_stats(q + i * d, dout + i * d, k, v, visible_keys(i, n_k, causal), d,
-              scale, scratch + thread_id() * n_k, &m[i], &l[i], &D[i]);
+    row_stats(q + i * d, dout + i * d, k, v,
+              visible_keys(i, n_k, causal, n_valid), d, scale,
+              scratch + thread_id() * n_k, &m[i], &l[i], &D[i]);
   free(scratch);
   /* Pass 2: per requested key, sum over the queries that see it. */
 #pragma omp parallel for schedule(dynamic, 8)
@@ -429,7 +462,8 @@ int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
     double* dvj = dv_rows ? dv_rows + r * d : NULL;
     if (dkj) for (int64_t t = 0; t < d; ++t) dkj[t] = 0.0;
     if (dvj) for (int64_t t = 0; t < d; ++t) dvj[t] = 0.0;
-    const int64_t i_first = causal ? j : 0; /* query i sees key j iff j <= i */
+    /* query i sees key j iff j < n_valid and, causal, j <= i */
+    const int64_t i_first = j >= n_valid ? n_q : (causal ? j : 0);
     for (int64_t i = i_first; i < n_q; ++i) {
       const double* qi = q + i * d;
       const double* doi = dout + i * d;
@@ -451,8 +485,8 @@ int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
 /* Full [B, H, n, d] backward. */
 int mea_oracle_bwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
                    int64_t d, const double* q, const double* k, const double* v,
-                   const double* dout, double scale, int causal, double* dq,
-                   double* dk, double* dv) {
+                   const double* dout, double scale, int causal,
+                   const int64_t* kv_len, double* dq, double* dk, double* dv) {
   if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || !dq || !dk || !dv)
     return ORACLE_EINVAL;
   const int64_t n_max = n_q > n_k ? n_q : n_k;
@@ -465,12 +499,13 @@ int mea_oracle_bwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
     const double* kh = k + bh * n_k * d;
     const double* vh = v + bh * n_k * d;
     const double* doh = dout + bh * n_q * d;
+    const int64_t n_valid = slice_valid(kv_len, bh, heads, n_k);
     err = mea_oracle_bwd_dq_rows(n_q, n_k, d, qh, kh, vh, doh, scale, causal,
-                                 idx, n_q, dq + bh * n_q * d);
+                                 n_valid, idx, n_q, dq + bh * n_q * d);
     if (err == ORACLE_OK)
       err = mea_oracle_bwd_dkdv_keys(n_q, n_k, d, qh, kh, vh, doh, scale,
-                                     causal, idx, n_k, dk + bh * n_k * d,
-                                     dv + bh * n_k * d);
+                                     causal, n_valid, idx, n_k,
+                                     dk + bh * n_k * d, dv + bh * n_k * d);
   }
   free(idx);
   return err;

@@ -55,6 +55,7 @@ class MeaProblem(ctypes.Structure):
         ("scale", ctypes.c_float),
         ("out_f32", ctypes.c_int32),
         ("strides", ctypes.POINTER(MeaStrides)),
+        ("kv_len", ctypes.c_void_p),
     ]
 
 
@@ -102,12 +103,14 @@ def check(name: str, status: int) -> None:
 
 
 def problem(batch, heads, n_q, n_k, d, dtype, causal, scale, out_f32=False,
-            strides: dict | None = None) -> MeaProblem:
+            strides: dict | None = None, kv_len: int | None = None) -> MeaProblem:
     """``strides`` maps tensor names (q, k, v, o, d_o, dq, dk, dv) to
     (batch, head, row) element strides; missing names and None mean contiguous
-    [B, H, n, d]."""
+    [B, H, n, d].  ``kv_len`` is the device address of an int32 [B] array of
+    valid key lengths (key padding), or None."""
     p = MeaProblem(int(batch), int(heads), int(n_q), int(n_k), int(d), int(dtype),
-                   int(bool(causal)), float(scale), int(bool(out_f32)), None)
+                   int(bool(causal)), float(scale), int(bool(out_f32)), None,
+                   int(kv_len) if kv_len else None)
     if strides:
         st = MeaStrides()
         for name, n in (("q", n_q), ("k", n_k), ("v", n_k), ("o", n_q), ("d_o", n_q),

@@ -23,9 +23,10 @@ _DTYPE_CODE = {torch.float32: _lib.MEA_F32, torch.float16: _lib.MEA_F16,
 
 
 def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: bool = False,
-             tensors: dict | None = None):
+             tensors: dict | None = None, kv_len: torch.Tensor | None = None):
     """``tensors`` maps ABI tensor names (q, k, v, o, d_o, dq, dk, dv) to the
-    tensors of a call, whose strides are passed when any is not contiguous."""
+    tensors of a call, whose strides are passed when any is not contiguous.
+    ``kv_len``: int32 [B] tensor on q's device (valid keys per batch) or None."""
     if q.dim() != 4 or k.dim() != 4:
         raise ValueError("q and k must be [B, H, n, d]")
     B, H, n_q, d = q.shape
@@ -37,8 +38,13 @@ def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: boo
     strides = None
     if tensors and any(not t.is_contiguous() for t in tensors.values() if t is not None):
         strides = {name: tuple(t.stride()[:3]) for name, t in tensors.items() if t is not None}
+    if kv_len is not None:
+        if kv_len.dtype != torch.int32 or kv_len.device != q.device or tuple(kv_len.shape) != (B,) \
+                or not kv_len.is_contiguous():
+            raise ValueError("kv_len must be a contiguous int32 [B] tensor on q's device")
     return _lib.problem(B, H, n_q, n_k, d, _DTYPE_CODE[q.dtype], causal, scale,
-                        out_f32 and q.dtype != torch.float32, strides)
+                        out_f32 and q.dtype != torch.float32, strides,
+                        kv_len.data_ptr() if kv_len is not None else None)
 
 
 def _check_tensors(names, tensors, dtype, device):
@@ -74,9 +80,11 @@ def bwd_workspace_bytes(q, k, causal=False, scale=None) -> int:
 
 def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: bool = False,
                   scale: float | None = None, need_lse: bool = True, out=None,
-                  out_dtype: torch.dtype | None = None):
+                  out_dtype: torch.dtype | None = None, kv_len: torch.Tensor | None = None):
     """Returns ``(o, lse)``; ``lse`` is float32 ``[B, H, n_q]`` (None if not needed).
-    ``out_dtype`` is q's dtype (default) or torch.float32."""
+    ``out_dtype`` is q's dtype (default) or torch.float32.  ``kv_len`` (int32
+    ``[B]`` on the GPU) masks keys ``j >= kv_len[b]`` of batch b (key padding);
+    a row with no visible key gets o = 0 and lse = -inf."""
     if k.shape != v.shape or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
         raise ValueError("shape mismatch: q %s k %s v %s" % (tuple(q.shape), tuple(k.shape),
                                                               tuple(v.shape)))
@@ -89,7 +97,7 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: boo
     if o.shape != q.shape:
         raise ValueError("out must have q's shape")
     p = _problem(q, k, causal, scale, out_dtype == torch.float32,
-                 {"q": q, "k": k, "v": v, "o": o})
+                 {"q": q, "k": k, "v": v, "o": o}, kv_len)
     lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if need_lse else None
     ws_bytes = _lib.fwd_workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device) if ws_bytes else None
@@ -101,10 +109,12 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: boo
 
 
 def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None = None,
-                  need_dq: bool = True, need_dkdv: bool = True, out=None):
+                  need_dq: bool = True, need_dkdv: bool = True, out=None,
+                  kv_len: torch.Tensor | None = None):
     """Returns ``(dq, dk, dv)`` for the upstream gradient ``do``; a gradient that
     is not needed is returned as None and its kernel is not run.  ``out`` may
-    give the (dq, dk, dv) tensors to write (any may be None: allocated)."""
+    give the (dq, dk, dv) tensors to write (any may be None: allocated).
+    ``kv_len`` must be the forward's; masked keys get zero dk and dv rows."""
     _check_tensors(("q", "k", "v"), (q, k, v), q.dtype, q.device)
     if o.dtype not in (q.dtype, torch.float32):
         raise TypeError("o must have q's dtype or float32")
@@ -127,7 +137,7 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
         if t.shape != (q.shape if n_ == "dq" else k.shape):
             raise ValueError("%s has the wrong shape" % n_)
     p = _problem(q, k, causal, scale, o.dtype == torch.float32,
-                 {"q": q, "k": k, "v": v, "o": o, "d_o": do, "dq": dq, "dk": dk, "dv": dv})
+                 {"q": q, "k": k, "v": v, "o": o, "d_o": do, "dq": dq, "dk": dk, "dv": dv}, kv_len)
     ws_bytes = _lib.bwd_workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     _lib.check("mea_attention_bwd", _lib.bwd(
@@ -143,20 +153,22 @@ class MemoryEfficientAttention(torch.autograd.Function):
     """Autograd wrapper: saves only q, k, v, o and the O(n) lse."""
 
     @staticmethod
-    def forward(ctx, q, k, v, causal=False, scale=None, out_dtype=None):
+    def forward(ctx, q, k, v, causal=False, scale=None, out_dtype=None, kv_len=None):
         q, k, v = (_feature_contiguous(t) for t in (q, k, v))
-        o, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out_dtype=out_dtype)
+        o, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out_dtype=out_dtype,
+                               kv_len=kv_len)
         ctx.save_for_backward(q, k, v, o, lse)
         ctx.causal = causal
         ctx.scale = scale
+        ctx.kv_len = kv_len
         return o
 
     @staticmethod
     def backward(ctx, do):
         q, k, v, o, lse = ctx.saved_tensors
         dq, dk, dv = attention_bwd(q, k, v, o, lse, _feature_contiguous(do.to(o.dtype)), ctx.causal,
-                                   ctx.scale)
-        return dq, dk, dv, None, None, None
+                                   ctx.scale, kv_len=ctx.kv_len)
+        return dq, dk, dv, None, None, None, None
 
 
 def _feature_contiguous(t: torch.Tensor) -> torch.Tensor:
@@ -177,16 +189,17 @@ class PackedQKVAttention(torch.autograd.Function):
     direction copies or transposes.  Saves qkv, o and the O(n) lse."""
 
     @staticmethod
-    def forward(ctx, qkv, causal=False, scale=None):
+    def forward(ctx, qkv, causal=False, scale=None, kv_len=None):
         if qkv.dim() != 5 or qkv.shape[2] != 3:
             raise ValueError("qkv must be [B, n, 3, H, d]")
         qkv = qkv if qkv.is_contiguous() else qkv.contiguous()
         B, n, _, H, d = qkv.shape
         q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))  # [B, H, n, d] views
         o = torch.empty(B, n, H, d, dtype=qkv.dtype, device=qkv.device)
-        _, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out=o.transpose(1, 2))
+        _, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out=o.transpose(1, 2),
+                               kv_len=kv_len)
         ctx.save_for_backward(qkv, o, lse)
-        ctx.causal, ctx.scale = causal, scale
+        ctx.causal, ctx.scale, ctx.kv_len = causal, scale, kv_len
         return o
 
     @staticmethod
@@ -196,17 +209,21 @@ class PackedQKVAttention(torch.autograd.Function):
         dqkv = torch.empty_like(qkv)
         dq, dk, dv = (dqkv[:, :, i].transpose(1, 2) for i in range(3))
         do_ = _feature_contiguous(do.to(o.dtype).transpose(1, 2))
-        attention_bwd(q, k, v, o.transpose(1, 2), lse, do_, ctx.causal, ctx.scale, out=(dq, dk, dv))
-        return dqkv, None, None
+        attention_bwd(q, k, v, o.transpose(1, 2), lse, do_, ctx.causal, ctx.scale, out=(dq, dk, dv),
+                      kv_len=ctx.kv_len)
+        return dqkv, None, None, None
 
 
-def attention_packed(qkv, causal: bool = False, scale: float | None = None):
+def attention_packed(qkv, causal: bool = False, scale: float | None = None,
+                     kv_len: torch.Tensor | None = None):
     """Exact softmax self-attention of a packed ``[B, n, 3, H, d]`` projection,
-    differentiable, O(n) extra memory; returns ``[B, n, H, d]``."""
-    return PackedQKVAttention.apply(qkv, causal, scale)
+    differentiable, O(n) extra memory; returns ``[B, n, H, d]``.  ``kv_len``:
+    optional int32 ``[B]`` valid key lengths (key padding)."""
+    return PackedQKVAttention.apply(qkv, causal, scale, kv_len)
 
 
 def attention(q, k, v, causal: bool = False, scale: float | None = None,
-              out_dtype: torch.dtype | None = None):
-    """Exact softmax attention, differentiable, O(n) extra memory."""
-    return MemoryEfficientAttention.apply(q, k, v, causal, scale, out_dtype)
+              out_dtype: torch.dtype | None = None, kv_len: torch.Tensor | None = None):
+    """Exact softmax attention, differentiable, O(n) extra memory.  ``kv_len``:
+    optional int32 ``[B]`` valid key lengths (keys ``j >= kv_len[b]`` masked)."""
+    return MemoryEfficientAttention.apply(q, k, v, causal, scale, out_dtype, kv_len)

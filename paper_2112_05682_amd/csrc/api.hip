@@ -31,6 +31,7 @@ mea_status check_problem(const mea_problem* p) {
   if (p->causal != 0 && p->causal != 1) return MEA_ERR_INVALID_ARG;
   if (p->out_f32 != 0 && p->out_f32 != 1) return MEA_ERR_INVALID_ARG;
   if (!(p->scale > 0.0f) || !isfinite(p->scale)) return MEA_ERR_INVALID_ARG;
+  if (p->kv_len && ((uintptr_t)p->kv_len & 3u)) return MEA_ERR_INVALID_ARG;
   int64_t bh, nq_d, nk_d, tot;
   if (!mul_ok(p->batch, p->heads, &bh) || bh >= kMaxSeq) return MEA_ERR_INVALID_ARG;
   if (!mul_ok(p->n_q, p->d, &nq_d) || !mul_ok(p->n_k, p->d, &nk_d)) return MEA_ERR_INVALID_ARG;
@@ -220,6 +221,7 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
   fp.v = v;
   fp.o = o;
   fp.lse = lse;
+  fp.kv_len = p->kv_len;
   fp.n_q = p->n_q;
   fp.n_k = p->n_k;
   fp.keys_per_split = pl.keys_per_split;
@@ -293,6 +295,7 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
     bp.s_init = align256(workspace, 0);
     bp.dp_init = bp.s_init + bwd_row_array_bytes(p, 4) / 4;
   }
+  bp.kv_len = p->kv_len;
   bp.n_q = p->n_q;
   bp.n_k = p->n_k;
   bp.bh = (int)(p->batch * p->heads);

@@ -92,8 +92,10 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
       r[3] = r[7] = (__bf16)0.0f;
       p.row_rec[prow] = __builtin_bit_cast(uint4, r);
     } else {
-      p.s_init[prow] = real ? -lse / p.scale : -INFINITY;
-      p.dp_init[prow] = real ? -acc : 0.0f;
+      // Rows with no finite lse (padding, or no visible key) get weights 0.
+      const bool live = real && __builtin_isfinite(lse);
+      p.s_init[prow] = live ? -lse / p.scale : -INFINITY;
+      p.dp_init[prow] = live ? -acc : 0.0f;
     }
   }
 }
@@ -171,9 +173,11 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       dv[dt][r] = 0.0f;
     }
 
-  // Queries before the first key of this tile see none of its keys.
+  // Queries before the first key of this tile see none of its keys; a tile
+  // past the batch's valid keys (key padding) is seen by none.
+  const int64_t n_kv = valid_keys(p.kv_len, bh, p.heads, p.n_k);
   const int64_t q_begin = CAUSAL ? (k0 / Cfg::BQ) * Cfg::BQ : 0;
-  const int n_iters = q_begin < p.n_q ? (int)((p.n_q - q_begin + Cfg::BQ - 1) / Cfg::BQ) : 0;
+  const int n_iters = q_begin < p.n_q && k0 < n_kv ? (int)((p.n_q - q_begin + Cfg::BQ - 1) / Cfg::BQ) : 0;
 
   u32x4 stage[Cfg::CPT];
   float stage_f = 0.0f;
@@ -323,9 +327,9 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int64_t kr = kw + c_row(r, h);
-      if (kr < p.n_k) {
-        dkg[kr * p.sdk.r + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
-        dvg[kr * p.sdv.r + 32 * dt + c] = (T)dv[dt][r];
+      if (kr < p.n_k) {  // keys past the valid length get zero gradients
+        dkg[kr * p.sdk.r + 32 * dt + c] = kr < n_kv ? (T)(dk[dt][r] * p.scale) : (T)0.0f;
+        dvg[kr * p.sdv.r + 32 * dt + c] = kr < n_kv ? (T)dv[dt][r] : (T)0.0f;
       }
     }
 }
@@ -402,9 +406,11 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
       dv[dt][r] = 0.0f;
     }
 
-  // Queries before the workgroup's first key see none of its keys (causal).
+  // Queries before the workgroup's first key see none of its keys (causal);
+  // a workgroup past the batch's valid keys (key padding) is seen by none.
+  const int64_t n_kv = valid_keys(p.kv_len, bh, p.heads, p.n_k);
   const int64_t q_begin = CAUSAL ? (k0 / BQ) * BQ : 0;
-  const int n_iters = q_begin < p.n_q ? (int)((p.n_q - q_begin + BQ - 1) / BQ) : 0;
+  const int n_iters = q_begin < p.n_q && k0 < n_kv ? (int)((p.n_q - q_begin + BQ - 1) / BQ) : 0;
   auto stage = [&](int i) { return smem + (i % NSTAGE) * STAGEB; };
 
   // Copy unit u (0 <= u < UNITS) of query tile i into its stage: units 0..8
@@ -669,9 +675,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int64_t kr = kw + c_row(r, h);
-      if (kr < p.n_k) {
-        dkg[kr * p.sdk.r + 32 * dt + c] = (T)(dk[dt][r] * p.scale);
-        dvg[kr * p.sdv.r + 32 * dt + c] = (T)dv[dt][r];
+      if (kr < p.n_k) {  // keys past the valid length get zero gradients
+        dkg[kr * p.sdk.r + 32 * dt + c] = kr < n_kv ? (T)(dk[dt][r] * p.scale) : (T)0.0f;
+        dvg[kr * p.sdv.r + 32 * dt + c] = kr < n_kv ? (T)dv[dt][r] : (T)0.0f;
       }
     }
 }
@@ -747,7 +753,10 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[t][dt][r] = 0.0f;
 
-  int64_t ke = p.n_k;
+  // Keys visible to this (batch, head): n_k, or the batch's valid length
+  // (key padding); loads stay bounded by n_k.
+  const int64_t n_kv = valid_keys(p.kv_len, bh, p.heads, p.n_k);
+  int64_t ke = n_kv;
   if (CAUSAL && ke > q0 + BQ) ke = q0 + BQ;
   const int n_tiles = (int)((ke + BK - 1) / BK);
 
@@ -787,7 +796,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 
   // Leading tiles that need no mask (all keys exist and, causal, precede the
   // workgroup's first query); masked tiles run in a second loop.
-  int n_plain = (int)(p.n_k / BK);
+  int n_plain = (int)(n_kv / BK);
   if (n_plain > n_tiles) n_plain = n_tiles;
   if (CAUSAL) {
     const int below = (int)((q0 + 1) / BK);
@@ -828,7 +837,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
     // under the causal mask, visible to query qw + 32t + c iff x <= q_rel + 32t.
     int key_lim = BK, q_rel = BK;
     if constexpr (MASK) {
-      key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+      key_lim = (int)(n_kv - k0 < BK ? n_kv - k0 : BK);
       if (CAUSAL) q_rel = (int)(qw - k0) + c;
     }
 #pragma unroll
@@ -973,8 +982,11 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[dt][r] = 0.0f;
 
-  // Keys after the workgroup's last query are invisible to all of it (causal).
-  int64_t ke = p.n_k;
+  // Keys after the workgroup's last query are invisible to all of it (causal),
+  // and so are keys past the batch's valid length (key padding); loads stay
+  // bounded by n_k.
+  const int64_t n_kv = valid_keys(p.kv_len, bh, p.heads, p.n_k);
+  int64_t ke = n_kv;
   if (CAUSAL && ke > q0 + BQG) ke = q0 + BQG;
   const int n_tiles = (int)((ke + BK - 1) / BK);
   auto stage = [&](int j) { return smem + (j % NSTAGE) * STAGEB; };
@@ -985,7 +997,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   // lane's byte offset within a tile is computed once per unit; a tile that
   // ends past n_k takes the clamped path, whose rows past n_k repeat the last
   // key (finite values; masked).
-  const int n_full = (int)(p.n_k / BK);  // tiles with no key past n_k
+  const int n_full = (int)(n_kv / BK);  // tiles with no key past the valid length
   auto unit_row = [&](int u) { return (64 * (u % 9) + lane) / 9; };
   auto unit_col = [&](int u) {
     const int ch = (64 * (u % 9) + lane) % 9;
@@ -1066,7 +1078,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   // Whether tile j needs the elementwise mask (ragged keys, causal diagonal).
   auto masked = [&](int j) {
     const int64_t k0 = (int64_t)j * BK;
-    return k0 + BK > p.n_k || (CAUSAL && k0 + BK - 1 > qw);
+    return k0 + BK > n_kv || (CAUSAL && k0 + BK - 1 > qw);
   };
   constexpr int AHEAD = CAUSAL ? 2 : MEA_T64_DQ_AHEAD;
   // dQ^T += K^T dS^T for tile j (column fragments of K: k = keys).
@@ -1122,7 +1134,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
   // key k0 + x is valid iff x < lim (ragged tail; causal: x <= query - k0).
   auto key_lim = [&](int j) {
     const int64_t k0 = (int64_t)j * BK;
-    int lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+    int lim = (int)(n_kv - k0 < BK ? n_kv - k0 : BK);
     if (CAUSAL) {
       const int64_t qr = query - k0 + 1;
       if (qr < lim) lim = qr > 0 ? (int)qr : 0;

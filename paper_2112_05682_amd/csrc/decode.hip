@@ -64,7 +64,9 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
   const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
   const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
-  const int64_t n_keys = decode_keys(p.n_q, p.n_k, CAUSAL);
+  // Keys visible to this (batch, head): n_k, or the batch's valid length
+  // (key padding); with the causal mask at most the first n_q of them.
+  const int64_t n_keys = decode_keys(p.n_q, valid_keys(p.kv_len, bh, p.heads, p.n_k), CAUSAL);
   const int64_t kb = (int64_t)split * p.keys_per_split;
   int64_t ke = kb + p.keys_per_split;
   if (ke > n_keys) ke = n_keys;
@@ -238,7 +240,7 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
     const int64_t row = 32 * t + c;
     if (row >= p.n_q) continue;
     if (p.n_splits == 1) {
-      const float inv = 1.0f / l_tot;
+      const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;  // no visible key: o = 0
       TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
@@ -249,7 +251,8 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
           for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
           *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
         }
-      if (h == 0 && p.lse) p.lse[(size_t)bh * p.n_q + row] = (m_run[t] + __log2f(l_tot)) * 0.6931471805599453f;
+      if (h == 0 && p.lse)
+        p.lse[(size_t)bh * p.n_q + row] = l_tot > 0.0f ? (m_run[t] + __log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
     } else {
       const size_t prow = ((size_t)split * p.bh + bh) * p.n_q + row;
       float* po = p.part_o + prow * D;

@@ -82,9 +82,11 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
   const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
+  // Keys visible to this (batch, head): n_k, or the batch's valid length.
+  const int64_t n_k = valid_keys(p.kv_len, bh, p.heads, p.n_k);
   const int64_t kb = (int64_t)split * p.keys_per_split;
   int64_t ke = kb + p.keys_per_split;
-  if (ke > p.n_k) ke = p.n_k;
+  if (ke > n_k) ke = n_k;
   if (CAUSAL && ke > q0 + Cfg::BQ) ke = q0 + Cfg::BQ;  // keys beyond the last query are masked
   const int n_tiles = ke > kb ? (int)((ke - kb + BK - 1) / BK) : 0;
 
@@ -156,7 +158,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   // tail) and, under the causal mask, precedes the workgroup's first query.
   int n_plain = n_tiles;
   {
-    const int64_t full = (p.n_k - kb) / BK;
+    const int64_t full = n_k > kb ? (n_k - kb) / BK : 0;
     if (full < n_plain) n_plain = (int)full;
     if (CAUSAL) {
       const int64_t below = q0 - kb + 1 > 0 ? (q0 - kb + 1) / BK : 0;
@@ -194,7 +196,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
     if constexpr (MASK) {
       // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
       // under the causal mask, visible to query qw + 32t + c iff x <= q_rel + 32t.
-      const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+      const int key_lim = (int)(n_k - k0 < BK ? n_k - k0 : BK);
       const int q_rel = CAUSAL ? (int)(qw - k0) + c : BK;
 #pragma unroll
       for (int t = 0; t < QT; ++t) {
@@ -288,7 +290,8 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
     const int64_t row = qw + 32 * t + c;
     if (row >= p.n_q) continue;
     if (p.n_splits == 1) {
-      const float inv = 1.0f / l_tot;
+      // A row with no visible key (key padding) has l = 0: o = 0, lse = -inf.
+      const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
       TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
@@ -300,7 +303,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
           *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
         }
       if (h == 0 && p.lse)
-        p.lse[(size_t)bh * p.n_q + row] = (m_ref[t] + __log2f(l_tot)) * kLn2;
+        p.lse[(size_t)bh * p.n_q + row] = l_tot > 0.0f ? (m_ref[t] + __log2f(l_tot)) * kLn2 : -INFINITY;
     } else {
       const size_t prow = ((size_t)split * p.bh + bh) * p.n_q + row;
       float* po = p.part_o + prow * D;
@@ -381,14 +384,17 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   const T* __restrict__ kg = static_cast<const T*>(p.k) + head_base(p.sk, bh, p.heads);
   const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
+  // Keys visible to this (batch, head): n_k, or the batch's valid length
+  // (key padding); loads stay bounded by n_k.
+  const int64_t n_k = valid_keys(p.kv_len, bh, p.heads, p.n_k);
   const int64_t kb = (int64_t)split * p.keys_per_split;
   int64_t ke = kb + p.keys_per_split;
-  if (ke > p.n_k) ke = p.n_k;
+  if (ke > n_k) ke = n_k;
   if (CAUSAL && ke > q0 + BQ) ke = q0 + BQ;
   const int n_tiles = ke > kb ? (int)((ke - kb + BK - 1) / BK) : 0;
   int n_plain = n_tiles;
   {
-    const int64_t full = (p.n_k - kb) / BK;
+    const int64_t full = n_k > kb ? (n_k - kb) / BK : 0;
     if (full < n_plain) n_plain = (int)full;
     if (CAUSAL) {
       const int64_t below = q0 - kb + 1 > 0 ? (q0 - kb + 1) / BK : 0;
@@ -504,7 +510,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   auto mask_sub = [&](int j, auto t_tag, f32x16 (&s)[NKT][QT]) __attribute__((always_inline)) {
     constexpr int t = decltype(t_tag)::value;
     const int64_t k0 = kb + (int64_t)j * BK;
-    const int key_lim = (int)(p.n_k - k0 < BK ? p.n_k - k0 : BK);
+    const int key_lim = (int)(n_k - k0 < BK ? n_k - k0 : BK);
     const int lim_c = CAUSAL ? (int)(qw - k0) + c + 32 * t + 1 : BK;
     const int lim = lim_c < key_lim ? lim_c : key_lim;
 #pragma unroll
@@ -734,7 +740,8 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
     const int64_t row = qw + 32 * t + c;
     if (row >= p.n_q) continue;
     if (p.n_splits == 1) {
-      const float inv = 1.0f / l_tot;
+      // A row with no visible key (key padding) has l = 0: o = 0, lse = -inf.
+      const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
       TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
@@ -746,7 +753,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
           *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
         }
       if (h == 0 && p.lse)
-        p.lse[(size_t)bh * p.n_q + row] = (m_ref[t] + __log2f(l_tot)) * kLn2;
+        p.lse[(size_t)bh * p.n_q + row] = l_tot > 0.0f ? (m_ref[t] + __log2f(l_tot)) * kLn2 : -INFINITY;
     } else {
       const size_t prow = ((size_t)split * p.bh + bh) * p.n_q + row;
       float* po = p.part_o + prow * D;
@@ -790,14 +797,15 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
     const f32x4 ps = *reinterpret_cast<const f32x4*>(p.part_o + (s * stride + row) * D + f0);
     o += wgt * ps;
   }
-  const float inv = 1.0f / l;
+  // No visible key in any range (key padding): o = 0, lse = -inf.
+  const float inv = l > 0.0f ? 1.0f / l : 0.0f;
   typename FragT<TO>::half out;
 #pragma unroll
   for (int e = 0; e < 4; ++e) out[e] = (TO)(o[e] * inv);
   const int bh = (int)(row / p.n_q);
   TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + (row - (int64_t)bh * p.n_q) * p.so.r;
   *reinterpret_cast<typename FragT<TO>::half*>(og + f0) = out;
-  if (f0 == 0 && p.lse) p.lse[row] = (m_g + __log2f(l)) * kLn2;
+  if (f0 == 0 && p.lse) p.lse[row] = l > 0.0f ? (m_g + __log2f(l)) * kLn2 : -INFINITY;
 }
 
 // One stage of the combine: each output range g summarises input ranges

@@ -15,6 +15,16 @@ __host__ __device__ inline int64_t head_base(const TensorStrides& s, int bh, int
   return (int64_t)(bh / heads) * s.b + (int64_t)(bh % heads) * s.h;
 }
 
+// Keys visible to every query of (batch, head) bh: the batch's valid key
+// length from kv_len (device array [B], clamped to [0, n_k]) or all n_k.
+// Keys from there to n_k are masked like keys past the end; they stay
+// readable memory, so loads are bounded by n_k.
+__device__ inline int64_t valid_keys(const int* kv_len, int bh, int heads, int64_t n_k) {
+  if (kv_len == nullptr) return n_k;
+  const int64_t l = kv_len[bh / heads];
+  return l < 0 ? 0 : (l > n_k ? n_k : l);
+}
+
 // Arguments of the forward kernels (passed by value).
 struct FwdParams {
   const void* q;
@@ -30,6 +40,7 @@ struct FwdParams {
   float* part2_o;
   float* part2_m;
   float* part2_l;
+  const int* kv_len;  // [B] valid keys per batch, or null (all n_k)
   int64_t n_q;
   int64_t n_k;
   int64_t keys_per_split;  // multiple of the key tile
@@ -78,6 +89,7 @@ struct BwdParams {
   float* s_init;
   float* dp_init;
   uint4* row_rec;
+  const int* kv_len;  // [B] valid keys per batch, or null (all n_k)
   int64_t n_q_pad;  // n_q rounded up to kBwdRowPad
   int64_t n_q;
   int64_t n_k;

@@ -22,7 +22,8 @@ class MultiheadAttention(nn.Module):
     ``[B, n, 3, H, d]`` tensor that the kernels read in place (strided views,
     ``num_heads`` heads of ``embed_dim // num_heads`` features); the output
     ``[B, n, H, d]`` is the heads' concatenation, projected back.  ``causal``
-    masks key j for query i when j > i.
+    masks key j for query i when j > i; ``kv_len`` (int32 ``[B]`` on the GPU,
+    optional) masks the padded positions j >= kv_len[b] of each sequence.
     """
 
     def __init__(self, embed_dim: int, num_heads: int, causal: bool = False, bias: bool = True,
@@ -38,12 +39,13 @@ class MultiheadAttention(nn.Module):
         self.qkv = nn.Linear(embed_dim, 3 * embed_dim, bias=bias, **kw)
         self.out = nn.Linear(embed_dim, embed_dim, bias=bias, **kw)
 
-    def forward(self, x: torch.Tensor) -> torch.Tensor:
+    def forward(self, x: torch.Tensor, kv_len: torch.Tensor | None = None) -> torch.Tensor:
         B, n, E = x.shape
         if E != self.embed_dim:
             raise ValueError("expected embed_dim %d, got %d" % (self.embed_dim, E))
         qkv = self.qkv(x).view(B, n, 3, self.num_heads, self.head_dim)
-        o = attention_packed(qkv, causal=self.causal)  # [B, n, H, d], no copies either way
+        # [B, n, H, d], no copies either way
+        o = attention_packed(qkv, causal=self.causal, kv_len=kv_len)
         return self.out(o.reshape(B, n, E))
 
 
@@ -61,8 +63,8 @@ class TransformerBlock(nn.Module):
         self.mlp = nn.Sequential(nn.Linear(embed_dim, mlp_ratio * embed_dim, **kw), nn.GELU(),
                                  nn.Linear(mlp_ratio * embed_dim, embed_dim, **kw))
 
-    def forward(self, x: torch.Tensor) -> torch.Tensor:
-        x = x + self.attn(self.norm1(x))
+    def forward(self, x: torch.Tensor, kv_len: torch.Tensor | None = None) -> torch.Tensor:
+        x = x + self.attn(self.norm1(x), kv_len)
         return x + self.mlp(self.norm2(x))
 
 

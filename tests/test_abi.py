@@ -149,12 +149,13 @@ def test_problem_struct_layout_matches_the_header(tmp_path):
     src = tmp_path / "layout.c"
     src.write_text(
         '#include <stddef.h>\n#include <stdio.h>\n#include "mea.h"\n'
-        'int main(void) { printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", '
+        'int main(void) { printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", '
         'sizeof(mea_problem), '
         'offsetof(mea_problem, batch), offsetof(mea_problem, heads), offsetof(mea_problem, n_q), '
         'offsetof(mea_problem, n_k), offsetof(mea_problem, d), offsetof(mea_problem, dtype), '
         'offsetof(mea_problem, causal), offsetof(mea_problem, scale), '
         'offsetof(mea_problem, out_f32), offsetof(mea_problem, strides), '
+        'offsetof(mea_problem, kv_len), '
         'sizeof(mea_strides), offsetof(mea_strides, d_o), offsetof(mea_strides, dv)); return 0; }\n')
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROOT, "include"),
@@ -205,3 +206,13 @@ def test_shared_key_heads_are_valid_input_strides():
     assert ok.strides.contents.k.head == 0
     bad = _strided_prob(dk=(300 * 64, 0, 64))
     assert _lib.bwd(bad, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+
+
+def test_rejects_misaligned_kv_len():
+    # kv_len is an int32 device array: a pointer that is not 4-byte aligned is
+    # rejected before anything is launched (the tensor pointers are fake).
+    p = _lib.problem(1, 2, 100, 100, 64, _lib.MEA_BF16, False, 0.125, kv_len=FAKE + 2)
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.bwd(p, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+    ok = _lib.problem(1, 2, 100, 100, 64, _lib.MEA_BF16, False, 0.125, kv_len=FAKE)
+    assert ok.kv_len == FAKE

@@ -27,28 +27,28 @@ class OracleAttention(torch.autograd.Function):
     hand-derived backward."""
 
     @staticmethod
-    def forward(ctx, q, k, v, causal):
-        o, _ = oracle.fwd(q.numpy(), k.numpy(), v.numpy(), causal=causal)
+    def forward(ctx, q, k, v, causal, kv_len=None):
+        o, _ = oracle.fwd(q.numpy(), k.numpy(), v.numpy(), causal=causal, kv_len=kv_len)
         ctx.save_for_backward(q, k, v)
-        ctx.causal = causal
+        ctx.causal, ctx.kv_len = causal, kv_len
         return torch.from_numpy(o)
 
     @staticmethod
     def backward(ctx, do):
         q, k, v = ctx.saved_tensors
         dq, dk, dv = oracle.bwd(q.numpy(), k.numpy(), v.numpy(), do.contiguous().numpy(),
-                                causal=ctx.causal)
-        return torch.from_numpy(dq), torch.from_numpy(dk), torch.from_numpy(dv), None
+                                causal=ctx.causal, kv_len=ctx.kv_len)
+        return torch.from_numpy(dq), torch.from_numpy(dk), torch.from_numpy(dv), None, None
 
 
-def reference_mha(m: MultiheadAttention, x: torch.Tensor) -> torch.Tensor:
+def reference_mha(m: MultiheadAttention, x: torch.Tensor, kv_len=None) -> torch.Tensor:
     """The module's computation in float64 on the CPU with the oracle's attention."""
     B, n, E = x.shape
     H, d = m.num_heads, m.head_dim
     qkv = torch.nn.functional.linear(x, m.qkv.weight, m.qkv.bias)
     qkv = qkv.view(B, n, 3, H, d).permute(2, 0, 3, 1, 4)
     q, k, v = (t.contiguous() for t in qkv.unbind(0))
-    o = OracleAttention.apply(q, k, v, m.causal)
+    o = OracleAttention.apply(q, k, v, m.causal, kv_len)
     return torch.nn.functional.linear(o.transpose(1, 2).reshape(B, n, E), m.out.weight, m.out.bias)
 
 
@@ -56,10 +56,11 @@ TOLS = {torch.float32: 1e-4, torch.bfloat16: 3e-2}
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["fp32", "bf16"])
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("d,kv_len", [(64, None), (128, None), (64, [50, 77])],
+                         ids=["d64", "d128", "d64-padded"])
 @pytest.mark.parametrize("causal", [False, True])
-def test_mha_module_matches_oracle_composition(dtype, d, causal):
-    print("mha case", dtype, d, causal, flush=True)
+def test_mha_module_matches_oracle_composition(dtype, d, kv_len, causal):
+    print("mha case", dtype, d, kv_len, causal, flush=True)
     torch.manual_seed(0)
     B, n, H = 2, 77, 2
     E = H * d
@@ -67,7 +68,8 @@ def test_mha_module_matches_oracle_composition(dtype, d, causal):
     x = torch.randn(B, n, E, generator=torch.Generator().manual_seed(1)).to("cuda", dtype)
     g = torch.randn(B, n, E, generator=torch.Generator().manual_seed(2)).to("cuda", dtype)
     x.requires_grad_(True)
-    y = m(x)
+    kl = torch.tensor(kv_len, dtype=torch.int32, device="cuda") if kv_len else None
+    y = m(x, kl)
     y.backward(g)
     torch.cuda.synchronize()
 
@@ -82,7 +84,7 @@ def test_mha_module_matches_oracle_composition(dtype, d, causal):
             dst.weight.copy_(src.weight.detach().to("cpu", torch.float64))
             dst.bias.copy_(src.bias.detach().to("cpu", torch.float64))
     xr = x.detach().to("cpu", torch.float64).requires_grad_(True)
-    yr = reference_mha(mr, xr)
+    yr = reference_mha(mr, xr, kv_len)
     yr.backward(g.to("cpu", torch.float64))
 
     tol = TOLS[dtype]

@@ -381,3 +381,169 @@ def test_large_logits_stay_finite_and_shift_invariant(oracle_mod, form):
     assert np.all(np.isfinite(o_big)) and np.all(np.isfinite(l_big))
     np.testing.assert_allclose(o_big, o_ref, rtol=1e-9, atol=1e-10)
     np.testing.assert_allclose(l_big - 1000.0 * scale, l_ref, rtol=1e-9, atol=1e-9)
+
+
+# ---------------------------------------------------------------- key padding
+# Batch b sees only keys j < kv_len[b] (on top of the causal mask); a row that
+# sees no key has o = 0, lse = -inf and zero gradients.  Pinned against scipy
+# with -inf scores, closed forms, invariance under changing the padded rows,
+# the empty batch, and central differences.
+
+def _masked_scores(q, k, scale, n_valid, causal):
+    s = scale * (q @ k.T)
+    nq, nk = s.shape
+    vis = np.arange(nk)[None, :] < n_valid
+    if causal:
+        vis = vis & (np.arange(nk)[None, :] <= np.arange(nq)[:, None])
+    return np.where(vis, s, -np.inf)
+
+
+def run_fwd_kv(oracle, form, q, k, v, scale, causal, kv_len):
+    if form == "direct":
+        return oracle.fwd(q, k, v, scale, causal, kv_len=kv_len)
+    if form == "lazy":
+        return oracle.fwd_lazy(q, k, v, scale, causal, kv_len=kv_len)
+    return oracle.fwd_chunked(q, k, v, scale, causal, query_chunk=2, key_chunk=3, kv_len=kv_len)
+
+
+@pytest.mark.parametrize("form", FORWARD_FORMS)
+@pytest.mark.parametrize("causal", [False, True])
+def test_key_padding_matches_scipy_softmax(oracle_mod, form, causal):
+    B, H, nq, nk, d = 3, 2, 7, 11, 5
+    q, k, v = rand((B, H, nq, d), 60), rand((B, H, nk, d), 61), rand((B, H, nk, d), 62)
+    kv_len = [4, 11, 1]
+    scale = 0.41
+    o, lse = run_fwd_kv(oracle_mod, form, q, k, v, scale, causal, kv_len)
+    for b in range(B):
+        for h in range(H):
+            s = _masked_scores(q[b, h], k[b, h], scale, kv_len[b], causal)
+            np.testing.assert_allclose(o[b, h], softmax(s, axis=1) @ v[b, h], rtol=1e-12,
+                                       atol=1e-13)
+            np.testing.assert_allclose(lse[b, h], logsumexp(s, axis=1), rtol=1e-13)
+
+
+@pytest.mark.parametrize("form", FORWARD_FORMS)
+@pytest.mark.parametrize("causal", [False, True])
+def test_key_padding_zero_query(oracle_mod, form, causal):
+    # Uniform scores: o_i is the mean of the values row i sees, lse_i = ln |J(i)|.
+    B, H, nq, nk, d = 2, 1, 6, 9, 3
+    v = rand((B, H, nk, d), 63)
+    q, k = np.zeros((B, H, nq, d)), rand((B, H, nk, d), 64)
+    kv_len = [5, 2]
+    o, lse = run_fwd_kv(oracle_mod, form, q, k, v, 0.5, causal, kv_len)
+    for b in range(B):
+        for i in range(nq):
+            n = min(kv_len[b], i + 1) if causal else kv_len[b]
+            np.testing.assert_allclose(o[b, 0, i], v[b, 0, :n].mean(axis=0), rtol=1e-13,
+                                       atol=1e-14)
+            np.testing.assert_allclose(lse[b, 0, i], math.log(n), rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_key_padding_zero_query_gradients(oracle_mod, causal):
+    # Q = 0: dK = 0 everywhere, dV_j = sum over the rows that see key j of
+    # dO_i / |J(i)|, and padded keys get dV = 0.
+    B, H, nq, nk, d = 2, 1, 6, 8, 3
+    q, k, v, do = (np.zeros((B, H, nq, d)), rand((B, H, nk, d), 65), rand((B, H, nk, d), 66),
+                   rand((B, H, nq, d), 67))
+    kv_len = [3, 8]
+    dq, dk, dv = oracle_mod.bwd(q, k, v, do, 0.7, causal, kv_len=kv_len)
+    np.testing.assert_allclose(dk, 0.0, atol=1e-14)
+    for b in range(B):
+        want = np.zeros((nk, d))
+        for i in range(nq):
+            n = min(kv_len[b], i + 1) if causal else kv_len[b]
+            want[:n] += do[b, 0, i] / n
+        np.testing.assert_allclose(dv[b, 0], want, rtol=1e-13, atol=1e-14)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_key_padding_ignores_padded_rows(oracle_mod, causal):
+    # Changing k and v at padded positions changes nothing, and the padded
+    # keys' gradients are exactly zero.
+    B, H, nq, nk, d = 2, 2, 9, 13, 4
+    q, k, v, do = (rand((B, H, nq, d), 68), rand((B, H, nk, d), 69), rand((B, H, nk, d), 70),
+                   rand((B, H, nq, d), 71))
+    kv_len = [6, 10]
+    k2, v2 = k.copy(), v.copy()
+    for b, n in enumerate(kv_len):
+        k2[b, :, n:] = rand(k2[b, :, n:].shape, 72 + b) * 50.0
+        v2[b, :, n:] = rand(v2[b, :, n:].shape, 74 + b) * 50.0
+    o1, l1 = oracle_mod.fwd(q, k, v, 0.5, causal, kv_len=kv_len)
+    o2, l2 = oracle_mod.fwd(q, k2, v2, 0.5, causal, kv_len=kv_len)
+    np.testing.assert_array_equal(o1, o2)
+    np.testing.assert_array_equal(l1, l2)
+    g1 = oracle_mod.bwd(q, k, v, do, 0.5, causal, kv_len=kv_len)
+    g2 = oracle_mod.bwd(q, k2, v2, do, 0.5, causal, kv_len=kv_len)
+    for a, b_ in zip(g1, g2):
+        for b, n in enumerate(kv_len):
+            np.testing.assert_array_equal(a[b, :, :n] if a.shape[2] == nk else a[b],
+                                          b_[b, :, :n] if b_.shape[2] == nk else b_[b])
+    for g in (g1[1], g1[2], g2[1], g2[2]):
+        for b, n in enumerate(kv_len):
+            assert np.all(g[b, :, n:] == 0.0)
+
+
+@pytest.mark.parametrize("form", FORWARD_FORMS)
+def test_key_padding_empty_batch(oracle_mod, form):
+    # kv_len = 0: every row of the batch sees no key (o = 0, lse = -inf, zero
+    # gradients); the other batch is unaffected.  Negative lengths clamp to 0
+    # and lengths past n_k to n_k.
+    B, H, nq, nk, d = 2, 2, 4, 6, 3
+    q, k, v, do = (rand((B, H, nq, d), 76), rand((B, H, nk, d), 77), rand((B, H, nk, d), 78),
+                   rand((B, H, nq, d), 79))
+    for lens in ([0, 6], [-3, 99]):
+        o, lse = run_fwd_kv(oracle_mod, form, q, k, v, 0.6, False, lens)
+        assert np.all(o[0] == 0.0) and np.all(lse[0] == -np.inf)
+        o_ref, l_ref = oracle_mod.fwd(q[1:], k[1:], v[1:], 0.6, False)
+        np.testing.assert_allclose(o[1], o_ref[0], rtol=1e-13, atol=1e-14)
+        np.testing.assert_allclose(lse[1], l_ref[0], rtol=1e-13)
+    dq, dk, dv = oracle_mod.bwd(q, k, v, do, 0.6, False, kv_len=[0, 6])
+    assert np.all(dq[0] == 0.0) and np.all(dk[0] == 0.0) and np.all(dv[0] == 0.0)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_key_padding_gradients_match_central_differences(oracle_mod, causal):
+    B, H, nq, nk, d = 2, 1, 5, 7, 3
+    q, k, v, do = (rand((B, H, nq, d), 80), rand((B, H, nk, d), 81), rand((B, H, nk, d), 82),
+                   rand((B, H, nq, d), 83))
+    scale, kv_len = 0.9, [4, 6]
+
+    def loss(q_, k_, v_):
+        o, _ = oracle_mod.fwd(q_, k_, v_, scale, causal, kv_len=kv_len)
+        return float((o * do).sum())
+
+    grads = oracle_mod.bwd(q, k, v, do, scale, causal, kv_len=kv_len)
+    h = 1e-6
+    for which, grad in enumerate(grads):
+        args = [q, k, v]
+        fd = np.zeros_like(args[which])
+        for idx in np.ndindex(fd.shape):
+            a_p, a_m = list(args), list(args)
+            a_p[which] = args[which].copy()
+            a_m[which] = args[which].copy()
+            a_p[which][idx] += h
+            a_m[which][idx] -= h
+            fd[idx] = (loss(*a_p) - loss(*a_m)) / (2 * h)
+        err = np.abs(fd - grad).max() / max(np.abs(grad).max(), 1e-300)
+        assert err < 1e-7, (which, err)
+
+
+def test_key_padding_subsets_match_full(oracle_mod):
+    nq, nk, d, n_valid = 21, 17, 4, 9
+    q, k, v, do = (rand((nq, d), 84), rand((nk, d), 85), rand((nk, d), 86), rand((nq, d), 87))
+    for causal in (False, True):
+        o, lse = oracle_mod.fwd(q[None, None], k[None, None], v[None, None], causal=causal,
+                                kv_len=[n_valid])
+        dq, dk, dv = oracle_mod.bwd(q[None, None], k[None, None], v[None, None], do[None, None],
+                                    causal=causal, kv_len=[n_valid])
+        rows, keys = np.array([20, 0, 8, 3]), np.array([16, 8, 9, 0])
+        orow, lrow = oracle_mod.fwd_rows(q, k, v, rows, causal=causal, n_valid=n_valid)
+        np.testing.assert_array_equal(orow, o[0, 0, rows])
+        np.testing.assert_array_equal(lrow, lse[0, 0, rows])
+        np.testing.assert_array_equal(
+            oracle_mod.bwd_dq_rows(q, k, v, do, rows, causal=causal, n_valid=n_valid),
+            dq[0, 0, rows])
+        dkr, dvr = oracle_mod.bwd_dkdv_keys(q, k, v, do, keys, causal=causal, n_valid=n_valid)
+        np.testing.assert_array_equal(dkr, dk[0, 0, keys])
+        np.testing.assert_array_equal(dvr, dv[0, 0, keys])
