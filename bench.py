@@ -97,6 +97,46 @@ def bench_decode(w, dev, calls: int = 50, warmup: int = 5):
             "traffic": load_traffic("attn_decode_kernel"), "includes": "combine of the key ranges"}
 
 
+def bench_key_padding(dev, calls: int = 5, warmup: int = 2):
+    """Forward + backward on a key-padded batch: 4 sequences of 8192 keys of
+    which 8192, 6144, 4096 and 2048 are valid (kv_len), 16 heads, d = 64,
+    bf16, against the same call without padding.  Credited work counts the
+    unmasked pairs only (14 d per pair), so equal TFLOP/s means the padded
+    keys cost nothing."""
+    import torch
+
+    from paper_2112_05682_amd import attention_bwd, attention_fwd
+    from paper_2112_05682_amd.inputs import attention_inputs
+
+    B, H, n, d = 4, 16, 8192, 64
+    lens = [8192, 6144, 4096, 2048]
+    x = {k_: t.to(dev) for k_, t in attention_inputs(B, H, n, n, d, "bf16").items()}
+    kl = torch.tensor(lens, dtype=torch.int32, device=dev)
+
+    def run(kv_len):
+        o, lse = attention_fwd(x["q"], x["k"], x["v"], kv_len=kv_len)
+        attention_bwd(x["q"], x["k"], x["v"], o, lse, x["do"], kv_len=kv_len)
+
+    out = {}
+    for name, kv_len, keys in (("padded", kl, sum(lens)), ("full", None, B * n)):
+        for _ in range(warmup):
+            run(kv_len)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(calls):
+            run(kv_len)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / calls
+        out[name] = {"ms": round(ms, 4), "tflops": round(14.0 * d * H * n * keys / (ms * 1e-3) / 1e12, 1)}
+    del x
+    return {"workload": "selfattn_bf16_b4h16_n8192_d64_kvlen", "kv_len": lens, "calls": calls,
+            "includes": "forward + backward (dK/dV and dQ in one call)",
+            "valid_key_fraction": sum(lens) / (B * n), **out,
+            "time_ratio": round(out["padded"]["ms"] / out["full"]["ms"], 4)}
+
+
 def cpu_baseline(w):
     """Time the float64 oracle (forward + backward) on whole (batch, head)
     slices of the workload (heads are independent, so a slice is exact)."""
@@ -137,6 +177,8 @@ def main() -> int:
                     help="also run a plain 256 MiB device copy (HBM counter calibration)")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the decode-shaped forward measurement")
+    ap.add_argument("--no-key-padding", action="store_true",
+                    help="skip the key-padding measurement")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -163,16 +205,22 @@ def main() -> int:
     f_fwd, f_dkdv, f_dq_credit = 4.0 * w.d * pairs, 8.0 * w.d * pairs, 2.0 * w.d * pairs
     f_step = 14.0 * w.d * pairs
 
-    def step():
+    def step(ev):
+        # ev: four events recorded before the forward, after it, after the
+        # dK/dV call and after the dQ call.
+        ev[0].record()
         o, lse = attention_fwd(q, k, v, causal=w.causal)
         ev[1].record()
         attention_bwd(q, k, v, o, lse, do, causal=w.causal, need_dq=False)
         ev[2].record()
         attention_bwd(q, k, v, o, lse, do, causal=w.causal, need_dkdv=False)
+        ev[3].record()
 
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    def events():
+        return [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+
     for _ in range(args.warmup):
-        step()
+        step(events())
     torch.cuda.synchronize()
 
     # Peak memory in excess of inputs and outputs (the paper's "memory
@@ -187,21 +235,22 @@ def main() -> int:
     out_bytes = sum(t.numel() * t.element_size() for t in (o_, *grads_))  # o, dq, dk, dv
     del o_, lse_, grads_
 
-    t_fwd = t_dkdv = t_dq = 0.0
+    # The timed steps are enqueued back to back (no synchronisation inside the
+    # timed region, so the GPU never waits for the host between kernels); the
+    # per-kernel event pairs of every step are read after the final
+    # synchronisation.
+    step_ev = [events() for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
-    for _ in range(args.steps):
-        ev[0].record()
-        step()
-        ev[3].record()
-        ev[3].synchronize()
-        t_fwd += ev[0].elapsed_time(ev[1])
-        t_dkdv += ev[1].elapsed_time(ev[2])
-        t_dq += ev[2].elapsed_time(ev[3])
+    for s_ in range(args.steps):
+        step(step_ev[s_])
     stop.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
+    t_fwd = sum(e[0].elapsed_time(e[1]) for e in step_ev)
+    t_dkdv = sum(e[1].elapsed_time(e[2]) for e in step_ev)
+    t_dq = sum(e[2].elapsed_time(e[3]) for e in step_ev)
     ms_step = total_ms / args.steps
     t_fwd, t_dkdv, t_dq = (t / args.steps for t in (t_fwd, t_dkdv, t_dq))
 
@@ -228,6 +277,7 @@ def main() -> int:
     n2_bytes = w.batch * w.heads * w.n_q * w.n_k * 4
 
     decode = None if args.no_decode else bench_decode(WORKLOADS[DECODE_WORKLOAD], dev)
+    key_padding = None if args.no_key_padding else bench_key_padding(dev)
 
     if args.copy_calibration:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -272,6 +322,8 @@ def main() -> int:
     }
     if decode is not None:
         out["decode"] = decode
+    if key_padding is not None:
+        out["key_padding"] = key_padding
     if not args.no_cpu_baseline:
         cb = cpu_baseline(w)
         out["cpu_baseline"] = {kk: (round(vv, 6) if isinstance(vv, float) else vv)

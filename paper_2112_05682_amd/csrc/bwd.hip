@@ -134,7 +134,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int kt_idx = w % p.n_ktiles;  // heaviest (earliest keys) first under causal
-  const int bh = w / p.n_ktiles;
+  const int bh = bh_of_group(w / p.n_ktiles, p.bh, p.heads);
   const int64_t k0 = (int64_t)kt_idx * Cfg::BKG;
   const int64_t kw = k0 + 32 * wave;
   const int64_t key = kw + c;
@@ -370,7 +370,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
 
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int kt_idx = w % p.n_ktiles;
-  const int bh = w / p.n_ktiles;
+  const int bh = bh_of_group(w / p.n_ktiles, p.bh, p.heads);
   const int64_t k0 = (int64_t)kt_idx * BKG;
   const int64_t kw = k0 + 32 * wave;
   const int64_t key = kw + c;
@@ -708,7 +708,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int qt_idx = w % p.n_qtiles;
-  const int bh = w / p.n_qtiles;
+  const int bh = bh_of_group(w / p.n_qtiles, p.bh, p.heads);
   const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;
   const int64_t q0 = (int64_t)qtile * BQ;
   const int64_t qw = q0 + 32 * QT * wave;  // first query of this wave
@@ -940,7 +940,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_pp_kernel(BwdParams p) {
 
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int qt_idx = w % p.n_qtiles;
-  const int bh = w / p.n_qtiles;
+  const int bh = bh_of_group(w / p.n_qtiles, p.bh, p.heads);
   const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;  // heaviest first
   const int64_t q0 = (int64_t)qtile * BQG;
   const int64_t qw = q0 + 32 * wave;  // first query of this wave

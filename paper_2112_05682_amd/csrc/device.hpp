@@ -287,4 +287,14 @@ __device__ __forceinline__ int xcd_remap(int w, int n) {
   return x * per + (x < rem ? x : rem) + i;
 }
 
+// (batch, head) index of the g-th (batch, head) pair in the order the grid
+// enumerates them: batch fastest, then head.  Consecutive logical tiles (and so
+// each XCD's contiguous range of them) then mix all batches, which keeps the
+// XCDs evenly loaded when batches have different valid key lengths, while the
+// tiles of one (batch, head) stay together.  Bijective on [0, bh).
+__device__ __forceinline__ int bh_of_group(int g, int bh, int heads) {
+  const int batch = bh / heads;
+  return (g % batch) * heads + g / batch;
+}
+
 }  // namespace mea

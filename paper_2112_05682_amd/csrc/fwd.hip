@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int qt_idx = w % p.n_qtiles;
   const int rest = w / p.n_qtiles;
-  const int bh = rest % p.bh;
+  const int bh = bh_of_group(rest % p.bh, p.bh, p.heads);
   const int split = rest / p.bh;
   const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;
   const int64_t q0 = (int64_t)qtile * Cfg::BQ;
@@ -374,7 +374,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   const int w = xcd_remap(blockIdx.x, gridDim.x);
   const int qt_idx = w % p.n_qtiles;
   const int rest = w / p.n_qtiles;
-  const int bh = rest % p.bh;
+  const int bh = bh_of_group(rest % p.bh, p.bh, p.heads);
   const int split = rest / p.bh;
   const int qtile = CAUSAL ? (p.n_qtiles - 1 - qt_idx) : qt_idx;
   const int64_t q0 = (int64_t)qtile * BQ;
