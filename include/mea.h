@@ -15,8 +15,9 @@
  * (the checkpointing of Section 5.2) from the saved per-row log-sum-exp.
  *
  * Conventions shared by every entry point:
- *   - Layout: q, o, do, dq are [B, H, n_q, d]; k, v, dk, dv are
- *     [B, H, n_k, d]; by default contiguous row-major with the feature index
+ *   - Layout: q, dq are [B, H, n_q, d]; k, dk are [B, H, n_k, d]; v, dv are
+ *     [B, H, n_k, d_v] and o, do [B, H, n_q, d_v] (d_v = d unless
+ *     mea_problem.d_v says otherwise); by default contiguous row-major with the feature index
  *     innermost, or with the batch, head and row strides given per tensor in
  *     mea_problem.strides (features always contiguous), which covers the
  *     paper's [n, heads, d] layout and views into a packed QKV projection;
@@ -41,7 +42,7 @@
  *     validation error nothing is enqueued and the status says why.  A
  *     launch failure reported by the HIP runtime returns MEA_ERR_HIP.  Errors
  *     during kernel execution surface at the caller's next synchronisation.
- *   - Supported: d in {64, 128}; dtype f32, f16 or bf16 (q, k, v and the
+ *   - Supported: d and d_v in {64, 128}; dtype f32, f16 or bf16 (q, k, v and the
  *     gradients share it; o and do share it too unless out_f32 asks for
  *     float32; lse, the workspace and all accumulation are float32).
  *     Sizes: batch, heads, n_q, n_k >= 1; every element count must fit in
@@ -103,6 +104,8 @@ typedef struct {
   const int32_t* kv_len;      /* DEVICE pointer to int32 [B] (4-byte aligned):
                                  valid keys per batch (key padding, see above),
                                  read by the kernels; NULL = all n_k keys */
+  int64_t d_v;                /* head dimension of v, o, do and dv: 0 (= d),
+                                 64 or 128; q, k, dq and dk have d features */
 } mea_problem;
 
 /* Bytes of device workspace mea_attention_fwd needs for `p` (written to

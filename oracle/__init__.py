@@ -11,7 +11,8 @@ definition, Section 3 running-max update, Section 4 chunk summaries and
 combine, hand-derived backward).  This module only converts arrays to
 contiguous float64 and calls the C entry points.
 
-Layout of every tensor argument: ``[B, H, n, d]`` (feature index innermost).
+Layout of every tensor argument: ``[B, H, n, features]`` (feature index
+innermost); q and k have d features, v, o and the upstream gradient d_v.
 """
 from __future__ import annotations
 
@@ -52,12 +53,12 @@ def _load():
         if not os.path.exists(_LIB):
             build(force=True)
         lib = ctypes.CDLL(_LIB)
-        full = [_i64, _i64, _i64, _i64, _i64, _dp, _dp, _dp, _dbl, _int, _lp]
+        full = [_i64, _i64, _i64, _i64, _i64, _i64, _dp, _dp, _dp, _dbl, _int, _lp]
         lib.mea_oracle_fwd.argtypes = full + [_dp, _dp]
         lib.mea_oracle_fwd_lazy.argtypes = full + [_dp, _dp]
         lib.mea_oracle_fwd_chunked.argtypes = full + [_i64, _i64, _dp, _dp]
-        lib.mea_oracle_bwd.argtypes = [_i64] * 5 + [_dp] * 4 + [_dbl, _int, _lp] + [_dp] * 3
-        head = [_i64, _i64, _i64, _dp, _dp, _dp]
+        lib.mea_oracle_bwd.argtypes = [_i64] * 6 + [_dp] * 4 + [_dbl, _int, _lp] + [_dp] * 3
+        head = [_i64, _i64, _i64, _i64, _dp, _dp, _dp]
         lib.mea_oracle_fwd_rows.argtypes = head + [_dbl, _int, _i64, _lp, _i64, _dp, _dp]
         lib.mea_oracle_bwd_dq_rows.argtypes = head + [_dp, _dbl, _int, _i64, _lp, _i64, _dp]
         lib.mea_oracle_bwd_dkdv_keys.argtypes = head + [_dp, _dbl, _int, _i64, _lp, _i64, _dp,
@@ -85,12 +86,13 @@ def _check(rc: int, name: str) -> None:
 
 
 def _dims(q, k, v):
+    """(B, H, n_q, n_k, d, d_v): q, k are [B, H, n, d], v is [B, H, n_k, d_v]."""
     if q.ndim != 4 or k.ndim != 4 or v.ndim != 4:
-        raise ValueError("q, k, v must be [B, H, n, d]")
+        raise ValueError("q, k, v must be [B, H, n, features]")
     B, H, nq, d = q.shape
-    if k.shape[:2] != (B, H) or v.shape != k.shape or k.shape[3] != d:
+    if k.shape[:2] != (B, H) or v.shape[:3] != k.shape[:3] or k.shape[3] != d:
         raise ValueError("shape mismatch: q %s k %s v %s" % (q.shape, k.shape, v.shape))
-    return B, H, nq, k.shape[2], d
+    return B, H, nq, k.shape[2], d, v.shape[3]
 
 
 def _kv_len(kv_len, batch: int):
@@ -120,12 +122,12 @@ def fwd(q, k, v, scale=None, causal=False, kv_len=None):
     """Direct form.  Returns (o [B,H,n_q,d], lse [B,H,n_q]) in float64.
     ``kv_len``: optional per-batch valid key lengths (key padding)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
-    B, H, nq, nk, d = _dims(q, k, v)
+    B, H, nq, nk, d, dv = _dims(q, k, v)
     scale = default_scale(d) if scale is None else float(scale)
     kl = _kv_len(kv_len, B)
-    o = np.empty((B, H, nq, d))
+    o = np.empty((B, H, nq, dv))
     lse = np.empty((B, H, nq))
-    _check(_load().mea_oracle_fwd(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), scale,
+    _check(_load().mea_oracle_fwd(B, H, nq, nk, d, dv, _ptr(q), _ptr(k), _ptr(v), scale,
                                   int(bool(causal)), _lptr(kl), _ptr(o), _ptr(lse)),
            "mea_oracle_fwd")
     return o, lse
@@ -134,12 +136,12 @@ def fwd(q, k, v, scale=None, causal=False, kv_len=None):
 def fwd_lazy(q, k, v, scale=None, causal=False, kv_len=None):
     """Section 3 single-pass form.  Returns (o, lse)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
-    B, H, nq, nk, d = _dims(q, k, v)
+    B, H, nq, nk, d, dv = _dims(q, k, v)
     scale = default_scale(d) if scale is None else float(scale)
     kl = _kv_len(kv_len, B)
-    o = np.empty((B, H, nq, d))
+    o = np.empty((B, H, nq, dv))
     lse = np.empty((B, H, nq))
-    _check(_load().mea_oracle_fwd_lazy(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), scale,
+    _check(_load().mea_oracle_fwd_lazy(B, H, nq, nk, d, dv, _ptr(q), _ptr(k), _ptr(v), scale,
                                        int(bool(causal)), _lptr(kl), _ptr(o), _ptr(lse)),
            "mea_oracle_fwd_lazy")
     return o, lse
@@ -149,12 +151,12 @@ def fwd_chunked(q, k, v, scale=None, causal=False, query_chunk=1024, key_chunk=4
                 kv_len=None):
     """Section 4 chunk-summary form.  Returns (o, lse)."""
     q, k, v = _f64(q), _f64(k), _f64(v)
-    B, H, nq, nk, d = _dims(q, k, v)
+    B, H, nq, nk, d, dv = _dims(q, k, v)
     scale = default_scale(d) if scale is None else float(scale)
     kl = _kv_len(kv_len, B)
-    o = np.empty((B, H, nq, d))
+    o = np.empty((B, H, nq, dv))
     lse = np.empty((B, H, nq))
-    _check(_load().mea_oracle_fwd_chunked(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), scale,
+    _check(_load().mea_oracle_fwd_chunked(B, H, nq, nk, d, dv, _ptr(q), _ptr(k), _ptr(v), scale,
                                           int(bool(causal)), _lptr(kl), int(query_chunk),
                                           int(key_chunk), _ptr(o), _ptr(lse)),
            "mea_oracle_fwd_chunked")
@@ -164,15 +166,15 @@ def fwd_chunked(q, k, v, scale=None, causal=False, query_chunk=1024, key_chunk=4
 def bwd(q, k, v, dout, scale=None, causal=False, kv_len=None):
     """Hand-derived gradients.  Returns (dq, dk, dv) in float64."""
     q, k, v, dout = _f64(q), _f64(k), _f64(v), _f64(dout)
-    B, H, nq, nk, d = _dims(q, k, v)
-    if dout.shape != q.shape:
-        raise ValueError("dout must have the shape of q")
+    B, H, nq, nk, d, d_v = _dims(q, k, v)
+    if dout.shape != (B, H, nq, d_v):
+        raise ValueError("dout must be [B, H, n_q, d_v]")
     scale = default_scale(d) if scale is None else float(scale)
     kl = _kv_len(kv_len, B)
     dq = np.empty_like(q)
     dk = np.empty_like(k)
     dv = np.empty_like(v)
-    _check(_load().mea_oracle_bwd(B, H, nq, nk, d, _ptr(q), _ptr(k), _ptr(v), _ptr(dout),
+    _check(_load().mea_oracle_bwd(B, H, nq, nk, d, d_v, _ptr(q), _ptr(k), _ptr(v), _ptr(dout),
                                   scale, int(bool(causal)), _lptr(kl), _ptr(dq), _ptr(dk),
                                   _ptr(dv)),
            "mea_oracle_bwd")
@@ -195,11 +197,11 @@ def fwd_rows(q, k, v, rows, scale=None, causal=False, n_valid=None):
     ``n_valid``: keys visible at most (key padding), default all."""
     q, k, v = _head(q), _head(k), _head(v)
     rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
-    d = q.shape[1]
+    d, dv = q.shape[1], v.shape[1]
     scale = default_scale(d) if scale is None else float(scale)
-    o = np.empty((rows.size, d))
+    o = np.empty((rows.size, dv))
     lse = np.empty(rows.size)
-    _check(_load().mea_oracle_fwd_rows(q.shape[0], k.shape[0], d, _ptr(q), _ptr(k), _ptr(v),
+    _check(_load().mea_oracle_fwd_rows(q.shape[0], k.shape[0], d, dv, _ptr(q), _ptr(k), _ptr(v),
                                        scale, int(bool(causal)), _n_valid(n_valid, k.shape[0]),
                                        rows.ctypes.data_as(_lp), rows.size, _ptr(o), _ptr(lse)),
            "mea_oracle_fwd_rows")
@@ -210,10 +212,10 @@ def bwd_dq_rows(q, k, v, dout, rows, scale=None, causal=False, n_valid=None):
     """dQ for selected query rows of one head."""
     q, k, v, dout = _head(q), _head(k), _head(v), _head(dout)
     rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
-    d = q.shape[1]
+    d, dv = q.shape[1], v.shape[1]
     scale = default_scale(d) if scale is None else float(scale)
     dq = np.empty((rows.size, d))
-    _check(_load().mea_oracle_bwd_dq_rows(q.shape[0], k.shape[0], d, _ptr(q), _ptr(k), _ptr(v),
+    _check(_load().mea_oracle_bwd_dq_rows(q.shape[0], k.shape[0], d, dv, _ptr(q), _ptr(k), _ptr(v),
                                           _ptr(dout), scale, int(bool(causal)),
                                           _n_valid(n_valid, k.shape[0]),
                                           rows.ctypes.data_as(_lp), rows.size, _ptr(dq)),
@@ -225,11 +227,11 @@ def bwd_dkdv_keys(q, k, v, dout, keys, scale=None, causal=False, n_valid=None):
     """dK and dV for selected key rows of one head."""
     q, k, v, dout = _head(q), _head(k), _head(v), _head(dout)
     keys = np.ascontiguousarray(np.asarray(keys, dtype=np.int64))
-    d = q.shape[1]
+    d, d_v = q.shape[1], v.shape[1]
     scale = default_scale(d) if scale is None else float(scale)
     dk = np.empty((keys.size, d))
-    dv = np.empty((keys.size, d))
-    _check(_load().mea_oracle_bwd_dkdv_keys(q.shape[0], k.shape[0], d, _ptr(q), _ptr(k),
+    dv = np.empty((keys.size, d_v))
+    _check(_load().mea_oracle_bwd_dkdv_keys(q.shape[0], k.shape[0], d, d_v, _ptr(q), _ptr(k),
                                             _ptr(v), _ptr(dout), scale, int(bool(causal)),
                                             _n_valid(n_valid, k.shape[0]),
                                             keys.ctypes.data_as(_lp), keys.size, _ptr(dk),

@@ -47,7 +47,9 @@
  *     row that sees no key has o = 0, lse = -inf and zero gradients, and a
  *     key no row sees has zero dK and dV (the sums over an empty set);
  *   - lse is the natural-log log-sum-exp of the scaled scores of a row;
- *   - layout: contiguous [B, H, n, d], feature index innermost.
+ *   - layout: contiguous [B, H, n, width], feature index innermost; q and k
+ *     have d features, v, o and the upstream gradient d_v (the definition
+ *     does not tie the value width to the key width).
  *
  * All sums run in ascending index order in plain double precision.  Rows
  * are distributed over OpenMP threads; each row is computed by one thread.
@@ -89,8 +91,8 @@ static double dot(const double* a, const double* b, int64_t d) {
   return acc;
 }
 
-static int dims_ok(int64_t n_q, int64_t n_k, int64_t d) {
-  return n_q >= 1 && n_k >= 1 && d >= 1;
+static int dims_ok(int64_t n_q, int64_t n_k, int64_t d, int64_t d_v) {
+  return n_q >= 1 && n_k >= 1 && d >= 1 && d_v >= 1;
 }
 
 int mea_oracle_num_threads(void) {
@@ -107,8 +109,8 @@ int mea_oracle_num_threads(void) {
 
 /* One query row.  s is scratch of length >= n_vis. */
 static void direct_row(const double* qi, const double* k, const double* v,
-                       int64_t n_vis, int64_t d, double scale, double* s,
-                       double* out, double* lse) {
+                       int64_t n_vis, int64_t d, int64_t d_v, double scale,
+                       double* s, double* out, double* lse) {
   double m = -INFINITY;
   for (int64_t j = 0; j < n_vis; ++j) {
     s[j] = scale * dot(qi, k + j * d, d);
@@ -116,11 +118,11 @@ static void direct_row(const double* qi, const double* k, const double* v,
   }
   double l = 0.0;
   for (int64_t j = 0; j < n_vis; ++j) l += exp(s[j] - m);
-  for (int64_t t = 0; t < d; ++t) out[t] = 0.0;
+  for (int64_t t = 0; t < d_v; ++t) out[t] = 0.0;
   for (int64_t j = 0; j < n_vis; ++j) {
     const double w = exp(s[j] - m) / l; /* normalised weight, as defined */
-    const double* vj = v + j * d;
-    for (int64_t t = 0; t < d; ++t) out[t] += w * vj[t];
+    const double* vj = v + j * d_v;
+    for (int64_t t = 0; t < d_v; ++t) out[t] += w * vj[t];
   }
   *lse = m + log(l);
 }
@@ -143,16 +145,17 @@ static int thread_id(void) {
 
 /* One (batch, head) slice, a subset of query rows.  o_rows is [n_rows, d],
  * lse_rows is [n_rows] (either may be NULL). */
-int mea_oracle_fwd_rows(int64_t n_q, int64_t n_k, int64_t d, const double* q,
-                        const double* k, const double* v, double scale,
-                        int causal, int64_t n_valid, const int64_t* rows,
-                        int64_t n_rows, double* o_rows, double* lse_rows) {
-  if (!dims_ok(n_q, n_k, d) || n_rows < 0 || !q || !k || !v || !rows ||
+int mea_oracle_fwd_rows(int64_t n_q, int64_t n_k, int64_t d, int64_t d_v,
+                        const double* q, const double* k, const double* v,
+                        double scale, int causal, int64_t n_valid,
+                        const int64_t* rows, int64_t n_rows, double* o_rows,
+                        double* lse_rows) {
+  if (!dims_ok(n_q, n_k, d, d_v) || n_rows < 0 || !q || !k || !v || !rows ||
       n_valid < 0 || n_valid > n_k)
     return ORACLE_EINVAL;
   for (int64_t r = 0; r < n_rows; ++r)
     if (rows[r] < 0 || rows[r] >= n_q) return ORACLE_EINVAL;
-  const int64_t per_thread = n_k + d;
+  const int64_t per_thread = n_k + d_v;
   double* scratch = thread_scratch(per_thread);
   if (!scratch) return ORACLE_ENOMEM;
 #pragma omp parallel for schedule(dynamic, 8)
@@ -161,9 +164,9 @@ int mea_oracle_fwd_rows(int64_t n_q, int64_t n_k, int64_t d, const double* q,
     double* out = s + n_k;
     const int64_t i = rows[r];
     double lse;
-    direct_row(q + i * d, k, v, visible_keys(i, n_k, causal, n_valid), d, scale,
-               s, out, &lse);
-    if (o_rows) memcpy(o_rows + r * d, out, sizeof(double) * (size_t)d);
+    direct_row(q + i * d, k, v, visible_keys(i, n_k, causal, n_valid), d, d_v,
+               scale, s, out, &lse);
+    if (o_rows) memcpy(o_rows + r * d_v, out, sizeof(double) * (size_t)d_v);
     if (lse_rows) lse_rows[r] = lse;
   }
   free(scratch);
@@ -172,20 +175,20 @@ int mea_oracle_fwd_rows(int64_t n_q, int64_t n_k, int64_t d, const double* q,
 
 /* Full [B, H, n_q, d] forward, direct form. */
 int mea_oracle_fwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
-                   int64_t d, const double* q, const double* k, const double* v,
-                   double scale, int causal, const int64_t* kv_len, double* o,
-                   double* lse) {
-  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || !o || !lse)
+                   int64_t d, int64_t d_v, const double* q, const double* k,
+                   const double* v, double scale, int causal,
+                   const int64_t* kv_len, double* o, double* lse) {
+  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d, d_v) || !o || !lse)
     return ORACLE_EINVAL;
   int64_t* rows = (int64_t*)malloc(sizeof(int64_t) * (size_t)n_q);
   if (!rows) return ORACLE_ENOMEM;
   for (int64_t i = 0; i < n_q; ++i) rows[i] = i;
   int err = ORACLE_OK;
   for (int64_t bh = 0; bh < batch * heads && err == ORACLE_OK; ++bh) {
-    err = mea_oracle_fwd_rows(n_q, n_k, d, q + bh * n_q * d, k + bh * n_k * d,
-                              v + bh * n_k * d, scale, causal,
-                              slice_valid(kv_len, bh, heads, n_k), rows, n_q,
-                              o + bh * n_q * d, lse + bh * n_q);
+    err = mea_oracle_fwd_rows(n_q, n_k, d, d_v, q + bh * n_q * d,
+                              k + bh * n_k * d, v + bh * n_k * d_v, scale,
+                              causal, slice_valid(kv_len, bh, heads, n_k), rows,
+                              n_q, o + bh * n_q * d_v, lse + bh * n_q);
   }
   free(rows);
   return err;
@@ -197,51 +200,51 @@ int mea_oracle_fwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
 /* ------------------------------------------------------------------------ */
 
 static void lazy_row(const double* qi, const double* k, const double* v,
-                     int64_t n_vis, int64_t d, double scale, double* vstar,
-                     double* out, double* lse) {
+                     int64_t n_vis, int64_t d, int64_t d_v, double scale,
+                     double* vstar, double* out, double* lse) {
   double sstar = 0.0;
   double mstar = -INFINITY;
-  for (int64_t t = 0; t < d; ++t) vstar[t] = 0.0;
+  for (int64_t t = 0; t < d_v; ++t) vstar[t] = 0.0;
   for (int64_t j = 0; j < n_vis; ++j) {
     const double sj = scale * dot(qi, k + j * d, d);
     const double mi = (sj > mstar) ? sj : mstar;
     const double old_factor = exp(mstar - mi); /* e^{-inf} = 0 on key 0 */
     const double new_factor = exp(sj - mi);
-    const double* vj = v + j * d;
-    for (int64_t t = 0; t < d; ++t)
+    const double* vj = v + j * d_v;
+    for (int64_t t = 0; t < d_v; ++t)
       vstar[t] = vstar[t] * old_factor + vj[t] * new_factor;
     sstar = sstar * old_factor + new_factor;
     mstar = mi;
   }
   if (n_vis == 0) { /* no visible key: the empty sums give o = 0 */
-    for (int64_t t = 0; t < d; ++t) out[t] = 0.0;
+    for (int64_t t = 0; t < d_v; ++t) out[t] = 0.0;
     *lse = -INFINITY;
     return;
   }
-  for (int64_t t = 0; t < d; ++t) out[t] = vstar[t] / sstar;
+  for (int64_t t = 0; t < d_v; ++t) out[t] = vstar[t] / sstar;
   *lse = mstar + log(sstar);
 }
 
 int mea_oracle_fwd_lazy(int64_t batch, int64_t heads, int64_t n_q,
-                        int64_t n_k, int64_t d, const double* q,
+                        int64_t n_k, int64_t d, int64_t d_v, const double* q,
                         const double* k, const double* v, double scale,
                         int causal, const int64_t* kv_len, double* o,
                         double* lse) {
-  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || !q || !k || !v ||
-      !o || !lse)
+  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d, d_v) || !q || !k ||
+      !v || !o || !lse)
     return ORACLE_EINVAL;
-  double* scratch = thread_scratch(d);
+  double* scratch = thread_scratch(d_v);
   if (!scratch) return ORACLE_ENOMEM;
   for (int64_t bh = 0; bh < batch * heads; ++bh) {
     const double* qh = q + bh * n_q * d;
     const double* kh = k + bh * n_k * d;
-    const double* vh = v + bh * n_k * d;
+    const double* vh = v + bh * n_k * d_v;
     const int64_t n_valid = slice_valid(kv_len, bh, heads, n_k);
 #pragma omp parallel for schedule(dynamic, 8)
     for (int64_t i = 0; i < n_q; ++i)
-      lazy_row(qh + i * d, kh, vh, visible_keys(i, n_k, causal, n_valid), d, scale,
-               scratch + thread_id() * d, o + (bh * n_q + i) * d,
-               lse + bh * n_q + i);
+      lazy_row(qh + i * d, kh, vh, visible_keys(i, n_k, causal, n_valid), d,
+               d_v, scale, scratch + thread_id() * d_v,
+               o + (bh * n_q + i) * d_v, lse + bh * n_q + i);
   }
   free(scratch);
   return ORACLE_OK;
@@ -258,7 +261,7 @@ int mea_oracle_fwd_lazy(int64_t batch, int64_t heads, int64_t n_q,
  *   weights[c]   = sum_{j in c} e^{s_j - m_c}
  *   maxes[c]     = max_{j in c} s_j                                         */
 static void chunk_summaries(const double* qi, const double* k, const double* v,
-                            int64_t n_vis, int64_t d, double scale,
+                            int64_t n_vis, int64_t d, int64_t d_v, double scale,
                             int64_t key_chunk, double* values, double* weights,
                             double* maxes, double* s) {
   int64_t c = 0;
@@ -269,13 +272,13 @@ static void chunk_summaries(const double* qi, const double* k, const double* v,
       s[j - j0] = scale * dot(qi, k + j * d, d);
       if (s[j - j0] > m) m = s[j - j0];
     }
-    double* vc = values + c * d;
-    for (int64_t t = 0; t < d; ++t) vc[t] = 0.0;
+    double* vc = values + c * d_v;
+    for (int64_t t = 0; t < d_v; ++t) vc[t] = 0.0;
     double wsum = 0.0;
     for (int64_t j = j0; j < j1; ++j) {
       const double e = exp(s[j - j0] - m);
-      const double* vj = v + j * d;
-      for (int64_t t = 0; t < d; ++t) vc[t] += e * vj[t];
+      const double* vj = v + j * d_v;
+      for (int64_t t = 0; t < d_v; ++t) vc[t] += e * vj[t];
       wsum += e;
     }
     weights[c] = wsum;
@@ -312,24 +315,24 @@ static void combine_summaries(int64_t n_chunks, int64_t d, double* values,
 }
 
 int mea_oracle_fwd_chunked(int64_t batch, int64_t heads, int64_t n_q,
-                           int64_t n_k, int64_t d, const double* q,
+                           int64_t n_k, int64_t d, int64_t d_v, const double* q,
                            const double* k, const double* v, double scale,
                            int causal, const int64_t* kv_len,
                            int64_t query_chunk, int64_t key_chunk, double* o,
                            double* lse) {
-  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || query_chunk < 1 ||
+  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d, d_v) || query_chunk < 1 ||
       key_chunk < 1 || !q || !k || !v || !o || !lse)
     return ORACLE_EINVAL;
   const int64_t max_chunks = (n_k + key_chunk - 1) / key_chunk;
   const int64_t chunk_len = key_chunk < n_k ? key_chunk : n_k;
-  /* values [max_chunks, d] | weights [max_chunks] | maxes [max_chunks] | s */
-  const int64_t per_thread = max_chunks * (d + 2) + chunk_len;
+  /* values [max_chunks, d_v] | weights [max_chunks] | maxes [max_chunks] | s */
+  const int64_t per_thread = max_chunks * (d_v + 2) + chunk_len;
   double* scratch = thread_scratch(per_thread);
   if (!scratch) return ORACLE_ENOMEM;
   for (int64_t bh = 0; bh < batch * heads; ++bh) {
     const double* qh = q + bh * n_q * d;
     const double* kh = k + bh * n_k * d;
-    const double* vh = v + bh * n_k * d;
+    const double* vh = v + bh * n_k * d_v;
     const int64_t n_valid = slice_valid(kv_len, bh, heads, n_k);
     /* Outer loop over query chunks; each chunk's rows go straight to o. */
     for (int64_t i0 = 0; i0 < n_q; i0 += query_chunk) {
@@ -337,15 +340,15 @@ int mea_oracle_fwd_chunked(int64_t batch, int64_t heads, int64_t n_q,
 #pragma omp parallel for schedule(dynamic, 4)
       for (int64_t i = i0; i < i1; ++i) {
         double* values = scratch + thread_id() * per_thread;
-        double* weights = values + max_chunks * d;
+        double* weights = values + max_chunks * d_v;
         double* maxes = weights + max_chunks;
         double* s = maxes + max_chunks;
         const int64_t n_vis = visible_keys(i, n_k, causal, n_valid);
         const int64_t n_chunks = (n_vis + key_chunk - 1) / key_chunk;
-        chunk_summaries(qh + i * d, kh, vh, n_vis, d, scale, key_chunk, values,
-                        weights, maxes, s);
-        combine_summaries(n_chunks, d, values, weights, maxes,
-                          o + (bh * n_q + i) * d, lse + bh * n_q + i);
+        chunk_summaries(qh + i * d, kh, vh, n_vis, d, d_v, scale, key_chunk,
+                        values, weights, maxes, s);
+        combine_summaries(n_chunks, d_v, values, weights, maxes,
+                          o + (bh * n_q + i) * d_v, lse + bh * n_q + i);
       }
     }
   }
@@ -360,8 +363,9 @@ int mea_oracle_fwd_chunked(int64_t batch, int64_t heads, int64_t n_q,
 /* Softmax statistics of one row: max m and denominator l = sum e^{s_j - m},
  * plus D = sum_j w_j dot(dO_i, v_j). */
 static void row_stats(const double* qi, const double* doi, const double* k,
-                      const double* v, int64_t n_vis, int64_t d, double scale,
-                      double* s, double* m_out, double* l_out, double* D_out) {
+                      const double* v, int64_t n_vis, int64_t d, int64_t d_v,
+                      double scale, double* s, double* m_out, double* l_out,
+                      double* D_out) {
   double m = -INFINITY;
   for (int64_t j = 0; j < n_vis; ++j) {
     s[j] = scale * dot(qi, k + j * d, d);
@@ -372,7 +376,7 @@ static void row_stats(const double* qi, const double* doi, const double* k,
   double D = 0.0;
   for (int64_t j = 0; j < n_vis; ++j) {
     const double w = exp(s[j] - m) / l;
-    D += w * dot(doi, v + j * d, d);
+    D += w * dot(doi, v + j * d_v, d_v);
   }
   *m_out = m;
   *l_out = l;
@@ -381,12 +385,12 @@ static void row_stats(const double* qi, const double* doi, const double* k,
 
 /* dQ for a subset of query rows of one (batch, head) slice.  dq_rows is
  * [n_rows, d]. */
-int mea_oracle_bwd_dq_rows(int64_t n_q, int64_t n_k, int64_t d,
+int mea_oracle_bwd_dq_rows(int64_t n_q, int64_t n_k, int64_t d, int64_t d_v,
                            const double* q, const double* k, const double* v,
                            const double* dout, double scale, int causal,
                            int64_t n_valid, const int64_t* rows,
                            int64_t n_rows, double* dq_rows) {
-  if (!dims_ok(n_q, n_k, d) || n_rows < 0 || !q || !k || !v || !dout ||
+  if (!dims_ok(n_q, n_k, d, d_v) || n_rows < 0 || !q || !k || !v || !dout ||
       !rows || !dq_rows || n_valid < 0 || n_valid > n_k)
     return ORACLE_EINVAL;
   for (int64_t r = 0; r < n_rows; ++r)
@@ -398,15 +402,15 @@ int mea_oracle_bwd_dq_rows(int64_t n_q, int64_t n_k, int64_t d,
     double* s = scratch + thread_id() * n_k;
     const int64_t i = rows[r];
     const double* qi = q + i * d;
-    const double* doi = dout + i * d;
+    const double* doi = dout + i * d_v;
     const int64_t n_vis = visible_keys(i, n_k, causal, n_valid);
     double m, l, D;
-    row_stats(qi, doi, k, v, n_vis, d, scale, s, &m, &l, &D);
+    row_stats(qi, doi, k, v, n_vis, d, d_v, scale, s, &m, &l, &D);
     double* dqi = dq_rows + r * d;
     for (int64_t t = 0; t < d; ++t) dqi[t] = 0.0;
     for (int64_t j = 0; j < n_vis; ++j) {
       const double w = exp(s[j] - m) / l;
-      const double ds = w * (dot(doi, v + j * d, d) - D);
+      const double ds = w * (dot(doi, v + j * d_v, d_v) - D);
       const double* kj = k + j * d;
       for (int64_t t = 0; t < d; ++t) dqi[t] += ds * kj[t];
     }
@@ -419,12 +423,12 @@ int mea_oracle_bwd_dq_rows(int64_t n_q, int64_t n_k, int64_t d,
 /* dK and dV for a subset of key rows of one (batch, head) slice.  Needs the
  * softmax statistics of every query row first.  dk_rows, dv_rows are
  * [n_keys, d] (either may be NULL). */
-int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
+int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d, int64_t d_v,
                              const double* q, const double* k, const double* v,
                              const double* dout, double scale, int causal,
                              int64_t n_valid, const int64_t* keys,
                              int64_t n_keys, double* dk_rows, double* dv_rows) {
-  if (!dims_ok(n_q, n_k, d) || n_keys < 0 || !q || !k || !v || !dout ||
+  if (!dims_ok(n_q, n_k, d, d_v) || n_keys < 0 || !q || !k || !v || !dout ||
       !keys || n_valid < 0 || n_valid > n_k)
     return ORACLE_EINVAL;
   for (int64_t r = 0; r < n_keys; ++r)
@@ -448,8 +452,8 @@ int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
   /* Pass 1: per-query softmax statistics. */
 #pragma omp parallel for schedule(dynamic, 8)
   for (int64_t i = 0; i < n_q; ++i)
-    row_stats(q + i * d, dout + i * d, k, v,
-              visible_keys(i, n_k, causal, n_valid), d, scale,
+    row_stats(q + i * d, dout + i * d_v, k, v,
+              visible_keys(i, n_k, causal, n_valid), d, d_v, scale,
               scratch + thread_id() * n_k, &m[i], &l[i], &D[i]);
   free(scratch);
   /* Pass 2: per requested key, sum over the queries that see it. */
@@ -457,20 +461,20 @@ int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
   for (int64_t r = 0; r < n_keys; ++r) {
     const int64_t j = keys[r];
     const double* kj = k + j * d;
-    const double* vj = v + j * d;
+    const double* vj = v + j * d_v;
     double* dkj = dk_rows ? dk_rows + r * d : NULL;
-    double* dvj = dv_rows ? dv_rows + r * d : NULL;
+    double* dvj = dv_rows ? dv_rows + r * d_v : NULL;
     if (dkj) for (int64_t t = 0; t < d; ++t) dkj[t] = 0.0;
-    if (dvj) for (int64_t t = 0; t < d; ++t) dvj[t] = 0.0;
+    if (dvj) for (int64_t t = 0; t < d_v; ++t) dvj[t] = 0.0;
     /* query i sees key j iff j < n_valid and, causal, j <= i */
     const int64_t i_first = j >= n_valid ? n_q : (causal ? j : 0);
     for (int64_t i = i_first; i < n_q; ++i) {
       const double* qi = q + i * d;
-      const double* doi = dout + i * d;
+      const double* doi = dout + i * d_v;
       const double w = exp(scale * dot(qi, kj, d) - m[i]) / l[i];
-      if (dvj) for (int64_t t = 0; t < d; ++t) dvj[t] += w * doi[t];
+      if (dvj) for (int64_t t = 0; t < d_v; ++t) dvj[t] += w * doi[t];
       if (dkj) {
-        const double ds = w * (dot(doi, vj, d) - D[i]);
+        const double ds = w * (dot(doi, vj, d_v) - D[i]);
         for (int64_t t = 0; t < d; ++t) dkj[t] += ds * qi[t];
       }
     }
@@ -484,10 +488,11 @@ int mea_oracle_bwd_dkdv_keys(int64_t n_q, int64_t n_k, int64_t d,
 
 /* Full [B, H, n, d] backward. */
 int mea_oracle_bwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
-                   int64_t d, const double* q, const double* k, const double* v,
-                   const double* dout, double scale, int causal,
-                   const int64_t* kv_len, double* dq, double* dk, double* dv) {
-  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d) || !dq || !dk || !dv)
+                   int64_t d, int64_t d_v, const double* q, const double* k,
+                   const double* v, const double* dout, double scale,
+                   int causal, const int64_t* kv_len, double* dq, double* dk,
+                   double* dv) {
+  if (batch < 1 || heads < 1 || !dims_ok(n_q, n_k, d, d_v) || !dq || !dk || !dv)
     return ORACLE_EINVAL;
   const int64_t n_max = n_q > n_k ? n_q : n_k;
   int64_t* idx = (int64_t*)malloc(sizeof(int64_t) * (size_t)n_max);
@@ -497,15 +502,15 @@ int mea_oracle_bwd(int64_t batch, int64_t heads, int64_t n_q, int64_t n_k,
   for (int64_t bh = 0; bh < batch * heads && err == ORACLE_OK; ++bh) {
     const double* qh = q + bh * n_q * d;
     const double* kh = k + bh * n_k * d;
-    const double* vh = v + bh * n_k * d;
-    const double* doh = dout + bh * n_q * d;
+    const double* vh = v + bh * n_k * d_v;
+    const double* doh = dout + bh * n_q * d_v;
     const int64_t n_valid = slice_valid(kv_len, bh, heads, n_k);
-    err = mea_oracle_bwd_dq_rows(n_q, n_k, d, qh, kh, vh, doh, scale, causal,
-                                 n_valid, idx, n_q, dq + bh * n_q * d);
+    err = mea_oracle_bwd_dq_rows(n_q, n_k, d, d_v, qh, kh, vh, doh, scale,
+                                 causal, n_valid, idx, n_q, dq + bh * n_q * d);
     if (err == ORACLE_OK)
-      err = mea_oracle_bwd_dkdv_keys(n_q, n_k, d, qh, kh, vh, doh, scale,
+      err = mea_oracle_bwd_dkdv_keys(n_q, n_k, d, d_v, qh, kh, vh, doh, scale,
                                      causal, n_valid, idx, n_k,
-                                     dk + bh * n_k * d, dv + bh * n_k * d);
+                                     dk + bh * n_k * d, dv + bh * n_k * d_v);
   }
   free(idx);
   return err;

@@ -56,6 +56,7 @@ class MeaProblem(ctypes.Structure):
         ("out_f32", ctypes.c_int32),
         ("strides", ctypes.POINTER(MeaStrides)),
         ("kv_len", ctypes.c_void_p),
+        ("d_v", ctypes.c_int64),
     ]
 
 
@@ -103,19 +104,22 @@ def check(name: str, status: int) -> None:
 
 
 def problem(batch, heads, n_q, n_k, d, dtype, causal, scale, out_f32=False,
-            strides: dict | None = None, kv_len: int | None = None) -> MeaProblem:
+            strides: dict | None = None, kv_len: int | None = None,
+            d_v: int | None = None) -> MeaProblem:
     """``strides`` maps tensor names (q, k, v, o, d_o, dq, dk, dv) to
     (batch, head, row) element strides; missing names and None mean contiguous
-    [B, H, n, d].  ``kv_len`` is the device address of an int32 [B] array of
-    valid key lengths (key padding), or None."""
+    [B, H, n, width].  ``kv_len`` is the device address of an int32 [B] array of
+    valid key lengths (key padding), or None.  ``d_v``: head dimension of v, o,
+    do and dv (None: d)."""
+    dv = int(d) if d_v is None else int(d_v)
     p = MeaProblem(int(batch), int(heads), int(n_q), int(n_k), int(d), int(dtype),
                    int(bool(causal)), float(scale), int(bool(out_f32)), None,
-                   int(kv_len) if kv_len else None)
+                   int(kv_len) if kv_len else None, 0 if dv == int(d) else dv)
     if strides:
         st = MeaStrides()
-        for name, n in (("q", n_q), ("k", n_k), ("v", n_k), ("o", n_q), ("d_o", n_q),
-                        ("dq", n_q), ("dk", n_k), ("dv", n_k)):
-            bs, hs, rs = strides.get(name) or (int(heads) * int(n) * int(d), int(n) * int(d), int(d))
+        for name, n, w in (("q", n_q, d), ("k", n_k, d), ("v", n_k, dv), ("o", n_q, dv),
+                           ("d_o", n_q, dv), ("dq", n_q, d), ("dk", n_k, d), ("dv", n_k, dv)):
+            bs, hs, rs = strides.get(name) or (int(heads) * int(n) * int(w), int(n) * int(w), int(w))
             setattr(st, name, MeaTensorStrides(int(bs), int(hs), int(rs)))
         p._strides_keepalive = st  # the struct must outlive the calls that read it
         p.strides = ctypes.pointer(st)

@@ -31,6 +31,7 @@ def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: boo
         raise ValueError("q and k must be [B, H, n, d]")
     B, H, n_q, d = q.shape
     n_k = k.shape[2]
+    d_v = tensors["v"].shape[3] if tensors and tensors.get("v") is not None else d
     if q.dtype not in _DTYPE_CODE:
         raise TypeError("unsupported dtype %s" % q.dtype)
     if scale is None:
@@ -44,7 +45,7 @@ def _problem(q: torch.Tensor, k: torch.Tensor, causal: bool, scale, out_f32: boo
             raise ValueError("kv_len must be a contiguous int32 [B] tensor on q's device")
     return _lib.problem(B, H, n_q, n_k, d, _DTYPE_CODE[q.dtype], causal, scale,
                         out_f32 and q.dtype != torch.float32, strides,
-                        kv_len.data_ptr() if kv_len is not None else None)
+                        kv_len.data_ptr() if kv_len is not None else None, d_v)
 
 
 def _check_tensors(names, tensors, dtype, device):
@@ -85,17 +86,18 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: boo
     ``out_dtype`` is q's dtype (default) or torch.float32.  ``kv_len`` (int32
     ``[B]`` on the GPU) masks keys ``j >= kv_len[b]`` of batch b (key padding);
     a row with no visible key gets o = 0 and lse = -inf."""
-    if k.shape != v.shape or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
+    if k.shape[:3] != v.shape[:3] or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
         raise ValueError("shape mismatch: q %s k %s v %s" % (tuple(q.shape), tuple(k.shape),
                                                               tuple(v.shape)))
+    o_shape = tuple(q.shape[:3]) + (v.shape[3],)  # o has v's head dimension
     _check_tensors(("q", "k", "v"), (q, k, v), q.dtype, q.device)
     out_dtype = q.dtype if out_dtype is None else out_dtype
     if out_dtype not in (q.dtype, torch.float32):
         raise TypeError("out_dtype must be q's dtype or float32")
-    o = torch.empty(q.shape, dtype=out_dtype, device=q.device) if out is None else out
+    o = torch.empty(o_shape, dtype=out_dtype, device=q.device) if out is None else out
     _check_tensors(("out",), (o,), out_dtype, q.device)
-    if o.shape != q.shape:
-        raise ValueError("out must have q's shape")
+    if tuple(o.shape) != o_shape:
+        raise ValueError("out must be [B, H, n_q, d_v]")
     p = _problem(q, k, causal, scale, out_dtype == torch.float32,
                  {"q": q, "k": k, "v": v, "o": o}, kv_len)
     lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if need_lse else None
@@ -120,8 +122,9 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
         raise TypeError("o must have q's dtype or float32")
     _check_tensors(("o", "do"), (o, do), o.dtype, q.device)
     _check_tensors(("lse",), (lse,), torch.float32, q.device)
-    if o.shape != q.shape or do.shape != q.shape or tuple(lse.shape) != tuple(q.shape[:3]):
-        raise ValueError("o, do must match q and lse must be [B, H, n_q]")
+    o_shape = tuple(q.shape[:3]) + (v.shape[3],)
+    if tuple(o.shape) != o_shape or tuple(do.shape) != o_shape or tuple(lse.shape) != tuple(q.shape[:3]):
+        raise ValueError("o, do must be [B, H, n_q, d_v] and lse [B, H, n_q]")
     if not (need_dq or need_dkdv):
         raise ValueError("nothing to compute")
     given = out if out is not None else (None, None, None)
@@ -134,7 +137,7 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
     outs = [(n_, t) for n_, t in (("dq", dq), ("dk", dk), ("dv", dv)) if t is not None]
     _check_tensors([n_ for n_, _ in outs], [t for _, t in outs], q.dtype, q.device)
     for n_, t in outs:
-        if t.shape != (q.shape if n_ == "dq" else k.shape):
+        if t.shape != {"dq": q.shape, "dk": k.shape, "dv": v.shape}[n_]:
             raise ValueError("%s has the wrong shape" % n_)
     p = _problem(q, k, causal, scale, o.dtype == torch.float32,
                  {"q": q, "k": k, "v": v, "o": o, "d_o": do, "dq": dq, "dk": dk, "dv": dv}, kv_len)

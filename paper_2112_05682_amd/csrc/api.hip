@@ -22,6 +22,9 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
   return true;
 }
 
+// Head dimension of v and o (d_v = 0 means d).
+int64_t dv_of(const mea_problem* p) { return p->d_v ? p->d_v : p->d; }
+
 // Shape, dtype and scale checks shared by every entry point.
 mea_status check_problem(const mea_problem* p) {
   if (!p) return MEA_ERR_INVALID_ARG;
@@ -32,32 +35,36 @@ mea_status check_problem(const mea_problem* p) {
   if (p->out_f32 != 0 && p->out_f32 != 1) return MEA_ERR_INVALID_ARG;
   if (!(p->scale > 0.0f) || !isfinite(p->scale)) return MEA_ERR_INVALID_ARG;
   if (p->kv_len && ((uintptr_t)p->kv_len & 3u)) return MEA_ERR_INVALID_ARG;
+  if (p->d_v < 0) return MEA_ERR_INVALID_ARG;
+  const int64_t dmax = p->d > dv_of(p) ? p->d : dv_of(p);
   int64_t bh, nq_d, nk_d, tot;
   if (!mul_ok(p->batch, p->heads, &bh) || bh >= kMaxSeq) return MEA_ERR_INVALID_ARG;
-  if (!mul_ok(p->n_q, p->d, &nq_d) || !mul_ok(p->n_k, p->d, &nk_d)) return MEA_ERR_INVALID_ARG;
+  if (!mul_ok(p->n_q, dmax, &nq_d) || !mul_ok(p->n_k, dmax, &nk_d)) return MEA_ERR_INVALID_ARG;
   if (!mul_ok(bh, nq_d, &tot) || !mul_ok(bh, nk_d, &tot)) return MEA_ERR_INVALID_ARG;
   if (!mul_ok(bh, p->n_q * 4, &tot)) return MEA_ERR_INVALID_ARG;
   if (p->d != 64 && p->d != 128) return MEA_ERR_UNSUPPORTED;
+  if (dv_of(p) != 64 && dv_of(p) != 128) return MEA_ERR_UNSUPPORTED;
   if (p->dtype != MEA_F32 && p->dtype != MEA_F16 && p->dtype != MEA_BF16) return MEA_ERR_UNSUPPORTED;
   return MEA_OK;
 }
 
-// Strides of a tensor of n rows: given, or contiguous [B, H, n, d].
-mea::TensorStrides strides_of(const mea_problem* p, const mea_tensor_strides* given, int64_t n) {
+// Strides of a tensor of n rows of w features: given, or contiguous [B, H, n, w].
+mea::TensorStrides strides_of(const mea_problem* p, const mea_tensor_strides* given, int64_t n, int64_t w) {
   if (given) return {given->batch, given->head, given->row};
-  return {p->heads * n * p->d, n * p->d, p->d};
+  return {p->heads * n * w, n * w, w};
 }
 
-// Validation of one tensor's strides (see mea.h).
-bool strides_ok(const mea_problem* p, const mea::TensorStrides& s, int64_t n, bool output, size_t elem) {
+// Validation of one tensor's strides (see mea.h); w = features per row.
+bool strides_ok(const mea_problem* p, const mea::TensorStrides& s, int64_t n, bool output, size_t elem,
+                int64_t w) {
   const int64_t align = 16 / (int64_t)elem;
-  if (s.b < 0 || s.h < 0 || s.r < p->d || s.r >= ((int64_t)1 << 24)) return false;
+  if (s.b < 0 || s.h < 0 || s.r < w || s.r >= ((int64_t)1 << 24)) return false;
   if (output && (s.b == 0 || s.h == 0)) return false;
   if (s.b % align || s.h % align || s.r % align) return false;
   int64_t a, b, c, tot;
   if (!mul_ok(p->batch - 1, s.b, &a) || !mul_ok(p->heads - 1, s.h, &b) || !mul_ok(n - 1, s.r, &c)) return false;
   if (__builtin_add_overflow(a, b, &tot) || __builtin_add_overflow(tot, c, &tot) ||
-      __builtin_add_overflow(tot, p->d, &tot))
+      __builtin_add_overflow(tot, w, &tot))
     return false;
   return true;
 }
@@ -75,11 +82,11 @@ struct FwdPlan {
   size_t workspace;
 };
 
-void fwd_tiles(int dtype, int64_t d, int* bq, int* bk) {
+void fwd_tiles(int dtype, int64_t d, int64_t dv, int* bq, int* bk) {
   if (dtype == MEA_F32) {
     *bq = mea::FwdShape<float, 64>::BQ;
     *bk = mea::FwdShape<float, 64>::BK;
-  } else if (d == 64) {
+  } else if (d == 64 && dv == 64) {
     *bq = mea::FwdShape<__bf16, 64>::BQ;
     *bk = mea::FwdShape<__bf16, 64>::BK;
   } else {
@@ -111,16 +118,16 @@ FwdPlan plan_decode(const mea_problem* p) {
   pl.workspace = 0;
   if (pl.n_splits > 1) {
     const size_t rows = (size_t)pl.n_splits * (size_t)bh * (size_t)p->n_q;
-    const size_t stage = mea::combine_stage_floats(pl.n_splits, bh * p->n_q, p->d);
-    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256 + (stage ? stage * 4 + 256 : 0);
+    const size_t stage = mea::combine_stage_floats(pl.n_splits, bh * p->n_q, dv_of(p));
+    pl.workspace = rows * (size_t)dv_of(p) * 4 + 2 * rows * 4 + 256 + (stage ? stage * 4 + 256 : 0);
   }
   return pl;
 }
 
 FwdPlan plan_fwd(const mea_problem* p) {
-  if (mea::fwd_uses_decode((int)p->dtype, p->n_q)) return plan_decode(p);
+  if (mea::fwd_uses_decode((int)p->dtype, (int)p->d, (int)dv_of(p), p->n_q)) return plan_decode(p);
   FwdPlan pl;
-  fwd_tiles(p->dtype, p->d, &pl.bq, &pl.bk);
+  fwd_tiles(p->dtype, p->d, dv_of(p), &pl.bq, &pl.bk);
   const int64_t bh = p->batch * p->heads;
   pl.n_qtiles = (p->n_q + pl.bq - 1) / pl.bq;
   const int64_t k_tiles = (p->n_k + pl.bk - 1) / pl.bk;
@@ -141,8 +148,8 @@ FwdPlan plan_fwd(const mea_problem* p) {
   pl.workspace = 0;
   if (pl.n_splits > 1) {
     const size_t rows = (size_t)pl.n_splits * (size_t)bh * (size_t)p->n_q;
-    const size_t stage = mea::combine_stage_floats(pl.n_splits, bh * p->n_q, p->d);
-    pl.workspace = rows * (size_t)p->d * 4 + 2 * rows * 4 + 256 + (stage ? stage * 4 + 256 : 0);
+    const size_t stage = mea::combine_stage_floats(pl.n_splits, bh * p->n_q, dv_of(p));
+    pl.workspace = rows * (size_t)dv_of(p) * 4 + 2 * rows * 4 + 256 + (stage ? stage * 4 + 256 : 0);
   }
   return pl;
 }
@@ -156,7 +163,8 @@ size_t bwd_row_array_bytes(const mea_problem* p, size_t elem) {
 }
 
 bool bwd_records(const mea_problem* p) {
-  return mea::bwd_uses_row_records((int)p->dtype, (int)p->d, p->dtype != MEA_F32 && p->out_f32 != 0);
+  return mea::bwd_uses_row_records((int)p->dtype, (int)p->d, (int)dv_of(p),
+                                   p->dtype != MEA_F32 && p->out_f32 != 0);
 }
 
 size_t bwd_workspace(const mea_problem* p) {
@@ -234,30 +242,32 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
   {
     const mea_strides* st_ = p->strides;
     const size_t e = elem_size(p->dtype), eo = p->out_f32 && p->dtype != MEA_F32 ? 4 : e;
-    fp.sq = strides_of(p, st_ ? &st_->q : nullptr, p->n_q);
-    fp.sk = strides_of(p, st_ ? &st_->k : nullptr, p->n_k);
-    fp.sv = strides_of(p, st_ ? &st_->v : nullptr, p->n_k);
-    fp.so = strides_of(p, st_ ? &st_->o : nullptr, p->n_q);
-    if (!strides_ok(p, fp.sq, p->n_q, false, e) || !strides_ok(p, fp.sk, p->n_k, false, e) ||
-        !strides_ok(p, fp.sv, p->n_k, false, e) || !strides_ok(p, fp.so, p->n_q, true, eo))
+    const int64_t d = p->d, dv = dv_of(p);
+    fp.sq = strides_of(p, st_ ? &st_->q : nullptr, p->n_q, d);
+    fp.sk = strides_of(p, st_ ? &st_->k : nullptr, p->n_k, d);
+    fp.sv = strides_of(p, st_ ? &st_->v : nullptr, p->n_k, dv);
+    fp.so = strides_of(p, st_ ? &st_->o : nullptr, p->n_q, dv);
+    if (!strides_ok(p, fp.sq, p->n_q, false, e, d) || !strides_ok(p, fp.sk, p->n_k, false, e, d) ||
+        !strides_ok(p, fp.sv, p->n_k, false, e, dv) || !strides_ok(p, fp.so, p->n_q, true, eo, dv))
       return MEA_ERR_INVALID_ARG;
   }
   if (pl.n_splits > 1) {
     const size_t rows = (size_t)pl.n_splits * (size_t)fp.bh * (size_t)p->n_q;
     fp.part_o = align256(workspace, 0);
-    fp.part_m = fp.part_o + rows * (size_t)p->d;
+    fp.part_m = fp.part_o + rows * (size_t)dv_of(p);
     fp.part_l = fp.part_m + rows;
     const int64_t rows1 = (int64_t)fp.bh * p->n_q;
-    if (mea::combine_stage_floats(pl.n_splits, rows1, p->d) > 0) {
+    if (mea::combine_stage_floats(pl.n_splits, rows1, dv_of(p)) > 0) {
       const size_t r2 = (size_t)((pl.n_splits + mea::kCombineGroup - 1) / mea::kCombineGroup) * (size_t)rows1;
       fp.part2_o = align256(fp.part_l + rows, 0);
-      fp.part2_m = fp.part2_o + r2 * (size_t)p->d;
+      fp.part2_m = fp.part2_o + r2 * (size_t)dv_of(p);
       fp.part2_l = fp.part2_m + r2;
     }
   }
   const int64_t grid = (int64_t)fp.n_qtiles * fp.bh * fp.n_splits;
   if (grid >= ((int64_t)1 << 31)) return MEA_ERR_INVALID_ARG;
-  const hipError_t e = mea::launch_fwd(fp, p->dtype, (int)p->d, p->causal != 0, p->out_f32 != 0, stream);
+  const hipError_t e = mea::launch_fwd(fp, p->dtype, (int)p->d, (int)dv_of(p), p->causal != 0,
+                                       p->out_f32 != 0, stream);
   return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;
 }
 
@@ -305,21 +315,23 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   {
     const mea_strides* st_ = p->strides;
     const size_t e = elem_size(p->dtype), eo = p->out_f32 && p->dtype != MEA_F32 ? 4 : e;
-    bp.sq = strides_of(p, st_ ? &st_->q : nullptr, p->n_q);
-    bp.sk = strides_of(p, st_ ? &st_->k : nullptr, p->n_k);
-    bp.sv = strides_of(p, st_ ? &st_->v : nullptr, p->n_k);
-    bp.so = strides_of(p, st_ ? &st_->o : nullptr, p->n_q);
-    bp.sdo = strides_of(p, st_ ? &st_->d_o : nullptr, p->n_q);
-    bp.sdq = strides_of(p, st_ ? &st_->dq : nullptr, p->n_q);
-    bp.sdk = strides_of(p, st_ ? &st_->dk : nullptr, p->n_k);
-    bp.sdv = strides_of(p, st_ ? &st_->dv : nullptr, p->n_k);
-    if (!strides_ok(p, bp.sq, p->n_q, false, e) || !strides_ok(p, bp.sk, p->n_k, false, e) ||
-        !strides_ok(p, bp.sv, p->n_k, false, e) || !strides_ok(p, bp.so, p->n_q, false, eo) ||
-        !strides_ok(p, bp.sdo, p->n_q, false, eo) || (dq && !strides_ok(p, bp.sdq, p->n_q, true, e)) ||
-        (dk && (!strides_ok(p, bp.sdk, p->n_k, true, e) || !strides_ok(p, bp.sdv, p->n_k, true, e))))
+    const int64_t d = p->d, dvw = dv_of(p);
+    bp.sq = strides_of(p, st_ ? &st_->q : nullptr, p->n_q, d);
+    bp.sk = strides_of(p, st_ ? &st_->k : nullptr, p->n_k, d);
+    bp.sv = strides_of(p, st_ ? &st_->v : nullptr, p->n_k, dvw);
+    bp.so = strides_of(p, st_ ? &st_->o : nullptr, p->n_q, dvw);
+    bp.sdo = strides_of(p, st_ ? &st_->d_o : nullptr, p->n_q, dvw);
+    bp.sdq = strides_of(p, st_ ? &st_->dq : nullptr, p->n_q, d);
+    bp.sdk = strides_of(p, st_ ? &st_->dk : nullptr, p->n_k, d);
+    bp.sdv = strides_of(p, st_ ? &st_->dv : nullptr, p->n_k, dvw);
+    if (!strides_ok(p, bp.sq, p->n_q, false, e, d) || !strides_ok(p, bp.sk, p->n_k, false, e, d) ||
+        !strides_ok(p, bp.sv, p->n_k, false, e, dvw) || !strides_ok(p, bp.so, p->n_q, false, eo, dvw) ||
+        !strides_ok(p, bp.sdo, p->n_q, false, eo, dvw) || (dq && !strides_ok(p, bp.sdq, p->n_q, true, e, d)) ||
+        (dk && (!strides_ok(p, bp.sdk, p->n_k, true, e, d) || !strides_ok(p, bp.sdv, p->n_k, true, e, dvw))))
       return MEA_ERR_INVALID_ARG;
   }
-  const hipError_t e = mea::launch_bwd(bp, p->dtype, (int)p->d, p->causal != 0, p->out_f32 != 0, stream);
+  const hipError_t e = mea::launch_bwd(bp, p->dtype, (int)p->d, (int)dv_of(p), p->causal != 0,
+                                       p->out_f32 != 0, stream);
   if (e == hipErrorNotSupported) return MEA_ERR_UNSUPPORTED;
   return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;
 }

@@ -101,29 +101,33 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------------- dK, dV
-template <typename T, int D, int QS>
+// D: head dimension of q and k; DV: of v, o and dO.
+template <typename T, int D, int DV, int QS>
 struct DkdvTile {
   static constexpr int NT = 256;
   static constexpr int BKG = 128;      // keys per workgroup (32 per wave)
   static constexpr int BQ = 32 * QS;   // queries per iteration
   static constexpr int E = sizeof(T);
-  static constexpr int RS = D + 16 / E;
-  static constexpr int TILE = BQ * RS;          // Q or dO tile (elements)
-  static constexpr int CPR = D * E / 16;
-  static constexpr int CHUNKS = 2 * BQ * CPR;   // Q and dO chunks per stage
+  static constexpr int RSQ = D + 16 / E;        // LDS row strides (elements), 16 B pad
+  static constexpr int RSO = DV + 16 / E;
+  static constexpr int TILEQ = BQ * RSQ;        // Q tile (elements)
+  static constexpr int TILEO = BQ * RSO;        // dO tile
+  static constexpr int CPRQ = D * E / 16;
+  static constexpr int CPRO = DV * E / 16;
+  static constexpr int CHUNKS = BQ * (CPRQ + CPRO);  // Q and dO chunks per stage
   static constexpr int CPT = (CHUNKS + NT - 1) / NT;
-  static constexpr int STAGE_ELEMS = 2 * TILE;
+  static constexpr int STAGE_ELEMS = TILEQ + TILEO;
   static constexpr int STAGE_BYTES = STAGE_ELEMS * E + 2 * BQ * 4;  // + accumulator initial values
   static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
   static_assert(kBwdRowPad % BQ == 0, "query tiles must not pass the padded row count");
 };
 
-template <typename T, typename TO, int D, int QS, int OCC, bool CAUSAL>
+template <typename T, typename TO, int D, int DV, int QS, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
-  using Cfg = DkdvTile<T, D, QS>;
-  constexpr int RS = Cfg::RS;
-  constexpr int KC = D / 16;
-  constexpr int NDT = D / 32;
+  using Cfg = DkdvTile<T, D, DV, QS>;
+  constexpr int RSQ = Cfg::RSQ, RSO = Cfg::RSO;
+  constexpr int KC = D / 16, KCV = DV / 16;
+  constexpr int NDT = D / 32, NDTV = DV / 32;
   constexpr int NQC = Cfg::BQ / 16;  // 16-query chunks per iteration
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -147,31 +151,37 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   // K^T and V^T as B operands: lane (h, key c) holds row `key`, k = 16kc + 8h + s.
-  Frag<T> kf[KC], vf[KC];
+  Frag<T> kf[KC], vf[KCV];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
     if (key < p.n_k) {
       kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * p.sk.r + 16 * kc + 8 * h);
+    } else {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) kf[kc][s] = (T)0.0f;
+    }
+  }
+#pragma unroll
+  for (int kc = 0; kc < KCV; ++kc) {
+    if (key < p.n_k) {
       vf[kc] = *reinterpret_cast<const Frag<T>*>(vg + key * p.sv.r + 16 * kc + 8 * h);
     } else {
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        kf[kc][s] = (T)0.0f;
-        vf[kc][s] = (T)0.0f;
-      }
+      for (int s = 0; s < 8; ++s) vf[kc][s] = (T)0.0f;
     }
   }
 
   wait_global_loads();
 
-  f32x16 dk[NDT], dv[NDT];
+  f32x16 dk[NDT], dv[NDTV];
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      dk[dt][r] = 0.0f;
-      dv[dt][r] = 0.0f;
-    }
+    for (int r = 0; r < 16; ++r) dk[dt][r] = 0.0f;
+#pragma unroll
+  for (int dt = 0; dt < NDTV; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dv[dt][r] = 0.0f;
 
   // Queries before the first key of this tile see none of its keys; a tile
   // past the batch's valid keys (key padding) is seen by none.
@@ -187,15 +197,17 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
     for (int i = 0; i < Cfg::CPT; ++i) {
       const int chunk = tid + i * Cfg::NT;
       if (chunk < Cfg::CHUNKS) {
-        const int which = chunk / (Cfg::BQ * Cfg::CPR);  // 0 = Q, 1 = dO
-        const int rem = chunk % (Cfg::BQ * Cfg::CPR);
-        const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
+        // The Q tile's BQ * CPRQ chunks, then the dO tile's.
+        const bool is_o = chunk >= Cfg::BQ * Cfg::CPRQ;
+        const int rem = is_o ? chunk - Cfg::BQ * Cfg::CPRQ : chunk;
+        const int cpr = is_o ? Cfg::CPRO : Cfg::CPRQ;
+        const int row = rem / cpr, col = rem % cpr;
         const int64_t q = q0 + row;
         const int64_t coff = col * (16 / Cfg::E);
         if (q >= p.n_q)
           stage[i] = u32x4{0u, 0u, 0u, 0u};
         else
-          stage[i] = which ? ld_chunk_as<T, TO>(dog + q * p.sdo.r + coff) : ld16(qg + q * p.sq.r + coff);
+          stage[i] = is_o ? ld_chunk_as<T, TO>(dog + q * p.sdo.r + coff) : ld16(qg + q * p.sq.r + coff);
       }
     }
     if (tid < 2 * Cfg::BQ) {
@@ -210,10 +222,11 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
     for (int i = 0; i < Cfg::CPT; ++i) {
       const int chunk = tid + i * Cfg::NT;
       if (chunk < Cfg::CHUNKS) {
-        const int which = chunk / (Cfg::BQ * Cfg::CPR);
-        const int rem = chunk % (Cfg::BQ * Cfg::CPR);
-        const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
-        st16(base + which * Cfg::TILE + row * RS + col * (16 / Cfg::E), stage[i]);
+        const bool is_o = chunk >= Cfg::BQ * Cfg::CPRQ;
+        const int rem = is_o ? chunk - Cfg::BQ * Cfg::CPRQ : chunk;
+        const int cpr = is_o ? Cfg::CPRO : Cfg::CPRQ;
+        const int row = rem / cpr, col = rem % cpr;
+        st16(base + (is_o ? Cfg::TILEQ + row * RSO : row * RSQ) + col * (16 / Cfg::E), stage[i]);
       }
     }
     if (tid < 2 * Cfg::BQ) {
@@ -240,7 +253,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
     if (has_next) load_stage(q0 + Cfg::BQ);
 
     const T* qs_t = reinterpret_cast<const T*>(stage_base(it & 1));
-    const T* dos_t = qs_t + Cfg::TILE;
+    const T* dos_t = qs_t + Cfg::TILEQ;
     const float* sinit_s = reinterpret_cast<const float*>(stage_base(it & 1) + Cfg::STAGE_ELEMS * Cfg::E);
     const float* dpinit_s = sinit_s + Cfg::BQ;
 
@@ -267,13 +280,17 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       // S = Q K^T - lse/scale and dP = dO V^T - D (rows: queries in perm32
       // order; lane: key).
 #pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
+      for (int kc = 0; kc < (KC > KCV ? KC : KCV); ++kc) {
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) {
-          const Frag<T> a = lds_frag<T>(qs_t + (32 * qs + qrow) * RS + 16 * kc + 8 * h);
-          s[qs] = mma(a, kf[kc], s[qs]);
-          const Frag<T> g = lds_frag<T>(dos_t + (32 * qs + qrow) * RS + 16 * kc + 8 * h);
-          dp[qs] = mma(g, vf[kc], dp[qs]);
+          if (kc < KC) {
+            const Frag<T> a = lds_frag<T>(qs_t + (32 * qs + qrow) * RSQ + 16 * kc + 8 * h);
+            s[qs] = mma(a, kf[kc], s[qs]);
+          }
+          if (kc < KCV) {
+            const Frag<T> g = lds_frag<T>(dos_t + (32 * qs + qrow) * RSO + 16 * kc + 8 * h);
+            dp[qs] = mma(g, vf[kc], dp[qs]);
+          }
         }
       }
       const bool need_mask = CAUSAL && q0 < kw + 31;
@@ -300,17 +317,25 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
         const Frag<T> pa = to_frag<T>(tp);
         const Frag<T> da = to_frag<T>(td);
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) {
-          Frag<T> bo, bq;
-          if constexpr (sizeof(T) == 2) {
-            bo = lds_col_frag<T>(dos_t, RS, 16 * qc, 32 * dt, lane);
-            bq = lds_col_frag<T>(qs_t, RS, 16 * qc, 32 * dt, lane);
-          } else {
-            bo = lds_col_frag_f32(reinterpret_cast<const float*>(dos_t), RS, 16 * qc, 32 * dt, lane);
-            bq = lds_col_frag_f32(reinterpret_cast<const float*>(qs_t), RS, 16 * qc, 32 * dt, lane);
+        for (int dt = 0; dt < (NDT > NDTV ? NDT : NDTV); ++dt) {
+          if (dt < NDTV) {
+            Frag<T> bo;
+            if constexpr (sizeof(T) == 2) {
+              bo = lds_col_frag<T>(dos_t, RSO, 16 * qc, 32 * dt, lane);
+            } else {
+              bo = lds_col_frag_f32(reinterpret_cast<const float*>(dos_t), RSO, 16 * qc, 32 * dt, lane);
+            }
+            dv[dt] = mma(pa, bo, dv[dt]);
           }
-          dv[dt] = mma(pa, bo, dv[dt]);
-          dk[dt] = mma(da, bq, dk[dt]);
+          if (dt < NDT) {
+            Frag<T> bq;
+            if constexpr (sizeof(T) == 2) {
+              bq = lds_col_frag<T>(qs_t, RSQ, 16 * qc, 32 * dt, lane);
+            } else {
+              bq = lds_col_frag_f32(reinterpret_cast<const float*>(qs_t), RSQ, 16 * qc, 32 * dt, lane);
+            }
+            dk[dt] = mma(da, bq, dk[dt]);
+          }
         }
       }
     }
@@ -327,10 +352,15 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int64_t kr = kw + c_row(r, h);
-      if (kr < p.n_k) {  // keys past the valid length get zero gradients
+      if (kr < p.n_k)  // keys past the valid length get zero gradients
         dkg[kr * p.sdk.r + 32 * dt + c] = kr < n_kv ? (T)(dk[dt][r] * p.scale) : (T)0.0f;
-        dvg[kr * p.sdv.r + 32 * dt + c] = kr < n_kv ? (T)dv[dt][r] : (T)0.0f;
-      }
+    }
+#pragma unroll
+  for (int dt = 0; dt < NDTV; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t kr = kw + c_row(r, h);
+      if (kr < p.n_k) dvg[kr * p.sdv.r + 32 * dt + c] = kr < n_kv ? (T)dv[dt][r] : (T)0.0f;
     }
 }
 
@@ -683,18 +713,19 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
 }
 
 // ------------------------------------------------------------------- dQ
-template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
+// D: head dimension of q and k; DV: of v and dO.
+template <typename T, typename TO, int D, int DV, int QT, int BK, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   constexpr int NT = 256;
   constexpr int BQ = 128 * QT;  // 4 waves x QT x 32 queries
   constexpr int E = sizeof(T);
-  constexpr int RS = D + 16 / E;
-  constexpr int TILE = BK * RS;
-  constexpr int CPR = D * E / 16;
-  constexpr int CHUNKS = 2 * BK * CPR;
+  constexpr int RSK = D + 16 / E, RSV = DV + 16 / E;  // LDS row strides (elements)
+  constexpr int TILEK = BK * RSK, TILEV = BK * RSV;
+  constexpr int CPRK = D * E / 16, CPRV = DV * E / 16;
+  constexpr int CHUNKS = BK * (CPRK + CPRV);
   constexpr int CPT = CHUNKS / NT;
   static_assert(CHUNKS % NT == 0, "tile must split evenly");
-  constexpr int KC = D / 16;
+  constexpr int KC = D / 16, KCV = DV / 16;
   constexpr int NKT = BK / 32;
   constexpr int NPC = BK / 16;
   constexpr int NDT = D / 32;
@@ -721,7 +752,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   // Q^T and dO^T as B operands: lane (h, query c of sub-tile t), k = 16kc + 8h + s.
   // Initial values of the S^T and dP^T accumulators of each query: -lse/scale
   // (P = 2^(c*acc)) and -D (dS = P*acc); -inf for a padding row.
-  Frag<T> qf[QT][KC], gf[QT][KC];
+  Frag<T> qf[QT][KC], gf[QT][KCV];
   float s_init[QT], dp_init[QT];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
@@ -731,13 +762,18 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
     for (int kc = 0; kc < KC; ++kc) {
       if (valid) {
         qf[t][kc] = *reinterpret_cast<const Frag<T>*>(qg + query * p.sq.r + 16 * kc + 8 * h);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[t][kc][e] = (T)0.0f;
+      }
+    }
+#pragma unroll
+    for (int kc = 0; kc < KCV; ++kc) {
+      if (valid) {
         gf[t][kc] = ld_frag_as<T, TO>(dog + query * p.sdo.r + 16 * kc + 8 * h);
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          qf[t][kc][e] = (T)0.0f;
-          gf[t][kc][e] = (T)0.0f;
-        }
+        for (int e = 0; e < 8; ++e) gf[t][kc][e] = (T)0.0f;
       }
     }
     s_init[t] = valid ? p.s_init[(size_t)bh * p.n_q_pad + query] : -INFINITY;
@@ -764,24 +800,27 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   auto load_stage = [&](int64_t k0) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
+      // The K tile's BK * CPRK chunks, then the V tile's.
       const int chunk = tid + i * NT;
-      const int which = chunk / (BK * CPR);
-      const int rem = chunk % (BK * CPR);
-      const int row = rem / CPR, col = rem % CPR;
+      const bool is_v = chunk >= BK * CPRK;
+      const int rem = is_v ? chunk - BK * CPRK : chunk;
+      const int cpr = is_v ? CPRV : CPRK;
+      const int row = rem / cpr, col = rem % cpr;
       const int64_t kr = k0 + row;
-      const T* src = (which ? vg + kr * p.sv.r : kg + kr * p.sk.r) + col * (16 / E);
+      const T* src = (is_v ? vg + kr * p.sv.r : kg + kr * p.sk.r) + col * (16 / E);
       stage[i] = kr < p.n_k ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
     }
   };
   auto store_stage = [&](int buf) {
-    T* base = smem + buf * 2 * TILE;
+    T* base = smem + buf * (TILEK + TILEV);
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int chunk = tid + i * NT;
-      const int which = chunk / (BK * CPR);
-      const int rem = chunk % (BK * CPR);
-      const int row = rem / CPR, col = rem % CPR;
-      st16(base + which * TILE + row * RS + col * (16 / E), stage[i]);
+      const bool is_v = chunk >= BK * CPRK;
+      const int rem = is_v ? chunk - BK * CPRK : chunk;
+      const int cpr = is_v ? CPRV : CPRK;
+      const int row = rem / cpr, col = rem % cpr;
+      st16(base + (is_v ? TILEK + row * RSV : row * RSK) + col * (16 / E), stage[i]);
     }
   };
 
@@ -806,8 +845,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   auto tile = [&](auto mask_tag, int it) {
     constexpr bool MASK = decltype(mask_tag)::value;
     const int64_t k0 = (int64_t)it * BK;
-    const T* ks = smem + (it & 1) * 2 * TILE;
-    const T* vs = ks + TILE;
+    const T* ks = smem + (it & 1) * (TILEK + TILEV);
+    const T* vs = ks + TILEK;
     if (MASK && CAUSAL && k0 > qw + 32 * QT - 1) return;  // all keys after this wave's queries
     f32x16 s[NKT][QT], dp[NKT][QT];
 #pragma unroll
@@ -822,15 +861,18 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
     // S^T = K Q^T - lse/scale and dP^T = V dO^T - D (rows: keys in perm32
     // order; lane: query).
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc)
+    for (int kc = 0; kc < (KC > KCV ? KC : KCV); ++kc)
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) {
-        const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
-        const Frag<T> b = lds_frag<T>(vs + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+        if (kc < KC) {
+          const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RSK + 16 * kc + 8 * h);
 #pragma unroll
-        for (int t = 0; t < QT; ++t) {
-          s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
-          dp[kt][t] = mma(b, gf[t][kc], dp[kt][t]);
+          for (int t = 0; t < QT; ++t) s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
+        }
+        if (kc < KCV) {
+          const Frag<T> b = lds_frag<T>(vs + (32 * kt + krow) * RSV + 16 * kc + 8 * h);
+#pragma unroll
+          for (int t = 0; t < QT; ++t) dp[kt][t] = mma(b, gf[t][kc], dp[kt][t]);
         }
       }
     // Tile-relative 32-bit bounds: key k0 + x is valid iff x < key_lim and,
@@ -868,9 +910,9 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
       for (int dt = 0; dt < NDT; ++dt) {
         Frag<T> a;
         if constexpr (sizeof(T) == 2) {
-          a = lds_col_frag<T>(ks, RS, 16 * pc, 32 * dt, lane);
+          a = lds_col_frag<T>(ks, RSK, 16 * pc, 32 * dt, lane);
         } else {
-          a = lds_col_frag_f32(reinterpret_cast<const float*>(ks), RS, 16 * pc, 32 * dt, lane);
+          a = lds_col_frag_f32(reinterpret_cast<const float*>(ks), RSK, 16 * pc, 32 * dt, lane);
         }
 #pragma unroll
         for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, b[t], acc[t][dt]);
@@ -1365,15 +1407,17 @@ template <> struct BwdShape<float, 128> {
   static constexpr int QS = 1, KV_OCC = 1, QT = 1, BK = 32, Q_OCC = 1;
 };
 
-template <typename T, typename TO, int D, bool CAUSAL>
+// D: head dimension of q and k; DV: of v, o and dO (tile shapes of the
+// larger of the two).
+template <typename T, typename TO, int D, int DV, bool CAUSAL>
 static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
-  using S = BwdShape<T, D>;
-  using Dk = DkdvTile<T, D, S::QS>;
+  using S = BwdShape<T, (D > DV ? D : DV)>;
+  using Dk = DkdvTile<T, D, DV, S::QS>;
   void* args[] = {&p};
   const int64_t rows = (int64_t)p.bh * p.n_q_pad;
-  constexpr int RPB = 256 / (D * (int)sizeof(TO) / 16);
-  constexpr bool PP = sizeof(T) == 2 && D == 64 && __is_same(T, TO);
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, D, PP>),
+  constexpr int RPB = 256 / (DV * (int)sizeof(TO) / 16);
+  constexpr bool PP = sizeof(T) == 2 && D == 64 && DV == 64 && __is_same(T, TO);
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, PP>),
                                  dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
   if (e != hipSuccess) return e;
   p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
@@ -1384,7 +1428,7 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
       e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_pp_kernel<T, CAUSAL>),
                           dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(kvpp::NW * 64), args, 0, stream);
     } else {
-      e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, S::QS, S::KV_OCC, CAUSAL>),
+      e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, DV, S::QS, S::KV_OCC, CAUSAL>),
                           dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
     }
     if (e != hipSuccess || !p.dq) return e;
@@ -1394,14 +1438,14 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
     return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_pp_kernel<T, CAUSAL>),
                            dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(qpp::NW * 64), args, 0, stream);
   }
-  const int dq_lds = 2 * 2 * S::BK * (D + 16 / (int)sizeof(T)) * (int)sizeof(T);
-  return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, S::QT, S::BK, S::Q_OCC, CAUSAL>),
+  const int dq_lds = 2 * S::BK * (D + DV + 2 * 16 / (int)sizeof(T)) * (int)sizeof(T);
+  return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, DV, S::QT, S::BK, S::Q_OCC, CAUSAL>),
                          dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(256), args, dq_lds, stream);
 }
 
-template <typename T, typename TO, int D>
+template <typename T, typename TO, int D, int DV = D>
 static hipError_t launch_bwd_dt(const BwdParams& p, bool causal, hipStream_t stream) {
-  return causal ? launch_bwd_impl<T, TO, D, true>(p, stream) : launch_bwd_impl<T, TO, D, false>(p, stream);
+  return causal ? launch_bwd_impl<T, TO, D, DV, true>(p, stream) : launch_bwd_impl<T, TO, D, DV, false>(p, stream);
 }
 
 template <typename T, int D>
@@ -1409,8 +1453,24 @@ static hipError_t launch_bwd_out(const BwdParams& p, bool causal, bool out_f32, 
   return out_f32 ? launch_bwd_dt<T, float, D>(p, causal, stream) : launch_bwd_dt<T, T, D>(p, causal, stream);
 }
 
-hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, bool out_f32,
+// Value head dimension different from the query/key one (64 and 128).
+template <typename T, typename TO>
+static hipError_t launch_bwd_dv_pair(const BwdParams& p, int d, bool causal, hipStream_t stream) {
+  return d == 64 ? launch_bwd_dt<T, TO, 64, 128>(p, causal, stream) : launch_bwd_dt<T, TO, 128, 64>(p, causal, stream);
+}
+
+hipError_t launch_bwd(const BwdParams& p, int dtype, int d, int dv, bool causal, bool out_f32,
                       hipStream_t stream) {
+  if (dv != d) {
+    switch (dtype) {
+      case 0: return launch_bwd_dv_pair<float, float>(p, d, causal, stream);
+      case 1: return out_f32 ? launch_bwd_dv_pair<_Float16, float>(p, d, causal, stream)
+                             : launch_bwd_dv_pair<_Float16, _Float16>(p, d, causal, stream);
+      case 2: return out_f32 ? launch_bwd_dv_pair<__bf16, float>(p, d, causal, stream)
+                             : launch_bwd_dv_pair<__bf16, __bf16>(p, d, causal, stream);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (dtype * 1000 + d) {
     case 0 * 1000 + 64: return launch_bwd_dt<float, float, 64>(p, causal, stream);
     case 0 * 1000 + 128: return launch_bwd_dt<float, float, 128>(p, causal, stream);

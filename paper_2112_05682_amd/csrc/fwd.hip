@@ -36,30 +36,35 @@ constexpr float kLn2 = 0.6931471805599453f;
 template <bool B> struct BoolC { static constexpr bool value = B; };
 template <int I> struct IntC { static constexpr int value = I; };
 
-template <typename T, int D, int QT, int BK>
+// D: head dimension of q and k; DV: of v and o.
+template <typename T, int D, int DV, int QT, int BK>
 struct FwdTile {
   static constexpr int NW = 4;
   static constexpr int NT = NW * 64;
   static constexpr int BQ = NW * QT * 32;
   static constexpr int E = sizeof(T);
-  static constexpr int RS = D + 16 / E;          // LDS row stride (elements), 16 B pad
-  static constexpr int TILE = BK * RS;           // elements per K or V tile
-  static constexpr int CPR = D * E / 16;         // 16-byte chunks per row
-  static constexpr int CHUNKS = 2 * BK * CPR;    // K and V chunks per stage
+  static constexpr int RSK = D + 16 / E;         // LDS row strides (elements), 16 B pad
+  static constexpr int RSV = DV + 16 / E;
+  static constexpr int TILEK = BK * RSK;         // elements of the K tile
+  static constexpr int TILEV = BK * RSV;         // elements of the V tile
+  static constexpr int STAGE = TILEK + TILEV;    // one K/V stage
+  static constexpr int CPRK = D * E / 16;        // 16-byte chunks per row
+  static constexpr int CPRV = DV * E / 16;
+  static constexpr int CHUNKS = BK * (CPRK + CPRV);  // K and V chunks per stage
   static constexpr int CPT = CHUNKS / NT;        // chunks per thread per stage
-  static constexpr int LDS_BYTES = 2 * 2 * TILE * E;  // double-buffered K and V
+  static constexpr int LDS_BYTES = 2 * STAGE * E;  // double-buffered K and V
   static_assert(CHUNKS % NT == 0, "tile must split evenly over the workgroup");
-  static_assert(BK % 32 == 0 && D % 32 == 0, "tile shapes are multiples of 32");
+  static_assert(BK % 32 == 0 && D % 32 == 0 && DV % 32 == 0, "tile shapes are multiples of 32");
 };
 
-template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
+template <typename T, typename TO, int D, int DV, int QT, int BK, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
-  using Cfg = FwdTile<T, D, QT, BK>;
-  constexpr int RS = Cfg::RS;
+  using Cfg = FwdTile<T, D, DV, QT, BK>;
+  constexpr int RSK = Cfg::RSK, RSV = Cfg::RSV;
   constexpr int KC = D / 16;    // 16-wide k chunks of the QK^T contraction
   constexpr int NKT = BK / 32;  // 32-key sub-tiles per tile
   constexpr int NPC = BK / 16;  // 16-key chunks of the PV contraction
-  constexpr int NDT = D / 32;   // 32-row tiles of O^T
+  constexpr int NDT = DV / 32;  // 32-row tiles of O^T
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* smem = reinterpret_cast<T*>(smem_raw);
@@ -126,28 +131,31 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 
   // ---- global -> register staging of one K/V stage (zero rows past n_k).
   u32x4 stage[Cfg::CPT];
+  // Chunk i of a stage: the K tile's BK * CPRK chunks, then the V tile's.
   auto load_stage = [&](int64_t k0) {
 #pragma unroll
     for (int i = 0; i < Cfg::CPT; ++i) {
       const int chunk = tid + i * Cfg::NT;
-      const int which = chunk / (BK * Cfg::CPR);  // 0 = K, 1 = V
-      const int rem = chunk % (BK * Cfg::CPR);
-      const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
+      const bool is_v = chunk >= BK * Cfg::CPRK;
+      const int rem = is_v ? chunk - BK * Cfg::CPRK : chunk;
+      const int cpr = is_v ? Cfg::CPRV : Cfg::CPRK;
+      const int row = rem / cpr, col = rem % cpr;
       const int64_t key = k0 + row;
-      const T* src = which ? vg + key * p.sv.r : kg + key * p.sk.r;
+      const T* src = is_v ? vg + key * p.sv.r : kg + key * p.sk.r;
       src += col * (16 / Cfg::E);
       stage[i] = key < p.n_k ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
     }
   };
   auto store_stage = [&](int buf) {
-    T* base = smem + buf * 2 * Cfg::TILE;
+    T* base = smem + buf * Cfg::STAGE;
 #pragma unroll
     for (int i = 0; i < Cfg::CPT; ++i) {
       const int chunk = tid + i * Cfg::NT;
-      const int which = chunk / (BK * Cfg::CPR);
-      const int rem = chunk % (BK * Cfg::CPR);
-      const int row = rem / Cfg::CPR, col = rem % Cfg::CPR;
-      st16(base + which * Cfg::TILE + row * RS + col * (16 / Cfg::E), stage[i]);
+      const bool is_v = chunk >= BK * Cfg::CPRK;
+      const int rem = is_v ? chunk - BK * Cfg::CPRK : chunk;
+      const int cpr = is_v ? Cfg::CPRV : Cfg::CPRK;
+      const int row = rem / cpr, col = rem % cpr;
+      st16(base + (is_v ? Cfg::TILEK + row * RSV : row * RSK) + col * (16 / Cfg::E), stage[i]);
     }
   };
 
@@ -171,8 +179,8 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   auto tile = [&](auto mask_tag, int it) {
     constexpr bool MASK = decltype(mask_tag)::value;
     const int64_t k0 = kb + (int64_t)it * BK;
-    const T* ks = smem + (it & 1) * 2 * Cfg::TILE;
-    const T* vs = ks + Cfg::TILE;
+    const T* ks = smem + (it & 1) * Cfg::STAGE;
+    const T* vs = ks + Cfg::TILEK;
     // A wave whose queries all precede the tile's first key has nothing to do.
     if (MASK && CAUSAL && k0 > qw + QT * 32 - 1) return;
 
@@ -187,7 +195,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
     for (int kc = 0; kc < KC; ++kc) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) {
-        const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+        const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RSK + 16 * kc + 8 * h);
 #pragma unroll
         for (int t = 0; t < QT; ++t) s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
       }
@@ -254,9 +262,9 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
       for (int pc = 0; pc < NPC; ++pc) {
         Frag<T> a;
         if constexpr (sizeof(T) == 2) {
-          a = lds_col_frag<T>(vs, RS, 16 * pc, 32 * dt, lane);
+          a = lds_col_frag<T>(vs, RSV, 16 * pc, 32 * dt, lane);
         } else {
-          a = lds_col_frag_f32(reinterpret_cast<const float*>(vs), RS, 16 * pc, 32 * dt, lane);
+          a = lds_col_frag_f32(reinterpret_cast<const float*>(vs), RSV, 16 * pc, 32 * dt, lane);
         }
 #pragma unroll
         for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, pf[t][pc], acc[t][dt]);
@@ -306,7 +314,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
         p.lse[(size_t)bh * p.n_q + row] = l_tot > 0.0f ? (m_ref[t] + __log2f(l_tot)) * kLn2 : -INFINITY;
     } else {
       const size_t prow = ((size_t)split * p.bh + bh) * p.n_q + row;
-      float* po = p.part_o + prow * D;
+      float* po = p.part_o + prow * DV;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -885,17 +893,17 @@ static hipError_t launch_combine(const FwdParams& p, hipStream_t stream) {
                          dim3((unsigned)((threads + 255) / 256)), dim3(256), args, 0, stream);
 }
 
-template <typename T, typename TO, int D, int QT, int BK, int OCC, bool CAUSAL>
+template <typename T, typename TO, int D, int DV, int QT, int BK, int OCC, bool CAUSAL>
 static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
-  using Cfg = FwdTile<T, D, QT, BK>;
-  auto kern = attn_fwd_kernel<T, TO, D, QT, BK, OCC, CAUSAL>;
+  using Cfg = FwdTile<T, D, DV, QT, BK>;
+  auto kern = attn_fwd_kernel<T, TO, D, DV, QT, BK, OCC, CAUSAL>;
   const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
   FwdParams pc = p;
   void* args[] = {&pc};
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid),
                                  dim3(Cfg::NT), args, Cfg::LDS_BYTES, stream);
   if (e != hipSuccess || p.n_splits == 1) return e;
-  return launch_combine<TO, D>(p, stream);
+  return launch_combine<TO, DV>(p, stream);
 }
 
 template <typename T, typename TO, bool CAUSAL>
@@ -916,9 +924,21 @@ static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t str
     return causal ? launch_fwd_pp<T, TO, true>(p, stream) : launch_fwd_pp<T, TO, false>(p, stream);
   } else {
     constexpr int QT = FwdShape<T, D>::QT, BK = FwdShape<T, D>::BK, OCC = FwdShape<T, D>::OCC;
-    return causal ? launch_fwd_impl<T, TO, D, QT, BK, OCC, true>(p, stream)
-                  : launch_fwd_impl<T, TO, D, QT, BK, OCC, false>(p, stream);
+    return causal ? launch_fwd_impl<T, TO, D, D, QT, BK, OCC, true>(p, stream)
+                  : launch_fwd_impl<T, TO, D, D, QT, BK, OCC, false>(p, stream);
   }
+}
+
+// Value head dimension DV != D: the 4-wave kernel with the d = 128 tile shape.
+template <typename T, typename TO, int D, int DV>
+static hipError_t launch_fwd_dv(const FwdParams& p, bool causal, hipStream_t stream) {
+  using S = FwdShape<T, 128>;
+  return causal ? launch_fwd_impl<T, TO, D, DV, S::QT, S::BK, S::OCC, true>(p, stream)
+                : launch_fwd_impl<T, TO, D, DV, S::QT, S::BK, S::OCC, false>(p, stream);
+}
+template <typename T, typename TO>
+static hipError_t launch_fwd_dv_pair(const FwdParams& p, int d, bool causal, hipStream_t stream) {
+  return d == 64 ? launch_fwd_dv<T, TO, 64, 128>(p, causal, stream) : launch_fwd_dv<T, TO, 128, 64>(p, causal, stream);
 }
 
 template <typename T, int D>
@@ -926,9 +946,19 @@ static hipError_t launch_fwd_out(const FwdParams& p, bool causal, bool out_f32, 
   return out_f32 ? launch_fwd_dt<T, float, D>(p, causal, stream) : launch_fwd_dt<T, T, D>(p, causal, stream);
 }
 
-hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, bool out_f32,
+hipError_t launch_fwd(const FwdParams& p, int dtype, int d, int dv, bool causal, bool out_f32,
                       hipStream_t stream) {
-  if (fwd_uses_decode(dtype, p.n_q)) {
+  if (dv != d) {
+    switch (dtype) {
+      case 0: return launch_fwd_dv_pair<float, float>(p, d, causal, stream);
+      case 1: return out_f32 ? launch_fwd_dv_pair<_Float16, float>(p, d, causal, stream)
+                             : launch_fwd_dv_pair<_Float16, _Float16>(p, d, causal, stream);
+      case 2: return out_f32 ? launch_fwd_dv_pair<__bf16, float>(p, d, causal, stream)
+                             : launch_fwd_dv_pair<__bf16, __bf16>(p, d, causal, stream);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (fwd_uses_decode(dtype, d, dv, p.n_q)) {
     const hipError_t e = launch_decode(p, dtype, d, causal, out_f32, stream);
     if (e != hipSuccess || p.n_splits == 1) return e;
     const bool f32 = out_f32;

@@ -107,8 +107,11 @@ struct BwdParams {
 constexpr int kBwdRowPad = 64;
 
 // Whether the backward of a problem runs the two-group kernels, which take
-// the per-row values as records (dtype: 0 float32, 1 fp16, 2 bf16).
-inline bool bwd_uses_row_records(int dtype, int d, bool out_f32) { return dtype != 0 && d == 64 && !out_f32; }
+// the per-row values as records (dtype: 0 float32, 1 fp16, 2 bf16; d and dv
+// the head dimensions of q, k and of v, o).
+inline bool bwd_uses_row_records(int dtype, int d, int dv, bool out_f32) {
+  return dtype != 0 && d == 64 && dv == 64 && !out_f32;
+}
 
 // Tile shapes per (element type, head dimension); shared by the host plan
 // and the kernel instantiations.
@@ -137,12 +140,13 @@ template <> struct FwdShape<float, 128> { static constexpr int QT = 1, BK = 32, 
 // out_f32: o (and, in the backward, do) are float32 instead of the input dtype.
 // Decode-shaped forward: 16-bit inputs and at most 64 queries per (batch,
 // head) run the key-streaming decode kernel (key tile fwd_decode_tile(d)).
-inline bool fwd_uses_decode(int dtype, int64_t n_q) { return dtype != 0 && n_q <= 64; }
+inline bool fwd_uses_decode(int dtype, int d, int dv, int64_t n_q) { return dtype != 0 && d == dv && n_q <= 64; }
 inline int fwd_decode_tile(int d) { return d == 64 ? 64 : 32; }
 hipError_t launch_decode(const FwdParams& p, int dtype, int d, bool causal, bool out_f32, hipStream_t stream);
-hipError_t launch_fwd(const FwdParams& p, int dtype, int d, bool causal, bool out_f32,
+// dv: head dimension of v and o (equal to d, or the other of 64 and 128).
+hipError_t launch_fwd(const FwdParams& p, int dtype, int d, int dv, bool causal, bool out_f32,
                       hipStream_t stream);
-hipError_t launch_bwd(const BwdParams& p, int dtype, int d, bool causal, bool out_f32,
+hipError_t launch_bwd(const BwdParams& p, int dtype, int d, int dv, bool causal, bool out_f32,
                       hipStream_t stream);
 
 }  // namespace mea

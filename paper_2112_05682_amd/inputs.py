@@ -77,15 +77,18 @@ def normal(shape, seed: int, std: float = 1.0, mult: float = 1.0,
 
 def attention_inputs(batch: int, heads: int, n_q: int, n_k: int, d: int,
                      dtype: str | torch.dtype = "bf16", std: float = 1.0,
-                     qk_mult: float = 1.0, seeds=(0, 1, 2, 3), with_grad: bool = True):
-    """Q, K, V (and dO) as CPU tensors of layout [B, H, n, d]."""
+                     qk_mult: float = 1.0, seeds=(0, 1, 2, 3), with_grad: bool = True,
+                     d_v: int | None = None):
+    """Q, K, V (and dO) as CPU tensors of layout [B, H, n, features]: q and k
+    with d features, v and dO with d_v (default d)."""
     dt = DTYPES[dtype] if isinstance(dtype, str) else dtype
+    d_v = d if d_v is None else d_v
     q = normal((batch, heads, n_q, d), seeds[0], std, qk_mult, dt)
     k = normal((batch, heads, n_k, d), seeds[1], std, qk_mult, dt)
-    v = normal((batch, heads, n_k, d), seeds[2], std, 1.0, dt)
+    v = normal((batch, heads, n_k, d_v), seeds[2], std, 1.0, dt)
     out = {"q": q, "k": k, "v": v}
     if with_grad:
-        out["do"] = normal((batch, heads, n_q, d), seeds[3], 1.0, 1.0, dt)
+        out["do"] = normal((batch, heads, n_q, d_v), seeds[3], 1.0, 1.0, dt)
     return out
 
 

@@ -149,13 +149,13 @@ def test_problem_struct_layout_matches_the_header(tmp_path):
     src = tmp_path / "layout.c"
     src.write_text(
         '#include <stddef.h>\n#include <stdio.h>\n#include "mea.h"\n'
-        'int main(void) { printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", '
+        'int main(void) { printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\\n", '
         'sizeof(mea_problem), '
         'offsetof(mea_problem, batch), offsetof(mea_problem, heads), offsetof(mea_problem, n_q), '
         'offsetof(mea_problem, n_k), offsetof(mea_problem, d), offsetof(mea_problem, dtype), '
         'offsetof(mea_problem, causal), offsetof(mea_problem, scale), '
         'offsetof(mea_problem, out_f32), offsetof(mea_problem, strides), '
-        'offsetof(mea_problem, kv_len), '
+        'offsetof(mea_problem, kv_len), offsetof(mea_problem, d_v), '
         'sizeof(mea_strides), offsetof(mea_strides, d_o), offsetof(mea_strides, dv)); return 0; }\n')
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROOT, "include"),
@@ -216,3 +216,28 @@ def test_rejects_misaligned_kv_len():
     assert _lib.bwd(p, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
     ok = _lib.problem(1, 2, 100, 100, 64, _lib.MEA_BF16, False, 0.125, kv_len=FAKE)
     assert ok.kv_len == FAKE
+
+
+@pytest.mark.parametrize("d,d_v,status", [(64, 128, None), (128, 64, None), (64, 96, "unsupported"),
+                                          (64, -64, "invalid")])
+def test_value_head_dimension_validation(d, d_v, status):
+    # d_v = 0 means d; 64 and 128 are supported in any combination with d.
+    p = _lib.problem(1, 2, 100, 100, d, _lib.MEA_BF16, False, 0.125, d_v=d_v)
+    st, _ = ws_status(p)
+    want = {None: _lib.MEA_OK, "unsupported": _lib.MEA_ERR_UNSUPPORTED,
+            "invalid": _lib.MEA_ERR_INVALID_ARG}[status]
+    assert st == want
+
+
+def test_value_head_dimension_sets_default_strides():
+    # Contiguous strides of v, o, do and dv follow d_v; those of q, k, dq, dk d.
+    p = _lib.problem(2, 3, 10, 20, 64, _lib.MEA_BF16, False, 0.125, d_v=128,
+                     strides={"q": (3 * 10 * 64, 10 * 64, 64)})
+    st = p.strides.contents
+    assert (st.v.batch, st.v.head, st.v.row) == (3 * 20 * 128, 20 * 128, 128)
+    assert (st.o.batch, st.o.head, st.o.row) == (3 * 10 * 128, 10 * 128, 128)
+    assert (st.k.batch, st.k.head, st.k.row) == (3 * 20 * 64, 20 * 64, 64)
+    # A value row stride below d_v is rejected before any launch.
+    bad = _lib.problem(1, 1, 10, 20, 64, _lib.MEA_BF16, False, 0.125, d_v=128,
+                       strides={"v": (20 * 128, 20 * 128, 64)})
+    assert _lib.fwd(bad, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.MEA_ERR_INVALID_ARG

@@ -547,3 +547,105 @@ def test_key_padding_subsets_match_full(oracle_mod):
         dkr, dvr = oracle_mod.bwd_dkdv_keys(q, k, v, do, keys, causal=causal, n_valid=n_valid)
         np.testing.assert_array_equal(dkr, dk[0, 0, keys])
         np.testing.assert_array_equal(dvr, dv[0, 0, keys])
+
+
+# ---------------------------------------------------------------- value width d_v != d
+# The definition puts no constraint between the key width d and the value
+# width d_v: scores use d, outputs have d_v features.
+
+def run_fwd_any(oracle, form, q, k, v, scale, causal, kv_len=None):
+    if form == "direct":
+        return oracle.fwd(q, k, v, scale, causal, kv_len=kv_len)
+    if form == "lazy":
+        return oracle.fwd_lazy(q, k, v, scale, causal, kv_len=kv_len)
+    return oracle.fwd_chunked(q, k, v, scale, causal, query_chunk=2, key_chunk=3, kv_len=kv_len)
+
+
+@pytest.mark.parametrize("form", FORWARD_FORMS)
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("d,d_v", [(5, 9), (8, 3)])
+def test_value_width_matches_scipy_softmax(oracle_mod, form, causal, d, d_v):
+    B, H, nq, nk = 2, 2, 6, 10
+    q, k, v = rand((B, H, nq, d), 90), rand((B, H, nk, d), 91), rand((B, H, nk, d_v), 92)
+    kv_len = [10, 7]
+    o, lse = run_fwd_any(oracle_mod, form, q, k, v, 0.45, causal, kv_len)
+    assert o.shape == (B, H, nq, d_v)
+    for b in range(B):
+        for h in range(H):
+            s = _masked_scores(q[b, h], k[b, h], 0.45, kv_len[b], causal)
+            np.testing.assert_allclose(o[b, h], softmax(s, axis=1) @ v[b, h], rtol=1e-12, atol=1e-13)
+            np.testing.assert_allclose(lse[b, h], logsumexp(s, axis=1), rtol=1e-13)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_value_width_zero_query(oracle_mod, causal):
+    B, H, nq, nk, d, d_v = 1, 2, 5, 8, 4, 7
+    q, k, v = np.zeros((B, H, nq, d)), rand((B, H, nk, d), 93), rand((B, H, nk, d_v), 94)
+    o, _ = oracle_mod.fwd(q, k, v, 0.3, causal)
+    for i in range(nq):
+        n = min(i + 1, nk) if causal else nk
+        np.testing.assert_allclose(o[:, :, i], v[:, :, :n].mean(axis=2), rtol=1e-13, atol=1e-14)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_value_width_split_is_linear(oracle_mod, causal):
+    # Attention is linear in v with weights independent of it: splitting the
+    # value columns into two problems concatenates o and dv, leaves lse alone,
+    # and adds the query and key gradients of the two halves.
+    B, H, nq, nk, d, d_v = 2, 1, 7, 9, 4, 10
+    q, k, v, do = (rand((B, H, nq, d), 95), rand((B, H, nk, d), 96), rand((B, H, nk, d_v), 97),
+                   rand((B, H, nq, d_v), 98))
+    cut = 3
+    o, lse = oracle_mod.fwd(q, k, v, 0.8, causal)
+    o1, l1 = oracle_mod.fwd(q, k, v[..., :cut], 0.8, causal)
+    o2, l2 = oracle_mod.fwd(q, k, v[..., cut:], 0.8, causal)
+    np.testing.assert_allclose(o, np.concatenate([o1, o2], axis=-1), rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(lse, l1, rtol=1e-14)
+    np.testing.assert_allclose(lse, l2, rtol=1e-14)
+    dq, dk, dv = oracle_mod.bwd(q, k, v, do, 0.8, causal)
+    g1 = oracle_mod.bwd(q, k, v[..., :cut], do[..., :cut], 0.8, causal)
+    g2 = oracle_mod.bwd(q, k, v[..., cut:], do[..., cut:], 0.8, causal)
+    np.testing.assert_allclose(dq, g1[0] + g2[0], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dk, g1[1] + g2[1], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dv, np.concatenate([g1[2], g2[2]], axis=-1), rtol=1e-13, atol=1e-14)
+
+
+@pytest.mark.parametrize("d,d_v", [(3, 5), (5, 2)])
+def test_value_width_gradients_match_central_differences(oracle_mod, d, d_v):
+    B, H, nq, nk = 1, 2, 4, 6
+    q, k, v, do = (rand((B, H, nq, d), 99), rand((B, H, nk, d), 100), rand((B, H, nk, d_v), 101),
+                   rand((B, H, nq, d_v), 102))
+
+    def loss(q_, k_, v_):
+        o, _ = oracle_mod.fwd(q_, k_, v_, 0.7, True, kv_len=[5])
+        return float((o * do).sum())
+
+    grads = oracle_mod.bwd(q, k, v, do, 0.7, True, kv_len=[5])
+    h = 1e-6
+    for which, grad in enumerate(grads):
+        args = [q, k, v]
+        fd = np.zeros_like(args[which])
+        for idx in np.ndindex(fd.shape):
+            a_p, a_m = list(args), list(args)
+            a_p[which] = args[which].copy()
+            a_m[which] = args[which].copy()
+            a_p[which][idx] += h
+            a_m[which][idx] -= h
+            fd[idx] = (loss(*a_p) - loss(*a_m)) / (2 * h)
+        err = np.abs(fd - grad).max() / max(np.abs(grad).max(), 1e-300)
+        assert err < 1e-7, (which, err)
+
+
+def test_value_width_subsets_match_full(oracle_mod):
+    nq, nk, d, d_v = 13, 11, 3, 6
+    q, k, v, do = (rand((nq, d), 103), rand((nk, d), 104), rand((nk, d_v), 105), rand((nq, d_v), 106))
+    o, lse = oracle_mod.fwd(q[None, None], k[None, None], v[None, None], causal=True)
+    dq, dk, dv = oracle_mod.bwd(q[None, None], k[None, None], v[None, None], do[None, None], causal=True)
+    rows, keys = np.array([12, 0, 5]), np.array([10, 0, 4])
+    orow, lrow = oracle_mod.fwd_rows(q, k, v, rows, causal=True)
+    np.testing.assert_array_equal(orow, o[0, 0, rows])
+    np.testing.assert_array_equal(lrow, lse[0, 0, rows])
+    np.testing.assert_array_equal(oracle_mod.bwd_dq_rows(q, k, v, do, rows, causal=True), dq[0, 0, rows])
+    dkr, dvr = oracle_mod.bwd_dkdv_keys(q, k, v, do, keys, causal=True)
+    np.testing.assert_array_equal(dkr, dk[0, 0, keys])
+    np.testing.assert_array_equal(dvr, dv[0, 0, keys])
