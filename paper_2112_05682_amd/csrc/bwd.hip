@@ -189,10 +189,19 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   const int64_t q_begin = CAUSAL ? (k0 / Cfg::BQ) * Cfg::BQ : 0;
   const int n_iters = q_begin < p.n_q && k0 < n_kv ? (int)((p.n_q - q_begin + Cfg::BQ - 1) / Cfg::BQ) : 0;
 
-  u32x4 stage[Cfg::CPT];
-  float stage_f = 0.0f;
+  // Two register sets for the global -> LDS staging.  With a prefetch
+  // distance PF = 2 the tile two iterations ahead is loaded into one set while
+  // the other, loaded an iteration earlier, is written to LDS, so each tile's
+  // loads have two iterations to land; PF = 1 (where the registers do not
+  // allow two sets: float32, or two waves per SIMD) loads the next tile at the
+  // start of the iteration that writes it.
+  constexpr int PF = sizeof(T) == 2 && OCC == 1 ? 2 : 1;
+  u32x4 stage_a[Cfg::CPT], stage_b[Cfg::CPT];
+  float stage_fa = 0.0f, stage_fb = 0.0f;
   auto stage_base = [&](int buf) { return smem_raw + buf * Cfg::STAGE_BYTES; };
-  auto load_stage = [&](int64_t q0) {
+  auto load_stage = [&](auto set_tag, int64_t q0) __attribute__((always_inline)) {
+    u32x4 (&stage)[Cfg::CPT] = decltype(set_tag)::value ? stage_b : stage_a;
+    float& stage_f = decltype(set_tag)::value ? stage_fb : stage_fa;
 #pragma unroll
     for (int i = 0; i < Cfg::CPT; ++i) {
       const int chunk = tid + i * Cfg::NT;
@@ -216,7 +225,9 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       stage_f = tid < Cfg::BQ ? sinitg[q] : dpinitg[q];
     }
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](auto set_tag, int buf) __attribute__((always_inline)) {
+    const u32x4 (&stage)[Cfg::CPT] = decltype(set_tag)::value ? stage_b : stage_a;
+    const float stage_f = decltype(set_tag)::value ? stage_fb : stage_fa;
     T* base = reinterpret_cast<T*>(stage_base(buf));
 #pragma unroll
     for (int i = 0; i < Cfg::CPT; ++i) {
@@ -242,16 +253,14 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   const float cl2 = p.scale_log2;
 
   if (n_iters > 0) {
-    load_stage(q_begin);
-    store_stage(0);
+    load_stage(BoolC<false>{}, q_begin);
+    store_stage(BoolC<false>{}, 0);
   }
+  if (PF == 2 && n_iters > 1) load_stage(BoolC<true>{}, q_begin + Cfg::BQ);
   __syncthreads();
 
-  for (int it = 0; it < n_iters; ++it) {
+  auto compute = [&](int it) __attribute__((always_inline)) {
     const int64_t q0 = q_begin + (int64_t)it * Cfg::BQ;
-    const bool has_next = it + 1 < n_iters;
-    if (has_next) load_stage(q0 + Cfg::BQ);
-
     const T* qs_t = reinterpret_cast<const T*>(stage_base(it & 1));
     const T* dos_t = qs_t + Cfg::TILEQ;
     const float* sinit_s = reinterpret_cast<const float*>(stage_base(it & 1) + Cfg::STAGE_ELEMS * Cfg::E);
@@ -339,9 +348,31 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
         }
       }
     }
-
-    if (has_next) store_stage((it + 1) & 1);
-    __syncthreads();
+  };
+  // Iteration it computes tile it from LDS buffer it & 1 and writes tile
+  // it + 1 to the other LDS buffer.  PF = 2: set A holds even tiles, set B
+  // odd ones, and tile it + 2 is loaded into the set that held tile it;
+  // PF = 1: tile it + 1 is loaded into set A in this iteration.
+  if constexpr (PF == 2) {
+    auto step = [&](auto odd_tag, int it) __attribute__((always_inline)) {
+      constexpr bool ODD = decltype(odd_tag)::value;
+      if (it + 2 < n_iters) load_stage(BoolC<ODD>{}, q_begin + (int64_t)(it + 2) * Cfg::BQ);
+      compute(it);
+      if (it + 1 < n_iters) store_stage(BoolC<!ODD>{}, (it + 1) & 1);
+      __syncthreads();
+    };
+    for (int it = 0; it < n_iters; it += 2) {
+      step(BoolC<false>{}, it);
+      if (it + 1 < n_iters) step(BoolC<true>{}, it + 1);
+    }
+  } else {
+    for (int it = 0; it < n_iters; ++it) {
+      const bool has_next = it + 1 < n_iters;
+      if (has_next) load_stage(BoolC<false>{}, q_begin + (int64_t)(it + 1) * Cfg::BQ);
+      compute(it);
+      if (has_next) store_stage(BoolC<false>{}, (it + 1) & 1);
+      __syncthreads();
+    }
   }
 
   // Accumulators: lane (h, feature c), register r <-> key kw + c_row(r, h).
@@ -796,8 +827,14 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   if (CAUSAL && ke > q0 + BQ) ke = q0 + BQ;
   const int n_tiles = (int)((ke + BK - 1) / BK);
 
-  u32x4 stage[CPT];
-  auto load_stage = [&](int64_t k0) {
+  // Register sets for the global -> LDS staging (see the dK/dV kernel): with
+  // PF = 2 tile j + 2 is loaded while tile j + 1 is written to LDS.  Off
+  // (PF = 1): with the causal early exit of a tile the compiler moved the
+  // two sets to scratch memory and the kernel ran 5x slower.
+  constexpr int PF = 1;
+  u32x4 stage_a[CPT], stage_b[CPT];
+  auto load_stage = [&](auto set_tag, int64_t k0) __attribute__((always_inline)) {
+    u32x4 (&stage)[CPT] = decltype(set_tag)::value ? stage_b : stage_a;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       // The K tile's BK * CPRK chunks, then the V tile's.
@@ -811,7 +848,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
       stage[i] = kr < p.n_k ? ld16(src) : u32x4{0u, 0u, 0u, 0u};
     }
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](auto set_tag, int buf) __attribute__((always_inline)) {
+    const u32x4 (&stage)[CPT] = decltype(set_tag)::value ? stage_b : stage_a;
     T* base = smem + buf * (TILEK + TILEV);
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
@@ -828,9 +866,10 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   const float cl2 = p.scale_log2;
 
   if (n_tiles > 0) {
-    load_stage(0);
-    store_stage(0);
+    load_stage(BoolC<false>{}, 0);
+    store_stage(BoolC<false>{}, 0);
   }
+  if (PF == 2 && n_tiles > 1) load_stage(BoolC<true>{}, BK);
   __syncthreads();
 
   // Leading tiles that need no mask (all keys exist and, causal, precede the
@@ -919,16 +958,28 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
       }
     }
   };
-  auto step = [&](auto mask_tag, int it) {
-    const bool has_next = it + 1 < n_tiles;
-    if (has_next) load_stage((int64_t)(it + 1) * BK);
+  // Tile j is computed from LDS buffer j & 1 while tile j + 1 is written to
+  // the other one.  PF = 2: set A holds even tiles, set B odd ones, and tile
+  // j + 2 is loaded into the set that held tile j; PF = 1: tile j + 1 is
+  // loaded into set A in this iteration.
+  auto step = [&](auto mask_tag, auto odd_tag, int it) __attribute__((always_inline)) {
+    constexpr bool ODD = decltype(odd_tag)::value;
+    if constexpr (PF == 2) {
+      if (it + 2 < n_tiles) load_stage(BoolC<ODD>{}, (int64_t)(it + 2) * BK);
+    } else {
+      if (it + 1 < n_tiles) load_stage(BoolC<false>{}, (int64_t)(it + 1) * BK);
+    }
     tile(mask_tag, it);
-    if (has_next) store_stage((it + 1) & 1);
+    if (it + 1 < n_tiles) store_stage(BoolC<PF == 2 && !ODD>{}, (it + 1) & 1);
     __syncthreads();
   };
+  auto run = [&](auto mask_tag, int it) __attribute__((always_inline)) {
+    if (PF == 2 && (it & 1)) step(mask_tag, BoolC<true>{}, it);
+    else step(mask_tag, BoolC<false>{}, it);
+  };
   int it = 0;
-  for (; it < n_plain; ++it) step(BoolC<false>{}, it);
-  for (; it < n_tiles; ++it) step(BoolC<true>{}, it);
+  for (; it < n_plain; ++it) run(BoolC<false>{}, it);
+  for (; it < n_tiles; ++it) run(BoolC<true>{}, it);
 
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
