@@ -28,6 +28,15 @@
 #ifndef MEA_T64_DQ_W
 #define MEA_T64_DQ_W 1
 #endif
+// 16-query chunks of a query tile's softmax computed in the MFMA phase of the
+// two-group dK/dV kernel (the rest in its softmax phase), without and with the
+// causal mask.
+#ifndef MEA_T64_DKDV_W
+#define MEA_T64_DKDV_W 0
+#endif
+#ifndef MEA_T64_DKDV_WC
+#define MEA_T64_DKDV_WC 1
+#endif
 // Keys per lane whose softmax stages the dQ kernel issues together.
 #ifndef MEA_T64_DQ_G
 #define MEA_T64_DQ_G 16
@@ -119,6 +128,10 @@ struct DkdvTile {
   static constexpr int STAGE_ELEMS = TILEQ + TILEO;
   static constexpr int STAGE_BYTES = STAGE_ELEMS * E + 2 * BQ * 4;  // + accumulator initial values
   static constexpr int LDS_BYTES = 2 * STAGE_BYTES;
+  // With K_LDS the K fragments of every lane follow the two stages.
+  static constexpr int KSLOT_BYTES = NT * (D / 16) * 16;
+  static constexpr bool k_lds(int occ) { return E == 2 && D == 128 && occ == 2; }
+  static constexpr int lds_bytes(int occ) { return LDS_BYTES + (k_lds(occ) ? KSLOT_BYTES : 0); }
   static_assert(kBwdRowPad % BQ == 0, "query tiles must not pass the padded row count");
 };
 
@@ -151,16 +164,28 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   const T* __restrict__ vg = static_cast<const T*>(p.v) + head_base(p.sv, bh, p.heads);
 
   // K^T and V^T as B operands: lane (h, key c) holds row `key`, k = 16kc + 8h + s.
-  Frag<T> kf[KC], vf[KCV];
+  // K_LDS (16-bit, d = 128, two workgroups per CU): the K fragments wait in a
+  // per-lane LDS slot instead of registers (each lane reads back only what it
+  // wrote, so no barrier is needed), which frees 32 registers per lane.
+  constexpr bool K_LDS = Cfg::k_lds(OCC);
+  T* const kslot = reinterpret_cast<T*>(smem_raw + Cfg::LDS_BYTES) + 8 * tid;
+  Frag<T> kf[K_LDS ? 1 : KC], vf[KCV];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
+    Frag<T> f;
     if (key < p.n_k) {
-      kf[kc] = *reinterpret_cast<const Frag<T>*>(kg + key * p.sk.r + 16 * kc + 8 * h);
+      f = *reinterpret_cast<const Frag<T>*>(kg + key * p.sk.r + 16 * kc + 8 * h);
     } else {
 #pragma unroll
-      for (int s = 0; s < 8; ++s) kf[kc][s] = (T)0.0f;
+      for (int s = 0; s < 8; ++s) f[s] = (T)0.0f;
     }
+    if constexpr (K_LDS) *reinterpret_cast<Frag<T>*>(kslot + 8 * Cfg::NT * kc) = f;
+    else kf[kc] = f;
   }
+  auto kfrag = [&](int kc) __attribute__((always_inline)) {
+    if constexpr (K_LDS) return lds_frag<T>(kslot + 8 * Cfg::NT * kc);
+    else return kf[kc];
+  };
 #pragma unroll
   for (int kc = 0; kc < KCV; ++kc) {
     if (key < p.n_k) {
@@ -294,7 +319,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
         for (int qs = 0; qs < QS; ++qs) {
           if (kc < KC) {
             const Frag<T> a = lds_frag<T>(qs_t + (32 * qs + qrow) * RSQ + 16 * kc + 8 * h);
-            s[qs] = mma(a, kf[kc], s[qs]);
+            s[qs] = mma(a, kfrag(kc), s[qs]);
           }
           if (kc < KCV) {
             const Frag<T> g = lds_frag<T>(dos_t + (32 * qs + qrow) * RSO + 16 * kc + 8 * h);
@@ -415,6 +440,21 @@ constexpr int STAGEB = 2 * TILEB + RECB;      // 19456 bytes
 constexpr int UNITS = 2 * TILEB / 1024 + 1;   // 1 KiB copies per stage (18 + 1)
 static_assert(TILEB % 1024 == 0 && RECB == 1024, "stage layout");
 }  // namespace kvpp
+
+// MFMA-phase step order of the two-group dK/dV kernel when part of the
+// softmax moves into that phase (steps of two MFMAs): 0, 1 dV/dK of query
+// chunk 0 of the previous tile (dt = 0, 1); 2..5 S/dP of query sub-tile 0 of
+// this tile (kc = 0..3); 6..11 dV/dK of chunks 1..3; 12..15 S/dP of sub-tile 1.
+struct KvStep {
+  int dvdk;  // 1: dV/dK step (a = query chunk, b = dt); 0: S/dP (a = qs, b = kc)
+  int a, b;
+};
+__device__ constexpr KvStep kv_step_split(int g) {
+  return g < 2 ? KvStep{1, 0, g}
+       : g < 6 ? KvStep{0, 0, g - 2}
+       : g < 12 ? KvStep{1, 1 + (g - 6) / 2, (g - 6) % 2}
+                : KvStep{0, 1, g - 12};
+}
 
 template <typename T, bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
@@ -614,13 +654,14 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
     for (int qs = 0; qs < QS; ++qs)
       rec[qs] = *reinterpret_cast<const bf16x8*>(stage(i) + 2 * TILEB + 16 * (32 * qs + qrow));
   };
-  auto init_sdp = [&]() __attribute__((always_inline)) {
+  auto init_sdp_qs = [&](int qs) __attribute__((always_inline)) {
     const f32x16 zero = {};
+    s[qs] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rec[qs], bsel_s, zero, 0, 0, 0);
+    dp[qs] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rec[qs], bsel_d, zero, 0, 0, 0);
+  };
+  auto init_sdp = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int qs = 0; qs < QS; ++qs) {
-      s[qs] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rec[qs], bsel_s, zero, 0, 0, 0);
-      dp[qs] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(rec[qs], bsel_d, zero, 0, 0, 0);
-    }
+    for (int qs = 0; qs < QS; ++qs) init_sdp_qs(qs);
   };
   // Steps [G0, G1) with dV/dK of tile i_dv and S/dP of tile i_sd; the ring
   // already holds steps G0 .. G0 + AHEAD - 1.  S and dP are initialised just
@@ -648,6 +689,83 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // phase of tile i_dv).
   auto dvdk = [&](int i_dv) __attribute__((always_inline)) { run(IntC<0>{}, IntC<NS1>{}, i_dv, i_dv); };
 
+  // Softmax of the first W 16-query chunks of a tile in its MFMA phase (the
+  // steady-state MFMA phase then takes the step order of kv_step_split).  In
+  // that order S and dP of sub-tile 0 are final after step 5, and chunk c is
+  // written only after the dV/dK step that reads the old chunk c (steps 1 and
+  // 7); half-chunk u (four queries per lane) runs in step 7 + 4u / W, between
+  // the step's two MFMAs.  The first two steps are the same in both orders,
+  // so the softmax phase's ring prefetch serves either.
+  constexpr int W = CAUSAL ? MEA_T64_DKDV_WC : MEA_T64_DKDV_W;
+  static_assert(W >= 0 && W <= 2, "only chunks of query sub-tile 0 are final before the dV/dK steps");
+  static_assert(W == 0 || AHEAD <= 2, "the prefetched steps must be dV/dK steps of chunk 0");
+  static_assert(NS1 == 8 && NS2 == 8 && QS == 2 && NDT == 2 && KC == 4, "step table shape");
+  // P = 2^(c S) and dS = P dP for four queries of chunk c (half hf), masked
+  // like the softmax phase, rounded and packed two per dword.
+  auto pd_half = [&](int cidx, int hf, bool need_mask, int key_rel, u32x2& pw, u32x2& dw)
+      __attribute__((always_inline)) {
+    const int qs = cidx >> 1;
+    float pr[4], ds[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 8 * (cidx & 1) + 4 * hf + e;
+      float x = fast_exp2(s[qs][r] * cl2);
+      if (need_mask && key_rel > 32 * qs + permuted_row(r, h)) x = 0.0f;
+      pr[e] = x;
+      ds[e] = x * dp[qs][r];
+    }
+    pw = u32x2{pack2<T>(pr[0], pr[1]), pack2<T>(pr[2], pr[3])};
+    dw = u32x2{pack2<T>(ds[0], ds[1]), pack2<T>(ds[2], ds[3])};
+  };
+  auto run_split = [&](int i_dv, int i_sd, bool need_mask, int key_rel) __attribute__((always_inline)) {
+    constexpr int NSS = NS1 + NS2;
+    auto fetch_split = [&](int g) __attribute__((always_inline)) {
+      const int slot = g % (AHEAD + 1);
+      const KvStep k = kv_step_split(g);
+      if (k.dvdk) {
+        const unsigned char* st = stage(i_dv);
+        rx[slot] = lds_col_frag<T>(reinterpret_cast<const T*>(st + TILEB), RSB / 2, 16 * k.a, 32 * k.b, lane);
+        ry[slot] = lds_col_frag<T>(reinterpret_cast<const T*>(st), RSB / 2, 16 * k.a, 32 * k.b, lane);
+      } else {
+        const unsigned char* st = stage(i_sd);
+        const int off = (32 * k.a + qrow) * (RSB / 2) + 16 * k.b + 8 * h;
+        rx[slot] = lds_frag<T>(reinterpret_cast<const T*>(st) + off);
+        ry[slot] = lds_frag<T>(reinterpret_cast<const T*>(st + TILEB) + off);
+      }
+    };
+    u32x2 pw0 = {0u, 0u}, dw0 = {0u, 0u};
+#pragma unroll
+    for (int g = 0; g < NSS; ++g) {
+      if (g + AHEAD < NSS) fetch_split(g + AHEAD);
+      if (g == 2) init_sdp_qs(0);
+      if (g == 12) init_sdp_qs(1);
+      const int slot = g % (AHEAD + 1);
+      const KvStep k = kv_step_split(g);
+      if (k.dvdk) dv[k.b] = mma(pa[k.a], rx[slot], dv[k.b]);
+      else s[k.a] = mma(rx[slot], kf[k.b], s[k.a]);
+      int u = -1;
+      if constexpr (W > 0) {
+#pragma unroll
+        for (int uu = 0; uu < 2 * W; ++uu)
+          if (g == 7 + (4 * uu) / W) u = uu;
+      }
+      if (k.dvdk) dk[k.b] = mma(da[k.a], ry[slot], dk[k.b]);
+      else dp[k.a] = mma(ry[slot], vf[k.b], dp[k.a]);
+      if (u >= 0) {
+        u32x2 pw, dw;
+        pd_half(u >> 1, u & 1, need_mask, key_rel, pw, dw);
+        if ((u & 1) == 0) {
+          pw0 = pw;
+          dw0 = dw;
+        } else {
+          pa[u >> 1] = __builtin_bit_cast(Frag<T>, u32x4{pw0[0], pw0[1], pw[0], pw[1]});
+          da[u >> 1] = __builtin_bit_cast(Frag<T>, u32x4{dw0[0], dw0[1], dw[0], dw[1]});
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
   // One iteration per query tile.  MODE 0: the tile is not active for this
   // wave (causal: all its queries precede the wave's keys), only the copies
   // and barriers run; MODE 1: the wave's first active tile (S/dP only); MODE 2:
@@ -657,6 +775,8 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   auto iteration = [&](auto mode_tag, int i) __attribute__((always_inline)) {
     constexpr int MODE = decltype(mode_tag)::value;
     const int64_t q0 = q_begin + (int64_t)i * BQ;
+    const bool need_mask = CAUSAL && q0 < kw + 31;
+    const int key_rel = (int)(key - q0);  // key minus the tile's first query
     // ---- MFMA phase (S and dP are free: the last softmax phase converted them)
     mfma_phase_priority();
     if constexpr (MODE == 1) {
@@ -666,7 +786,8 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
       run(IntC<NS1>{}, IntC<NS>{}, i, i);
     } else if constexpr (MODE == 2) {
       read_rec(i);
-      run(IntC<0>{}, IntC<NS>{}, i - 1, i);
+      if constexpr (W > 0) run_split(i - 1, i, need_mask, key_rel);
+      else run(IntC<0>{}, IntC<NS>{}, i - 1, i);
     }
     // Group 1: tile i + 1 must land before this barrier (its share of tile
     // i + 2 may still run).
@@ -675,19 +796,21 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
     // ---- VALU phase
     valu_phase_priority();
     if constexpr (MODE != 0) {
-      const bool need_mask = CAUSAL && q0 < kw + 31;
-      const int key_rel = (int)(key - q0);  // key minus the tile's first query
+      // Chunks C0 .. NQC - 1 (the MFMA phase of a steady-state tile did the
+      // first W).
+      constexpr int C0 = MODE == 2 ? W : 0;
 #pragma unroll
       for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
+          if (2 * qs + r / 8 < C0) continue;
           float pr = fast_exp2(s[qs][r] * cl2);
           if (need_mask && key_rel > 32 * qs + permuted_row(r, h)) pr = 0.0f;
           s[qs][r] = pr;
           dp[qs][r] = pr * dp[qs][r];
         }
 #pragma unroll
-      for (int qc = 0; qc < NQC; ++qc) {
+      for (int qc = C0; qc < NQC; ++qc) {
         float tp[8], td[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -1446,8 +1569,15 @@ template <> struct BwdShape<__bf16, 64> {
   static constexpr int QS = MEA_T64_DKDV_QS, KV_OCC = MEA_T64_DKDV_OCC;
   static constexpr int QT = MEA_T64_DQ_QT, BK = MEA_T64_DQ_BK, Q_OCC = MEA_T64_DQ_OCC;
 };
+// d = 128, 16-bit: dK/dV at one workgroup per CU (the K, V, dK and dV
+// registers of 32 keys leave no room for a second); dQ with 32-key tiles fits
+// two workgroups per CU, whose waves overlap each other's MFMA, softmax and
+// LDS work (37 % less time than 64-key tiles at one workgroup per CU).
+#ifndef MEA_T128_DKDV_OCC
+#define MEA_T128_DKDV_OCC 2
+#endif
 template <> struct BwdShape<__bf16, 128> {
-  static constexpr int QS = 1, KV_OCC = 1, QT = 1, BK = 64, Q_OCC = 1;
+  static constexpr int QS = 1, KV_OCC = MEA_T128_DKDV_OCC, QT = 1, BK = 32, Q_OCC = 2;
 };
 template <> struct BwdShape<_Float16, 64> : BwdShape<__bf16, 64> {};
 template <> struct BwdShape<_Float16, 128> : BwdShape<__bf16, 128> {};
@@ -1480,7 +1610,7 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
                           dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(kvpp::NW * 64), args, 0, stream);
     } else {
       e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, DV, S::QS, S::KV_OCC, CAUSAL>),
-                          dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::LDS_BYTES, stream);
+                          dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::lds_bytes(S::KV_OCC), stream);
     }
     if (e != hipSuccess || !p.dq) return e;
   }
