@@ -298,10 +298,12 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "heads": w.heads, "n_q": w.n_q,
-                   "n_k": w.n_k, "d": w.d, "causal": w.causal, "inputs": "N(0,1) bf16",
+                   "n_k": w.n_k, "d": w.d, "causal": w.causal,
+                   "inputs": "N(0,%g^2) %s%s" % (w.std, w.dtype,
+                                                 ", q and k x%g" % w.qk_mult if w.qk_mult != 1.0 else ""),
                    "accumulation": "fp32"},
         "frac_of_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
         "fwd_tflops": round(kernels["fwd"]["tflops"], 2),
