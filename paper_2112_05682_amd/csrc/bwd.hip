@@ -693,9 +693,10 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // steady-state MFMA phase then takes the step order of kv_step_split).  In
   // that order S and dP of sub-tile 0 are final after step 5, and chunk c is
   // written only after the dV/dK step that reads the old chunk c (steps 1 and
-  // 7); half-chunk u (four queries per lane) runs in step 7 + 4u / W, between
-  // the step's two MFMAs.  The first two steps are the same in both orders,
-  // so the softmax phase's ring prefetch serves either.
+  // 7); half-chunk u (four queries per lane) is issued in step 7 + 4u / W,
+  // after the step's two MFMAs, and runs while they execute.  The first two
+  // steps are the same in both orders, so the softmax phase's ring prefetch
+  // serves either.
   constexpr int W = CAUSAL ? MEA_T64_DKDV_WC : MEA_T64_DKDV_W;
   static_assert(W >= 0 && W <= 2, "only chunks of query sub-tile 0 are final before the dV/dK steps");
   static_assert(W == 0 || AHEAD <= 2, "the prefetched steps must be dV/dK steps of chunk 0");
