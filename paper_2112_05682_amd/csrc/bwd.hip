@@ -131,7 +131,17 @@ struct DkdvTile {
   // With K_LDS the K fragments of every lane follow the two stages.
   static constexpr int KSLOT_BYTES = NT * (D / 16) * 16;
   static constexpr bool k_lds(int occ) { return E == 2 && D == 128 && occ == 2; }
-  static constexpr int lds_bytes(int occ) { return LDS_BYTES + (k_lds(occ) ? KSLOT_BYTES : 0); }
+  // Asynchronous stage copies (K_LDS with dO in the input dtype): each tile is
+  // a whole number of 1 KiB copy units, one 16-byte slot per row chunk plus
+  // one for the row pad.
+  static constexpr bool async(int occ, bool same_out) { return k_lds(occ) && same_out; }
+  static constexpr int UQ = (BQ * (CPRQ + 1) * 16 + 1023) / 1024;
+  static constexpr int UO = (BQ * (CPRO + 1) * 16 + 1023) / 1024;
+  static constexpr int ASTAGE_BYTES = (UQ + UO) * 1024 + 2 * BQ * 4;
+  static constexpr int stage_bytes(bool as) { return as ? ASTAGE_BYTES : STAGE_BYTES; }
+  static constexpr int lds_bytes(int occ, bool same_out) {
+    return 2 * stage_bytes(async(occ, same_out)) + (k_lds(occ) ? KSLOT_BYTES : 0);
+  }
   static_assert(kBwdRowPad % BQ == 0, "query tiles must not pass the padded row count");
 };
 
@@ -168,7 +178,13 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   // per-lane LDS slot instead of registers (each lane reads back only what it
   // wrote, so no barrier is needed), which frees 32 registers per lane.
   constexpr bool K_LDS = Cfg::k_lds(OCC);
-  T* const kslot = reinterpret_cast<T*>(smem_raw + Cfg::LDS_BYTES) + 8 * tid;
+  // ASYNC: the Q and dO tiles go global -> LDS by asynchronous copies instead
+  // of through registers (only where dO needs no conversion).
+  constexpr bool ASYNC = Cfg::async(OCC, __is_same(T, TO));
+  constexpr int STAGE_B = Cfg::stage_bytes(ASYNC);
+  constexpr int TILEQ_L = ASYNC ? Cfg::UQ * 1024 / Cfg::E : Cfg::TILEQ;  // dO tile offset (elements)
+  constexpr int INIT_OFF = ASYNC ? (Cfg::UQ + Cfg::UO) * 1024 : Cfg::STAGE_ELEMS * Cfg::E;
+  T* const kslot = reinterpret_cast<T*>(smem_raw + 2 * STAGE_B) + 8 * tid;
   Frag<T> kf[K_LDS ? 1 : KC], vf[KCV];
 #pragma unroll
   for (int kc = 0; kc < KC; ++kc) {
@@ -223,7 +239,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   constexpr int PF = sizeof(T) == 2 && OCC == 1 ? 2 : 1;
   u32x4 stage_a[Cfg::CPT], stage_b[Cfg::CPT];
   float stage_fa = 0.0f, stage_fb = 0.0f;
-  auto stage_base = [&](int buf) { return smem_raw + buf * Cfg::STAGE_BYTES; };
+  auto stage_base = [&](int buf) { return smem_raw + buf * STAGE_B; };
   auto load_stage = [&](auto set_tag, int64_t q0) __attribute__((always_inline)) {
     u32x4 (&stage)[Cfg::CPT] = decltype(set_tag)::value ? stage_b : stage_a;
     float& stage_f = decltype(set_tag)::value ? stage_fb : stage_fa;
@@ -274,21 +290,61 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
     }
   };
 
+  // ASYNC copies of a stage: unit u of the Q tile (u < UQ) or of the dO tile
+  // covers slots 64 u + lane; slot s is row s / (CPR + 1), chunk s % (CPR + 1),
+  // the last chunk of a row (its pad) a repeat of the one before.  Slots past
+  // the tile's rows and rows past n_q copy the last valid row (finite values;
+  // those queries start at -inf, so their weights are 0).  Wave w issues units
+  // w, w + 4, ...; the per-row initial values go through a register as above.
+  auto copy_stage = [&](int64_t q0, int buf) __attribute__((always_inline)) {
+    for (int u = __builtin_amdgcn_readfirstlane(wave); u < Cfg::UQ + Cfg::UO; u += 4) {
+      const bool is_o = u >= Cfg::UQ;
+      const int uu = is_o ? u - Cfg::UQ : u;
+      const int cpr = is_o ? Cfg::CPRO : Cfg::CPRQ;
+      const int slot = 64 * uu + lane;
+      int row = slot / (cpr + 1), ch = slot % (cpr + 1);
+      if (ch == cpr) ch = cpr - 1;
+      if (row > Cfg::BQ - 1) row = Cfg::BQ - 1;
+      int64_t q = q0 + row;
+      if (q > p.n_q - 1) q = p.n_q - 1;
+      const T* src = (is_o ? reinterpret_cast<const T*>(dog) + q * p.sdo.r : qg + q * p.sq.r) + ch * (16 / Cfg::E);
+      const unsigned dst = __builtin_amdgcn_readfirstlane(
+          lds_addr(stage_base(buf) + (is_o ? Cfg::UQ * 1024 : 0) + 1024 * uu));
+      copy_to_lds16(src, dst);
+    }
+    if (tid < 2 * Cfg::BQ) {
+      const int64_t q = q0 + (tid % Cfg::BQ);
+      stage_fa = tid < Cfg::BQ ? sinitg[q] : dpinitg[q];
+    }
+  };
+  // Wait for this wave's copies and loads, then write the initial values.
+  auto finish_stage = [&](int buf) __attribute__((always_inline)) {
+    wait_global_loads();
+    if (tid < 2 * Cfg::BQ) reinterpret_cast<float*>(stage_base(buf) + INIT_OFF)[tid] = stage_fa;
+  };
+
   const int qrow = perm32(c);
   const float cl2 = p.scale_log2;
 
-  if (n_iters > 0) {
-    load_stage(BoolC<false>{}, q_begin);
-    store_stage(BoolC<false>{}, 0);
+  if constexpr (ASYNC) {
+    if (n_iters > 0) {
+      copy_stage(q_begin, 0);
+      finish_stage(0);
+    }
+  } else {
+    if (n_iters > 0) {
+      load_stage(BoolC<false>{}, q_begin);
+      store_stage(BoolC<false>{}, 0);
+    }
+    if (PF == 2 && n_iters > 1) load_stage(BoolC<true>{}, q_begin + Cfg::BQ);
   }
-  if (PF == 2 && n_iters > 1) load_stage(BoolC<true>{}, q_begin + Cfg::BQ);
   __syncthreads();
 
   auto compute = [&](int it) __attribute__((always_inline)) {
     const int64_t q0 = q_begin + (int64_t)it * Cfg::BQ;
     const T* qs_t = reinterpret_cast<const T*>(stage_base(it & 1));
-    const T* dos_t = qs_t + Cfg::TILEQ;
-    const float* sinit_s = reinterpret_cast<const float*>(stage_base(it & 1) + Cfg::STAGE_ELEMS * Cfg::E);
+    const T* dos_t = qs_t + TILEQ_L;
+    const float* sinit_s = reinterpret_cast<const float*>(stage_base(it & 1) + INIT_OFF);
     const float* dpinit_s = sinit_s + Cfg::BQ;
 
     // Nothing to do when every query of the tile precedes this wave's keys.
@@ -393,9 +449,15 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   } else {
     for (int it = 0; it < n_iters; ++it) {
       const bool has_next = it + 1 < n_iters;
-      if (has_next) load_stage(BoolC<false>{}, q_begin + (int64_t)(it + 1) * Cfg::BQ);
-      compute(it);
-      if (has_next) store_stage(BoolC<false>{}, (it + 1) & 1);
+      if constexpr (ASYNC) {
+        if (has_next) copy_stage(q_begin + (int64_t)(it + 1) * Cfg::BQ, (it + 1) & 1);
+        compute(it);
+        if (has_next) finish_stage((it + 1) & 1);
+      } else {
+        if (has_next) load_stage(BoolC<false>{}, q_begin + (int64_t)(it + 1) * Cfg::BQ);
+        compute(it);
+        if (has_next) store_stage(BoolC<false>{}, (it + 1) & 1);
+      }
       __syncthreads();
     }
   }
@@ -1611,7 +1673,8 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
                           dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(kvpp::NW * 64), args, 0, stream);
     } else {
       e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, DV, S::QS, S::KV_OCC, CAUSAL>),
-                          dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args, Dk::lds_bytes(S::KV_OCC), stream);
+                          dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args,
+                          Dk::lds_bytes(S::KV_OCC, __is_same(T, TO)), stream);
     }
     if (e != hipSuccess || !p.dq) return e;
   }
