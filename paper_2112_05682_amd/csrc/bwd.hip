@@ -1632,10 +1632,11 @@ template <> struct BwdShape<__bf16, 64> {
   static constexpr int QS = MEA_T64_DKDV_QS, KV_OCC = MEA_T64_DKDV_OCC;
   static constexpr int QT = MEA_T64_DQ_QT, BK = MEA_T64_DQ_BK, Q_OCC = MEA_T64_DQ_OCC;
 };
-// d = 128, 16-bit: dK/dV at one workgroup per CU (the K, V, dK and dV
-// registers of 32 keys leave no room for a second); dQ with 32-key tiles fits
-// two workgroups per CU, whose waves overlap each other's MFMA, softmax and
-// LDS work (37 % less time than 64-key tiles at one workgroup per CU).
+// d = 128, 16-bit: two workgroups per CU, whose waves overlap each other's
+// MFMA, softmax and LDS work.  dK/dV fits them by keeping each lane's K
+// fragments in LDS (K, V, dK and dV of 32 keys in registers would not fit;
+// 25 % less time than one workgroup per CU), dQ by using 32-key tiles (37 %
+// less time than 64-key tiles at one workgroup per CU).
 #ifndef MEA_T128_DKDV_OCC
 #define MEA_T128_DKDV_OCC 2
 #endif
