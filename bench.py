@@ -114,8 +114,8 @@ def bench_key_padding(dev, calls: int = 5, warmup: int = 2):
     kl = torch.tensor(lens, dtype=torch.int32, device=dev)
 
     def run(kv_len):
-        o, lse = attention_fwd(x["q"], x["k"], x["v"], kv_len=kv_len)
-        attention_bwd(x["q"], x["k"], x["v"], o, lse, x["do"], kv_len=kv_len)
+        o, lse, o_lo = attention_fwd(x["q"], x["k"], x["v"], kv_len=kv_len, residual=True)
+        attention_bwd(x["q"], x["k"], x["v"], o, lse, x["do"], kv_len=kv_len, o_lo=o_lo)
 
     out = {}
     for name, kv_len, keys in (("padded", kl, sum(lens)), ("full", None, B * n)):
@@ -209,11 +209,11 @@ def main() -> int:
         # ev: four events recorded before the forward, after it, after the
         # dK/dV call and after the dQ call.
         ev[0].record()
-        o, lse = attention_fwd(q, k, v, causal=w.causal)
+        o, lse, o_lo = attention_fwd(q, k, v, causal=w.causal, residual=True)
         ev[1].record()
-        attention_bwd(q, k, v, o, lse, do, causal=w.causal, need_dq=False)
+        attention_bwd(q, k, v, o, lse, do, causal=w.causal, need_dq=False, o_lo=o_lo)
         ev[2].record()
-        attention_bwd(q, k, v, o, lse, do, causal=w.causal, need_dkdv=False)
+        attention_bwd(q, k, v, o, lse, do, causal=w.causal, need_dkdv=False, o_lo=o_lo)
         ev[3].record()
 
     def events():
@@ -228,12 +228,12 @@ def main() -> int:
     # kept alive, from torch's allocator.
     torch.cuda.reset_peak_memory_stats(dev)
     base_alloc = torch.cuda.memory_allocated(dev)
-    o_, lse_ = attention_fwd(q, k, v, causal=w.causal)
-    grads_ = attention_bwd(q, k, v, o_, lse_, do, causal=w.causal)
+    o_, lse_, olo_ = attention_fwd(q, k, v, causal=w.causal, residual=True)
+    grads_ = attention_bwd(q, k, v, o_, lse_, do, causal=w.causal, o_lo=olo_)
     torch.cuda.synchronize()
     peak_extra = torch.cuda.max_memory_allocated(dev) - base_alloc
     out_bytes = sum(t.numel() * t.element_size() for t in (o_, *grads_))  # o, dq, dk, dv
-    del o_, lse_, grads_
+    del o_, lse_, olo_, grads_
 
     # The timed steps are enqueued back to back (no synchronisation inside the
     # timed region, so the GPU never waits for the host between kernels); the

@@ -22,8 +22,8 @@
  *     mea_problem.strides (features always contiguous), which covers the
  *     paper's [n, heads, d] layout and views into a packed QKV projection;
  *     lse is always contiguous [B, H, n_q] float32.
- *   - Pointers: q, k, v, o, do, dq, dk, dv, lse and workspace are DEVICE
- *     pointers, 16-byte aligned.  The mea_problem pointer is a HOST pointer.
+ *   - Pointers: q, k, v, o, o_lo, do, dq, dk, dv, lse and workspace are
+ *     DEVICE pointers, 16-byte aligned.  The mea_problem pointer is a HOST pointer.
  *   - Ownership: the caller allocates every buffer, including the workspace.
  *     The library allocates no device memory, keeps no mutable global state
  *     and never synchronises: work is enqueued on `stream` (0 = the null
@@ -127,11 +127,20 @@ mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes)
  * tile with the running max / numerator / denominator; writes o (in dtype, or
  * float32 with out_f32) and,
  * if lse != NULL, lse_i = max_j s_ij + ln sum_j e^{s_ij - max_j s_ij} in
- * natural-log units (float32), which the backward needs.  `workspace` may be
- * NULL only when the required size is 0. */
+ * natural-log units (float32), which the backward needs.
+ * o_lo (DEVICE pointer or NULL; must be NULL when o is float32): for a 16-bit
+ * o, the rounding residual of o in the same dtype, o_lo = round(o_f32 - o)
+ * with o_f32 the float32 quotient before rounding, contiguous
+ * [B, H, n_q, d_v] whatever o's strides.  o + o_lo carries about 16
+ * significant bits, and the backward forms D_i = do_i . (o_i + o_lo_i) from
+ * it: D enters dS_ij = w_ij (do_i . v_j - D_i), which is a small difference
+ * of two O(1) numbers wherever the softmax saturates (large logits, the
+ * numerical-stability setting of Section 3), so o's own 2^-9 rounding would
+ * dominate the true dS there.  Caller-owned, O(n d) like o.
+ * `workspace` may be NULL only when the required size is 0. */
 mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
-                             const void* v, void* o, float* lse, void* workspace,
-                             size_t workspace_bytes, hipStream_t stream);
+                             const void* v, void* o, float* lse, void* o_lo,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Backward (Section 5.2, recompute instead of storing the n_q x n_k matrix):
  * given the forward's o and lse and the upstream gradient do (both in the
@@ -140,13 +149,18 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
  *   dk_j = scale sum_i w_ij (do_i . v_j - D_i) q_i,
  *   dq_i = scale sum_j w_ij (do_i . v_j - D_i) k_j,
  * with D_i = do_i . o_i and w_ij = exp(s_ij - lse_i) recomputed per tile.
+ * o_lo is the forward's residual of a 16-bit o (see mea_attention_fwd), or
+ * NULL: then D_i uses the rounded o alone, which is accurate to the 16-bit
+ * tolerance for ordinary inputs but not where the softmax saturates (with
+ * logits of order 1e3, gradients can be off by more than 2e-2 of their
+ * largest element).  It must be NULL when o is float32.
  * All inputs must come from one mea_attention_fwd call on the same problem.
  * dq may be NULL to skip dQ; dk and dv may be NULL together to skip dK and dV
  * (at least one of the two groups must be requested). */
 mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
-                             const void* v, const void* o, const void* d_o,
-                             const float* lse, void* dq, void* dk, void* dv,
-                             void* workspace, size_t workspace_bytes,
+                             const void* v, const void* o, const void* o_lo,
+                             const void* d_o, const float* lse, void* dq, void* dk,
+                             void* dv, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
 /* Static description of a status code (never NULL). */

@@ -83,8 +83,8 @@ def load(path: str = LIB_PATH):
     prob = ctypes.POINTER(MeaProblem)
     lib.mea_attention_fwd_workspace_size.argtypes = [prob, ctypes.POINTER(sz)]
     lib.mea_attention_bwd_workspace_size.argtypes = [prob, ctypes.POINTER(sz)]
-    lib.mea_attention_fwd.argtypes = [prob, vp, vp, vp, vp, vp, vp, sz, vp]
-    lib.mea_attention_bwd.argtypes = [prob, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.mea_attention_fwd.argtypes = [prob, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.mea_attention_bwd.argtypes = [prob, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for name in ("mea_attention_fwd_workspace_size", "mea_attention_bwd_workspace_size",
                  "mea_attention_fwd", "mea_attention_bwd"):
         getattr(lib, name).restype = ctypes.c_int
@@ -140,13 +140,13 @@ def bwd_workspace_size(p: MeaProblem) -> int:
     return int(out.value)
 
 
-def fwd(p: MeaProblem, q, k, v, o, lse, workspace, workspace_bytes, stream) -> int:
-    """Raw call; pointers are ints (device addresses), returns the status."""
-    return load().mea_attention_fwd(ctypes.byref(p), q, k, v, o, lse, workspace,
+def fwd(p: MeaProblem, q, k, v, o, lse, o_lo, workspace, workspace_bytes, stream) -> int:
+    """Raw call; pointers are ints (device addresses) or None, returns the status."""
+    return load().mea_attention_fwd(ctypes.byref(p), q, k, v, o, lse, o_lo, workspace,
                                     workspace_bytes, stream)
 
 
-def bwd(p: MeaProblem, q, k, v, o, d_o, lse, dq, dk, dv, workspace, workspace_bytes,
+def bwd(p: MeaProblem, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, workspace, workspace_bytes,
         stream) -> int:
-    return load().mea_attention_bwd(ctypes.byref(p), q, k, v, o, d_o, lse, dq, dk, dv,
+    return load().mea_attention_bwd(ctypes.byref(p), q, k, v, o, o_lo, d_o, lse, dq, dk, dv,
                                     workspace, workspace_bytes, stream)

@@ -81,11 +81,16 @@ def bwd_workspace_bytes(q, k, causal=False, scale=None) -> int:
 
 def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: bool = False,
                   scale: float | None = None, need_lse: bool = True, out=None,
-                  out_dtype: torch.dtype | None = None, kv_len: torch.Tensor | None = None):
+                  out_dtype: torch.dtype | None = None, kv_len: torch.Tensor | None = None,
+                  residual: bool = False):
     """Returns ``(o, lse)``; ``lse`` is float32 ``[B, H, n_q]`` (None if not needed).
     ``out_dtype`` is q's dtype (default) or torch.float32.  ``kv_len`` (int32
     ``[B]`` on the GPU) masks keys ``j >= kv_len[b]`` of batch b (key padding);
-    a row with no visible key gets o = 0 and lse = -inf."""
+    a row with no visible key gets o = 0 and lse = -inf.  With ``residual``
+    the call returns ``(o, lse, o_lo)``: for a 16-bit o, ``o_lo`` is o's
+    rounding residual (contiguous, o's dtype), which the backward uses to form
+    D_i = do_i . o_i accurately where the softmax saturates; None for a
+    float32 o."""
     if k.shape[:3] != v.shape[:3] or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
         raise ValueError("shape mismatch: q %s k %s v %s" % (tuple(q.shape), tuple(k.shape),
                                                               tuple(v.shape)))
@@ -101,22 +106,27 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, causal: boo
     p = _problem(q, k, causal, scale, out_dtype == torch.float32,
                  {"q": q, "k": k, "v": v, "o": o}, kv_len)
     lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device) if need_lse else None
+    o_lo = torch.empty(o_shape, dtype=out_dtype, device=q.device) \
+        if residual and out_dtype != torch.float32 else None
     ws_bytes = _lib.fwd_workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device) if ws_bytes else None
     _lib.check("mea_attention_fwd", _lib.fwd(
         p, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
         lse.data_ptr() if lse is not None else None,
+        o_lo.data_ptr() if o_lo is not None else None,
         ws.data_ptr() if ws is not None else None, ws_bytes, _stream(q.device)))
-    return o, lse
+    return (o, lse, o_lo) if residual else (o, lse)
 
 
 def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None = None,
                   need_dq: bool = True, need_dkdv: bool = True, out=None,
-                  kv_len: torch.Tensor | None = None):
+                  kv_len: torch.Tensor | None = None, o_lo: torch.Tensor | None = None):
     """Returns ``(dq, dk, dv)`` for the upstream gradient ``do``; a gradient that
     is not needed is returned as None and its kernel is not run.  ``out`` may
     give the (dq, dk, dv) tensors to write (any may be None: allocated).
-    ``kv_len`` must be the forward's; masked keys get zero dk and dv rows."""
+    ``kv_len`` must be the forward's; masked keys get zero dk and dv rows.
+    ``o_lo``: the forward's residual of a 16-bit o (``attention_fwd(...,
+    residual=True)``); without it D_i is formed from the rounded o alone."""
     _check_tensors(("q", "k", "v"), (q, k, v), q.dtype, q.device)
     if o.dtype not in (q.dtype, torch.float32):
         raise TypeError("o must have q's dtype or float32")
@@ -125,6 +135,10 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
     o_shape = tuple(q.shape[:3]) + (v.shape[3],)
     if tuple(o.shape) != o_shape or tuple(do.shape) != o_shape or tuple(lse.shape) != tuple(q.shape[:3]):
         raise ValueError("o, do must be [B, H, n_q, d_v] and lse [B, H, n_q]")
+    if o_lo is not None:
+        _check_tensors(("o_lo",), (o_lo,), o.dtype, q.device)
+        if tuple(o_lo.shape) != o_shape or not o_lo.is_contiguous():
+            raise ValueError("o_lo must be a contiguous [B, H, n_q, d_v] tensor")
     if not (need_dq or need_dkdv):
         raise ValueError("nothing to compute")
     given = out if out is not None else (None, None, None)
@@ -144,7 +158,8 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
     ws_bytes = _lib.bwd_workspace_size(p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     _lib.check("mea_attention_bwd", _lib.bwd(
-        p, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), do.data_ptr(),
+        p, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+        o_lo.data_ptr() if o_lo is not None else None, do.data_ptr(),
         lse.data_ptr(), dq.data_ptr() if need_dq else None,
         dk.data_ptr() if need_dkdv else None, dv.data_ptr() if need_dkdv else None,
         ws.data_ptr(), ws_bytes,
@@ -153,14 +168,15 @@ def attention_bwd(q, k, v, o, lse, do, causal: bool = False, scale: float | None
 
 
 class MemoryEfficientAttention(torch.autograd.Function):
-    """Autograd wrapper: saves only q, k, v, o and the O(n) lse."""
+    """Autograd wrapper: saves q, k, v, o, the O(n) lse and, for a 16-bit o,
+    o's rounding residual (O(n d), like o)."""
 
     @staticmethod
     def forward(ctx, q, k, v, causal=False, scale=None, out_dtype=None, kv_len=None):
         q, k, v = (_feature_contiguous(t) for t in (q, k, v))
-        o, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out_dtype=out_dtype,
-                               kv_len=kv_len)
-        ctx.save_for_backward(q, k, v, o, lse)
+        o, lse, o_lo = attention_fwd(q, k, v, causal, scale, need_lse=True, out_dtype=out_dtype,
+                                     kv_len=kv_len, residual=True)
+        ctx.save_for_backward(q, k, v, o, lse, o_lo)
         ctx.causal = causal
         ctx.scale = scale
         ctx.kv_len = kv_len
@@ -168,9 +184,9 @@ class MemoryEfficientAttention(torch.autograd.Function):
 
     @staticmethod
     def backward(ctx, do):
-        q, k, v, o, lse = ctx.saved_tensors
+        q, k, v, o, lse, o_lo = ctx.saved_tensors
         dq, dk, dv = attention_bwd(q, k, v, o, lse, _feature_contiguous(do.to(o.dtype)), ctx.causal,
-                                   ctx.scale, kv_len=ctx.kv_len)
+                                   ctx.scale, kv_len=ctx.kv_len, o_lo=o_lo)
         return dq, dk, dv, None, None, None, None
 
 
@@ -189,7 +205,8 @@ class PackedQKVAttention(torch.autograd.Function):
     shape ``[B, n, 3, H, d]``: q, k and v are read as strided views of it, the
     output is ``[B, n, H, d]`` (so ``reshape(B, n, H * d)`` is free) and the
     gradient is written as one packed ``[B, n, 3, H, d]`` tensor -- neither
-    direction copies or transposes.  Saves qkv, o and the O(n) lse."""
+    direction copies or transposes.  Saves qkv, o, the O(n) lse and o's
+    rounding residual."""
 
     @staticmethod
     def forward(ctx, qkv, causal=False, scale=None, kv_len=None):
@@ -199,21 +216,21 @@ class PackedQKVAttention(torch.autograd.Function):
         B, n, _, H, d = qkv.shape
         q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))  # [B, H, n, d] views
         o = torch.empty(B, n, H, d, dtype=qkv.dtype, device=qkv.device)
-        _, lse = attention_fwd(q, k, v, causal, scale, need_lse=True, out=o.transpose(1, 2),
-                               kv_len=kv_len)
-        ctx.save_for_backward(qkv, o, lse)
+        _, lse, o_lo = attention_fwd(q, k, v, causal, scale, need_lse=True, out=o.transpose(1, 2),
+                                     kv_len=kv_len, residual=True)
+        ctx.save_for_backward(qkv, o, lse, o_lo)
         ctx.causal, ctx.scale, ctx.kv_len = causal, scale, kv_len
         return o
 
     @staticmethod
     def backward(ctx, do):
-        qkv, o, lse = ctx.saved_tensors
+        qkv, o, lse, o_lo = ctx.saved_tensors
         q, k, v = (qkv[:, :, i].transpose(1, 2) for i in range(3))
         dqkv = torch.empty_like(qkv)
         dq, dk, dv = (dqkv[:, :, i].transpose(1, 2) for i in range(3))
         do_ = _feature_contiguous(do.to(o.dtype).transpose(1, 2))
         attention_bwd(q, k, v, o.transpose(1, 2), lse, do_, ctx.causal, ctx.scale, out=(dq, dk, dv),
-                      kv_len=ctx.kv_len)
+                      kv_len=ctx.kv_len, o_lo=o_lo)
         return dqkv, None, None, None
 
 

@@ -71,6 +71,9 @@ bool strides_ok(const mea_problem* p, const mea::TensorStrides& s, int64_t n, bo
 
 size_t elem_size(int32_t dtype) { return dtype == MEA_F32 ? 4 : 2; }
 
+// Whether o and do are float32 (float32 inputs, or 16-bit inputs with out_f32).
+bool out_is_f32(const mea_problem* p) { return p->dtype == MEA_F32 || p->out_f32 != 0; }
+
 bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
 bool dev_ptr_ok(const void* ptr) { return ptr != nullptr && aligned16(ptr); }
 
@@ -213,13 +216,14 @@ mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes)
 }
 
 mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k, const void* v,
-                             void* o, float* lse, void* workspace, size_t workspace_bytes,
+                             void* o, float* lse, void* o_lo, void* workspace, size_t workspace_bytes,
                              hipStream_t stream) {
   const mea_status st = check_problem(p);
   if (st != MEA_OK) return st;
   if (!dev_ptr_ok(q) || !dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(o))
     return MEA_ERR_INVALID_ARG;
   if (lse && !aligned16(lse)) return MEA_ERR_INVALID_ARG;
+  if (o_lo && (!aligned16(o_lo) || out_is_f32(p))) return MEA_ERR_INVALID_ARG;
   const FwdPlan pl = plan_fwd(p);
   if (pl.workspace > 0 && (!workspace || workspace_bytes < pl.workspace)) return MEA_ERR_WORKSPACE;
 
@@ -229,6 +233,7 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
   fp.v = v;
   fp.o = o;
   fp.lse = lse;
+  fp.o_lo = o_lo;
   fp.kv_len = p->kv_len;
   fp.n_q = p->n_q;
   fp.n_k = p->n_k;
@@ -272,14 +277,15 @@ mea_status mea_attention_fwd(const mea_problem* p, const void* q, const void* k,
 }
 
 mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k, const void* v,
-                             const void* o, const void* d_o, const float* lse, void* dq, void* dk,
-                             void* dv, void* workspace, size_t workspace_bytes,
+                             const void* o, const void* o_lo, const void* d_o, const float* lse, void* dq,
+                             void* dk, void* dv, void* workspace, size_t workspace_bytes,
                              hipStream_t stream) {
   const mea_status st = check_problem(p);
   if (st != MEA_OK) return st;
   if (!dev_ptr_ok(q) || !dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(o) || !dev_ptr_ok(d_o) ||
       !dev_ptr_ok(lse))
     return MEA_ERR_INVALID_ARG;
+  if (o_lo && (!aligned16(o_lo) || out_is_f32(p))) return MEA_ERR_INVALID_ARG;
   // dq may be NULL (dQ skipped); dk and dv are both given or both NULL.
   if ((dq && !aligned16(dq)) || (dk && !aligned16(dk)) || (dv && !aligned16(dv)))
     return MEA_ERR_INVALID_ARG;
@@ -293,6 +299,7 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   bp.k = k;
   bp.v = v;
   bp.o = o;
+  bp.o_lo = o_lo;
   bp.d_o = d_o;
   bp.lse = lse;
   bp.dq = dq;

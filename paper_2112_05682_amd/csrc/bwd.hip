@@ -63,7 +63,8 @@ __device__ __forceinline__ void split3_bf16(float x, __bf16& hi, __bf16& mid, __
 }
 
 // D_i = dO_i . O_i and the accumulator initial values of every (padded) row,
-// as records (REC) or as two float32 arrays.
+// as records (REC) or as two float32 arrays.  For a 16-bit O with the
+// forward's residual, O_i is taken as o_i + o_lo_i.
 template <typename TO, int D, bool REC>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
   using T = TO;  // o and do share the output dtype
@@ -83,8 +84,21 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
     const T* grow = static_cast<const T*>(p.d_o) + head_base(p.sdo, (int)bh, p.heads) + i * p.sdo.r;
     const vec16 o = *reinterpret_cast<const vec16*>(orow + part * (16 / E));
     const vec16 g = *reinterpret_cast<const vec16*>(grow + part * (16 / E));
+    float of[16 / E];
 #pragma unroll
-    for (int e = 0; e < 16 / E; ++e) acc = fmaf((float)o[e], (float)g[e], acc);
+    for (int e = 0; e < 16 / E; ++e) of[e] = (float)o[e];
+    if constexpr (E == 2) {
+      // o + o_lo (the forward's rounding residual) is exact in float32 and
+      // carries about 16 significant bits of the unrounded output.
+      if (p.o_lo) {
+        const vec16 lo = *reinterpret_cast<const vec16*>(static_cast<const T*>(p.o_lo) + (bh * p.n_q + i) * D +
+                                                         part * (16 / E));
+#pragma unroll
+        for (int e = 0; e < 16 / E; ++e) of[e] += (float)lo[e];
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 16 / E; ++e) acc = fmaf(of[e], (float)g[e], acc);
   }
 #pragma unroll
   for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, TPR);

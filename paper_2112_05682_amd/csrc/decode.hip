@@ -242,14 +242,16 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
     if (p.n_splits == 1) {
       const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;  // no visible key: o = 0
       TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
+      TO* gl = p.o_lo ? static_cast<TO*>(p.o_lo) + ((size_t)bh * p.n_q + row) * D : nullptr;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int a4 = 0; a4 < 4; ++a4) {
-          typename FragT<TO>::half v4;
+          float x4[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
-          *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
+          for (int e = 0; e < 4; ++e) x4[e] = acc[t][dt][4 * a4 + e] * inv;
+          const int f = 32 * dt + 8 * a4 + 4 * h;
+          store_out4<TO>(og + f, gl ? gl + f : nullptr, x4);
         }
       if (h == 0 && p.lse)
         p.lse[(size_t)bh * p.n_q + row] = l_tot > 0.0f ? (m_run[t] + __log2f(l_tot)) * 0.6931471805599453f : -INFINITY;

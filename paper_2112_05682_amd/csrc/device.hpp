@@ -240,6 +240,28 @@ __device__ __forceinline__ float tree_sum(const float* x, float acc) {
   }
 }
 
+// Four float32 results stored as TO at og.  For a 16-bit TO with a residual
+// buffer (lo != null) their rounding residuals x - (float)(TO)x, themselves
+// rounded to TO, go to lo: the difference of a float32 value and its 16-bit
+// rounding is exact in float32, so the pair carries about twice the 16-bit
+// precision.
+template <typename TO>
+__device__ __forceinline__ void store_out4(TO* og, TO* lo, const float (&x)[4]) {
+  typedef typename FragT<TO>::half H4;
+  H4 v4;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v4[e] = (TO)x[e];
+  *reinterpret_cast<H4*>(og) = v4;
+  if constexpr (sizeof(TO) == 2) {
+    if (lo) {
+      H4 r4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) r4[e] = (TO)(x[e] - (float)v4[e]);
+      *reinterpret_cast<H4*>(lo) = r4;
+    }
+  }
+}
+
 // 16-byte global load / store helpers.
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }

@@ -301,14 +301,16 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
       // A row with no visible key (key padding) has l = 0: o = 0, lse = -inf.
       const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
       TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
+      TO* gl = p.o_lo ? static_cast<TO*>(p.o_lo) + ((size_t)bh * p.n_q + row) * DV : nullptr;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int a4 = 0; a4 < 4; ++a4) {
-          typename FragT<TO>::half v4;
+          float x4[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
-          *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
+          for (int e = 0; e < 4; ++e) x4[e] = acc[t][dt][4 * a4 + e] * inv;
+          const int f = 32 * dt + 8 * a4 + 4 * h;
+          store_out4<TO>(og + f, gl ? gl + f : nullptr, x4);
         }
       if (h == 0 && p.lse)
         p.lse[(size_t)bh * p.n_q + row] = l_tot > 0.0f ? (m_ref[t] + __log2f(l_tot)) * kLn2 : -INFINITY;
@@ -751,14 +753,16 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
       // A row with no visible key (key padding) has l = 0: o = 0, lse = -inf.
       const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
       TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + row * p.so.r;
+      TO* gl = p.o_lo ? static_cast<TO*>(p.o_lo) + ((size_t)bh * p.n_q + row) * D : nullptr;
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int a4 = 0; a4 < 4; ++a4) {
-          typename FragT<TO>::half v4;
+          float x4[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v4[e] = (TO)(acc[t][dt][4 * a4 + e] * inv);
-          *reinterpret_cast<typename FragT<TO>::half*>(og + 32 * dt + 8 * a4 + 4 * h) = v4;
+          for (int e = 0; e < 4; ++e) x4[e] = acc[t][dt][4 * a4 + e] * inv;
+          const int f = 32 * dt + 8 * a4 + 4 * h;
+          store_out4<TO>(og + f, gl ? gl + f : nullptr, x4);
         }
       if (h == 0 && p.lse)
         p.lse[(size_t)bh * p.n_q + row] = l_tot > 0.0f ? (m_ref[t] + __log2f(l_tot)) * kLn2 : -INFINITY;
@@ -807,12 +811,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
   }
   // No visible key in any range (key padding): o = 0, lse = -inf.
   const float inv = l > 0.0f ? 1.0f / l : 0.0f;
-  typename FragT<TO>::half out;
+  float x4[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) out[e] = (TO)(o[e] * inv);
+  for (int e = 0; e < 4; ++e) x4[e] = o[e] * inv;
   const int bh = (int)(row / p.n_q);
   TO* og = static_cast<TO*>(p.o) + head_base(p.so, bh, p.heads) + (row - (int64_t)bh * p.n_q) * p.so.r;
-  *reinterpret_cast<typename FragT<TO>::half*>(og + f0) = out;
+  TO* gl = p.o_lo ? static_cast<TO*>(p.o_lo) + row * D : nullptr;
+  store_out4<TO>(og + f0, gl ? gl + f0 : nullptr, x4);
   if (f0 == 0 && p.lse) p.lse[row] = l > 0.0f ? (m_g + __log2f(l)) * kLn2 : -INFINITY;
 }
 

@@ -32,6 +32,7 @@ struct FwdParams {
   const void* v;
   void* o;
   float* lse;     // [B*H, n_q] or null
+  void* o_lo;     // 16-bit o only: rounding residual of o, contiguous [B*H, n_q, DV], or null
   float* part_o;  // split partials [S, B*H, n_q, D] (n_splits > 1)
   float* part_m;  // [S, B*H, n_q]
   float* part_l;  // [S, B*H, n_q]
@@ -71,6 +72,7 @@ struct BwdParams {
   const void* k;
   const void* v;
   const void* o;
+  const void* o_lo;  // residual of a 16-bit o (contiguous [B*H, n_q, DV]) or null
   const void* d_o;
   const float* lse;
   void* dq;

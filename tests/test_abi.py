@@ -88,8 +88,8 @@ def test_problem_validation(kw, status):
     lib = _lib.load()
     out = ctypes.c_size_t(0)
     assert lib.mea_attention_bwd_workspace_size(ctypes.byref(p), ctypes.byref(out)) == status
-    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == status
-    assert _lib.bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == status
+    assert _lib.bwd(p, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30,
                     None) == status
 
 
@@ -107,15 +107,16 @@ def test_fwd_rejects_null_or_misaligned_pointers(which):
     for bad in (None, FAKE + 2):
         ptrs = [FAKE] * 4
         ptrs[which] = bad
-        assert _lib.fwd(p, *ptrs, None, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+        assert _lib.fwd(p, *ptrs, None, None, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
     # misaligned lse
-    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE + 4, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE + 4, None, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("which", range(6))
+@pytest.mark.parametrize("which", [0, 1, 2, 3, 5, 6])
 def test_bwd_rejects_null_inputs(which):
+    # q, k, v, o, (o_lo: optional), do, lse, dq, dk, dv
     p = prob()
-    ptrs = [FAKE] * 9
+    ptrs = [FAKE] * 10
     ptrs[which] = None
     assert _lib.bwd(p, *ptrs, FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
 
@@ -125,18 +126,18 @@ def test_bwd_rejects_null_inputs(which):
 def test_bwd_rejects_bad_gradient_pointer_sets(grads):
     # dq optional; dk and dv both or neither; at least one group; 16 B aligned.
     p = prob()
-    assert _lib.bwd(p, *([FAKE] * 6), *grads, FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.bwd(p, *([FAKE] * 7), *grads, FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
 
 
 def test_workspace_too_small_is_rejected_before_launch():
     p = prob(heads=1, n_q=256, n_k=1 << 20)
     need = _lib.fwd_workspace_size(p)
     assert need > 0
-    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.MEA_ERR_WORKSPACE
-    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None) == _lib.MEA_ERR_WORKSPACE
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == _lib.MEA_ERR_WORKSPACE
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, need - 1, None) == _lib.MEA_ERR_WORKSPACE
     need_b = _lib.bwd_workspace_size(p)
-    assert _lib.bwd(p, *([FAKE] * 9), None, 0, None) == _lib.MEA_ERR_WORKSPACE
-    assert _lib.bwd(p, *([FAKE] * 9), FAKE, need_b - 1, None) == _lib.MEA_ERR_WORKSPACE
+    assert _lib.bwd(p, *([FAKE] * 10), None, 0, None) == _lib.MEA_ERR_WORKSPACE
+    assert _lib.bwd(p, *([FAKE] * 10), FAKE, need_b - 1, None) == _lib.MEA_ERR_WORKSPACE
 
 
 def test_problem_struct_layout_matches_the_header(tmp_path):
@@ -188,7 +189,7 @@ def _strided_prob(**over):
 ])
 def test_fwd_rejects_bad_strides(bad):
     # Validation fails before anything is launched (the pointers are fake).
-    assert _lib.fwd(_strided_prob(**bad), FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == \
+    assert _lib.fwd(_strided_prob(**bad), FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == \
         _lib.MEA_ERR_INVALID_ARG
 
 
@@ -196,7 +197,7 @@ def test_fwd_rejects_bad_strides(bad):
                                  {"d_o": (100 * 256, 64, 36)}])
 def test_bwd_rejects_bad_strides(bad):
     p = _strided_prob(**bad)
-    assert _lib.bwd(p, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.bwd(p, *([FAKE] * 10), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
 
 
 def test_shared_key_heads_are_valid_input_strides():
@@ -205,15 +206,15 @@ def test_shared_key_heads_are_valid_input_strides():
     ok = _strided_prob(k=(300 * 64, 0, 64), v=(300 * 64, 0, 64))
     assert ok.strides.contents.k.head == 0
     bad = _strided_prob(dk=(300 * 64, 0, 64))
-    assert _lib.bwd(bad, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.bwd(bad, *([FAKE] * 10), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
 
 
 def test_rejects_misaligned_kv_len():
     # kv_len is an int32 device array: a pointer that is not 4-byte aligned is
     # rejected before anything is launched (the tensor pointers are fake).
     p = _lib.problem(1, 2, 100, 100, 64, _lib.MEA_BF16, False, 0.125, kv_len=FAKE + 2)
-    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
-    assert _lib.bwd(p, *([FAKE] * 9), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.bwd(p, *([FAKE] * 10), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
     ok = _lib.problem(1, 2, 100, 100, 64, _lib.MEA_BF16, False, 0.125, kv_len=FAKE)
     assert ok.kv_len == FAKE
 
@@ -240,4 +241,20 @@ def test_value_head_dimension_sets_default_strides():
     # A value row stride below d_v is rejected before any launch.
     bad = _lib.problem(1, 1, 10, 20, 64, _lib.MEA_BF16, False, 0.125, d_v=128,
                        strides={"v": (20 * 128, 20 * 128, 64)})
-    assert _lib.fwd(bad, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.fwd(bad, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("dtype,out_f32", [(_lib.MEA_F32, False), (_lib.MEA_BF16, True)])
+def test_residual_is_rejected_for_a_float32_output(dtype, out_f32):
+    # o_lo exists only for a 16-bit o: with a float32 o it must be NULL.
+    p = _lib.problem(1, 2, 100, 100, 64, dtype, False, 0.125, out_f32=out_f32)
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+    assert _lib.bwd(p, *([FAKE] * 10), FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG
+
+
+def test_residual_must_be_aligned():
+    p = _lib.problem(1, 2, 100, 100, 64, _lib.MEA_BF16, False, 0.125)
+    assert _lib.fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 8, None, 0, None) == _lib.MEA_ERR_INVALID_ARG
+    ptrs = [FAKE] * 10
+    ptrs[4] = FAKE + 8
+    assert _lib.bwd(p, *ptrs, FAKE, 1 << 30, None) == _lib.MEA_ERR_INVALID_ARG

@@ -2,7 +2,9 @@
 
 Every case runs the HIP kernels through the C ABI (via the Python binding) on
 seeded synthetic inputs and compares O and LSE with the oracle evaluated on the
-exact same (widened) inputs, with rel_err = max|x - ref| / max|ref| per tensor.
+exact same (widened) inputs: O by rel_err = max|x - ref| / max|ref| per tensor
+and per row (row_err, each row against its own scale), LSE elementwise to
+1e-4 + 1e-5 |lse| (see parity_util).
 """
 import numpy as np
 import pytest
@@ -11,7 +13,7 @@ import torch
 import oracle
 from paper_2112_05682_amd import _lib, attention_fwd
 from paper_2112_05682_amd.inputs import WORKLOADS, attention_inputs, workload_inputs
-from parity_util import TOL, f64, rel_err, to_gpu
+from parity_util import TOL, check, check_lse, f64, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -26,10 +28,9 @@ def run_and_compare(B, H, nq, nk, d, dtype, causal, std=1.0, qk_mult=1.0, seeds=
     torch.cuda.synchronize()
     assert o.dtype == (out_dtype or g["q"].dtype)
     ro, rl = oracle.fwd(f64(x["q"]), f64(x["k"]), f64(x["v"]), scale=d ** -0.5, causal=causal)
-    eo, el = rel_err(f64(o), ro), rel_err(f64(lse), rl)
-    assert np.all(np.isfinite(f64(o))) and np.all(np.isfinite(f64(lse)))
-    assert eo <= TOL[dtype], ("O", eo)
-    assert el <= TOL[dtype], ("LSE", el)
+    assert np.all(np.isfinite(f64(lse)))
+    eo = check("O", f64(o), ro, TOL[dtype])
+    el = check_lse(f64(lse), rl)
     return eo, el
 
 
@@ -119,10 +120,9 @@ def test_forward_full_size_sampled(name):
         rows = sampled_rows(w.n_q, n_rows, 100 + b * 7 + h)
         ro, rl = oracle.fwd_rows(f64(x["q"][b, h]), f64(x["k"][b, h]), f64(x["v"][b, h]), rows,
                                  scale=w.d ** -0.5, causal=w.causal)
-        eo = rel_err(f64(o_c[b, h, rows]), ro)
-        el = rel_err(f64(l_c[b, h, rows]), rl)
-        print("  slice", (b, h), "rel_err O %.3g LSE %.3g" % (eo, el), flush=True)
-        assert eo <= TOL[w.dtype] and el <= TOL[w.dtype], (b, h, eo, el)
+        print("  slice", (b, h), flush=True)
+        check("O", f64(o_c[b, h, rows]), ro, TOL[w.dtype])
+        check_lse(f64(l_c[b, h, rows]), rl)
     assert torch.isfinite(o).all() and torch.isfinite(lse).all()
 
 

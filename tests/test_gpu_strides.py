@@ -10,14 +10,13 @@ tensors through batch, head and row strides (features contiguous).
 * One key head shared by all query heads (head stride 0 for k and v).
 Every case is compared with the float64 oracle on the same (widened) values.
 """
-import numpy as np
 import pytest
 import torch
 
 import oracle
 from paper_2112_05682_amd import attention_bwd, attention_fwd, attention_packed
 from paper_2112_05682_amd.inputs import attention_inputs
-from parity_util import TOL, TORCH_DT, f64, rel_err
+from parity_util import TOL, TORCH_DT, check, check_lse, f64, gradient_row_scales
 
 pytestmark = pytest.mark.gpu
 
@@ -46,22 +45,21 @@ def test_paper_layout_forward_and_backward(case):
     x = attention_inputs(B, H, nq, nk, d, dtype, with_grad=True)
     g = {k: as_bnhd_view(t) for k, t in x.items()}
     assert not g["q"].is_contiguous()
-    o, lse = attention_fwd(g["q"], g["k"], g["v"], causal=causal)
+    o, lse, o_lo = attention_fwd(g["q"], g["k"], g["v"], causal=causal, residual=True)
     # Gradients into strided views of [B, n, H, d] buffers.
     bufs = {n_: torch.empty(B, t.shape[2], H, d, dtype=TORCH_DT[dtype], device="cuda")
             for n_, t in (("dq", x["q"]), ("dk", x["k"]), ("dv", x["v"]))}
     views = tuple(bufs[n_].transpose(1, 2) for n_ in ("dq", "dk", "dv"))
-    attention_bwd(g["q"], g["k"], g["v"], o, lse, g["do"], causal=causal, out=views)
+    attention_bwd(g["q"], g["k"], g["v"], o, lse, g["do"], causal=causal, out=views, o_lo=o_lo)
     torch.cuda.synchronize()
     qq, kk, vv, dd = (f64(x[n_]) for n_ in ("q", "k", "v", "do"))
     ro, rl = oracle.fwd(qq, kk, vv, causal=causal)
     rdq, rdk, rdv = oracle.bwd(qq, kk, vv, dd, causal=causal)
-    errs = {"O": rel_err(f64(o), ro), "LSE": rel_err(f64(lse), rl),
-            "dQ": rel_err(f64(views[0]), rdq), "dK": rel_err(f64(views[1]), rdk),
-            "dV": rel_err(f64(views[2]), rdv)}
-    print("  ", {k_: "%.3g" % v_ for k_, v_ in errs.items()}, flush=True)
-    for name, e in errs.items():
-        assert np.isfinite(e) and e <= TOL[dtype], (name, e)
+    cq, ck = gradient_row_scales(qq, kk, vv, dd, rl, d ** -0.5, causal)
+    for name, got, ref, t_ in (("O", o, ro, None), ("dQ", views[0], rdq, cq), ("dK", views[1], rdk, ck),
+                               ("dV", views[2], rdv, None)):
+        check(name, f64(got), ref, TOL[dtype], terms=t_)
+    check_lse(f64(lse), rl)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
@@ -79,16 +77,15 @@ def test_packed_qkv_forward_and_backward(dtype, d, nq):
     torch.cuda.synchronize()
     assert o.shape == (B, nq, H, d) and t.grad.shape == qkv.shape
     q, k, v = (f64(qkv[:, :, i].transpose(1, 2)) for i in range(3))
-    ro, _ = oracle.fwd(q, k, v, causal=True)
+    ro, rl = oracle.fwd(q, k, v, causal=True)
     rdq, rdk, rdv = oracle.bwd(q, k, v, f64(up.transpose(1, 2)), causal=True)
+    cq, ck = gradient_row_scales(q, k, v, f64(up.transpose(1, 2)), rl, d ** -0.5, True)
     grad = t.grad.cpu()
-    errs = {"O": rel_err(f64(o.transpose(1, 2)), ro),
-            "dQ": rel_err(f64(grad[:, :, 0].transpose(1, 2)), rdq),
-            "dK": rel_err(f64(grad[:, :, 1].transpose(1, 2)), rdk),
-            "dV": rel_err(f64(grad[:, :, 2].transpose(1, 2)), rdv)}
-    print("  ", {k_: "%.3g" % v_ for k_, v_ in errs.items()}, flush=True)
-    for name, e in errs.items():
-        assert np.isfinite(e) and e <= TOL[dtype], (name, e)
+    for name, got, ref, t_ in (("O", o.transpose(1, 2), ro, None),
+                               ("dQ", grad[:, :, 0].transpose(1, 2), rdq, cq),
+                               ("dK", grad[:, :, 1].transpose(1, 2), rdk, ck),
+                               ("dV", grad[:, :, 2].transpose(1, 2), rdv, None)):
+        check(name, f64(got), ref, TOL[dtype], terms=t_)
 
 
 @pytest.mark.parametrize("nq", [1, 200])
@@ -103,4 +100,5 @@ def test_one_key_head_shared_by_all_query_heads(nq):
     o, lse = attention_fwd(q.to("cuda"), k, v)
     torch.cuda.synchronize()
     ro, rl = oracle.fwd(f64(q), f64(x["k"].expand(B, H, nk, d)), f64(x["v"].expand(B, H, nk, d)))
-    assert rel_err(f64(o), ro) <= TOL["bf16"] and rel_err(f64(lse), rl) <= TOL["bf16"]
+    check("O", f64(o), ro, TOL["bf16"])
+    check_lse(f64(lse), rl)
