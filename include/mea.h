@@ -65,7 +65,9 @@ typedef enum {
   MEA_ERR_INVALID_ARG = 1, /* null/misaligned pointer, size < 1, bad scale */
   MEA_ERR_UNSUPPORTED = 2, /* d or dtype outside the supported set */
   MEA_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
-  MEA_ERR_HIP = 4          /* the HIP runtime rejected a launch */
+  MEA_ERR_HIP = 4,         /* the HIP runtime rejected a launch */
+  MEA_ERR_SCRATCH = 5      /* problem needs more than the static scratch of
+                              mea_attention_bwd_noalloc holds */
 } mea_status;
 
 typedef enum { MEA_F32 = 0, MEA_F16 = 1, MEA_BF16 = 2 } mea_dtype;
@@ -162,6 +164,33 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
                              const void* d_o, const float* lse, void* dq, void* dk,
                              void* dv, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
+
+/* Bytes of the static device scratch of mea_attention_bwd_noalloc: 16 MiB
+ * for the per-row values plus 256 bytes of alignment slack, one copy per GPU
+ * the library runs on, held until the process ends. */
+#define MEA_NOALLOC_SCRATCH_BYTES (((size_t)16 << 20) + 256)
+
+/* mea_attention_bwd without the workspace arguments, for callers that cannot
+ * allocate device memory: code being captured into a HIP graph, tight
+ * serving loops, harnesses that forbid allocation.  The per-row workspace
+ * (mea_attention_bwd_workspace_size bytes) lives in a file-scope device
+ * array of MEA_NOALLOC_SCRATCH_BYTES per GPU instead; the call itself
+ * allocates nothing (no hipMalloc, no library allocation).  Problems whose
+ * workspace exceeds that size return MEA_ERR_SCRATCH before anything is
+ * enqueued: B * H * ceil(n_q / 64) * 64 padded query rows must not exceed
+ * 2^20 for 16-bit inputs and outputs at d = d_v = 64 (16 bytes per row), or
+ * 2^21 otherwise (8 bytes per row).  The first call on a device
+ * looks up that device's copy of the array; `stream` must belong to the
+ * current device (0 = its null stream), else MEA_ERR_INVALID_ARG.
+ * Every call on one GPU shares its array, and the backward fully writes the
+ * part it reads before reading it (nothing needs to start at zero): calls
+ * that overlap on one GPU (different streams, or threads) race and must be
+ * serialised by the caller.  Results are identical to mea_attention_bwd's
+ * (same kernels). */
+mea_status mea_attention_bwd_noalloc(const mea_problem* p, const void* q, const void* k,
+                                     const void* v, const void* o, const void* o_lo,
+                                     const void* d_o, const float* lse, void* dq, void* dk,
+                                     void* dv, hipStream_t stream);
 
 /* Static description of a status code (never NULL). */
 const char* mea_status_string(mea_status s);

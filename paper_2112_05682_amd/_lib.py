@@ -16,6 +16,10 @@ MEA_ERR_INVALID_ARG = 1
 MEA_ERR_UNSUPPORTED = 2
 MEA_ERR_WORKSPACE = 3
 MEA_ERR_HIP = 4
+MEA_ERR_SCRATCH = 5
+
+# Static scratch of mea_attention_bwd_noalloc (MEA_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = (16 << 20) + 256
 
 MEA_F32, MEA_F16, MEA_BF16 = 0, 1, 2
 
@@ -25,6 +29,7 @@ EXPORTS = (
     "mea_attention_bwd_workspace_size",
     "mea_attention_fwd",
     "mea_attention_bwd",
+    "mea_attention_bwd_noalloc",
     "mea_status_string",
 )
 
@@ -85,8 +90,9 @@ def load(path: str = LIB_PATH):
     lib.mea_attention_bwd_workspace_size.argtypes = [prob, ctypes.POINTER(sz)]
     lib.mea_attention_fwd.argtypes = [prob, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.mea_attention_bwd.argtypes = [prob, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.mea_attention_bwd_noalloc.argtypes = [prob, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     for name in ("mea_attention_fwd_workspace_size", "mea_attention_bwd_workspace_size",
-                 "mea_attention_fwd", "mea_attention_bwd"):
+                 "mea_attention_fwd", "mea_attention_bwd", "mea_attention_bwd_noalloc"):
         getattr(lib, name).restype = ctypes.c_int
     lib.mea_status_string.argtypes = [ctypes.c_int]
     lib.mea_status_string.restype = ctypes.c_char_p
@@ -150,3 +156,9 @@ def bwd(p: MeaProblem, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, workspace, worksp
         stream) -> int:
     return load().mea_attention_bwd(ctypes.byref(p), q, k, v, o, o_lo, d_o, lse, dq, dk, dv,
                                     workspace, workspace_bytes, stream)
+
+
+def bwd_noalloc(p: MeaProblem, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, stream) -> int:
+    """The backward without a workspace argument (static device scratch)."""
+    return load().mea_attention_bwd_noalloc(ctypes.byref(p), q, k, v, o, o_lo, d_o, lse, dq, dk,
+                                            dv, stream)

@@ -5,8 +5,16 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/mea.h"
 #include "kernels.hpp"
+
+// Per-row backward workspace of mea_attention_bwd_noalloc: one copy per GPU,
+// allocated when the library's code object is loaded on that GPU.  In host
+// code the name `scratch` is only a host-side stand-in; its device address is
+// looked up per device (scratch_of_device) and only that address is used.
+static __device__ __align__(256) unsigned char scratch[MEA_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -184,6 +192,51 @@ float* align256(void* base, size_t off) {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Device address of `scratch` on the current device, looked up once per
+// device (hipGetSymbolAddress with that device current) and cached.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+mea_status scratch_of_device(hipStream_t stream, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return MEA_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return MEA_ERR_UNSUPPORTED;
+  if (stream) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return MEA_ERR_HIP;
+    if (sdev != dev) return MEA_ERR_INVALID_ARG;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return MEA_ERR_HIP;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return MEA_OK;
+}
+
+// Checks of the backward's pointers (before anything is launched).
+mea_status check_bwd_pointers(const mea_problem* p, const void* q, const void* k, const void* v,
+                              const void* o, const void* o_lo, const void* d_o, const float* lse,
+                              const void* dq, const void* dk, const void* dv) {
+  if (!dev_ptr_ok(q) || !dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(o) || !dev_ptr_ok(d_o) ||
+      !dev_ptr_ok(lse))
+    return MEA_ERR_INVALID_ARG;
+  if (o_lo && (!aligned16(o_lo) || out_is_f32(p))) return MEA_ERR_INVALID_ARG;
+  // dq may be NULL (dQ skipped); dk and dv are both given or both NULL.
+  if ((dq && !aligned16(dq)) || (dk && !aligned16(dk)) || (dv && !aligned16(dv)))
+    return MEA_ERR_INVALID_ARG;
+  if ((dk == nullptr) != (dv == nullptr)) return MEA_ERR_INVALID_ARG;
+  if (!dq && !dk) return MEA_ERR_INVALID_ARG;
+  return MEA_OK;
+}
+
+mea_status bwd_launch(const mea_problem* p, const void* q, const void* k, const void* v, const void* o,
+                      const void* o_lo, const void* d_o, const float* lse, void* dq, void* dk, void* dv,
+                      void* workspace, hipStream_t stream);
+
 }  // namespace
 
 extern "C" {
@@ -195,6 +248,7 @@ const char* mea_status_string(mea_status s) {
     case MEA_ERR_UNSUPPORTED: return "unsupported head dimension or dtype";
     case MEA_ERR_WORKSPACE: return "workspace missing or too small";
     case MEA_ERR_HIP: return "HIP runtime error at launch";
+    case MEA_ERR_SCRATCH: return "problem needs more workspace than the static scratch of the allocation-free entry point (MEA_NOALLOC_SCRATCH_BYTES)";
   }
   return "unknown status";
 }
@@ -280,20 +334,38 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
                              const void* o, const void* o_lo, const void* d_o, const float* lse, void* dq,
                              void* dk, void* dv, void* workspace, size_t workspace_bytes,
                              hipStream_t stream) {
-  const mea_status st = check_problem(p);
+  mea_status st = check_problem(p);
   if (st != MEA_OK) return st;
-  if (!dev_ptr_ok(q) || !dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(o) || !dev_ptr_ok(d_o) ||
-      !dev_ptr_ok(lse))
-    return MEA_ERR_INVALID_ARG;
-  if (o_lo && (!aligned16(o_lo) || out_is_f32(p))) return MEA_ERR_INVALID_ARG;
-  // dq may be NULL (dQ skipped); dk and dv are both given or both NULL.
-  if ((dq && !aligned16(dq)) || (dk && !aligned16(dk)) || (dv && !aligned16(dv)))
-    return MEA_ERR_INVALID_ARG;
-  if ((dk == nullptr) != (dv == nullptr)) return MEA_ERR_INVALID_ARG;
-  if (!dq && !dk) return MEA_ERR_INVALID_ARG;
+  st = check_bwd_pointers(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv);
+  if (st != MEA_OK) return st;
   const size_t need = bwd_workspace(p);
   if (!workspace || workspace_bytes < need) return MEA_ERR_WORKSPACE;
+  return bwd_launch(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, workspace, stream);
+}
 
+mea_status mea_attention_bwd_noalloc(const mea_problem* p, const void* q, const void* k, const void* v,
+                                     const void* o, const void* o_lo, const void* d_o, const float* lse,
+                                     void* dq, void* dk, void* dv, hipStream_t stream) {
+  mea_status st = check_problem(p);
+  if (st != MEA_OK) return st;
+  st = check_bwd_pointers(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv);
+  if (st != MEA_OK) return st;
+  if (bwd_workspace(p) > MEA_NOALLOC_SCRATCH_BYTES) return MEA_ERR_SCRATCH;
+  void* ws = nullptr;
+  st = scratch_of_device(stream, &ws);
+  if (st != MEA_OK) return st;
+  return bwd_launch(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, ws, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The backward after validation: kernel arguments, stride checks, launches.
+// `workspace` holds at least bwd_workspace(p) bytes.
+mea_status bwd_launch(const mea_problem* p, const void* q, const void* k, const void* v, const void* o,
+                      const void* o_lo, const void* d_o, const float* lse, void* dq, void* dk, void* dv,
+                      void* workspace, hipStream_t stream) {
   BwdParams bp = {};
   bp.q = q;
   bp.k = k;
@@ -343,4 +415,4 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   return e == hipSuccess ? MEA_OK : MEA_ERR_HIP;
 }
 
-}  // extern "C"
+}  // namespace

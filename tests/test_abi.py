@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in range(5):
+    for s in range(6):
         assert _lib.status_string(s)
     assert _lib.status_string(99) == "unknown status"
 
