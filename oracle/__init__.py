@@ -68,6 +68,8 @@ def _load():
                      "mea_oracle_bwd_dkdv_keys", "mea_oracle_num_threads"):
             getattr(lib, name).restype = _int
         lib.mea_oracle_num_threads.argtypes = []
+        lib.mea_oracle_set_num_threads.argtypes = [_int]
+        lib.mea_oracle_set_num_threads.restype = None
         _lib = lib
     return _lib
 
@@ -116,6 +118,11 @@ def default_scale(d: int) -> float:
 
 def num_threads() -> int:
     return int(_load().mea_oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the oracle's later calls from this thread."""
+    _load().mea_oracle_set_num_threads(int(n))
 
 
 def fwd(q, k, v, scale=None, causal=False, kv_len=None):

@@ -103,6 +103,16 @@ int mea_oracle_num_threads(void) {
 #endif
 }
 
+/* Threads used by the calling thread's later parallel loops (n >= 1); for
+ * timing the oracle on one core and on all of them in one process. */
+void mea_oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  omp_set_num_threads(n > 0 ? n : 1);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------ */
 /* Direct form (Section 1 definition with the max subtraction of Section 3). */
 /* ------------------------------------------------------------------------ */

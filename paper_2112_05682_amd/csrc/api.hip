@@ -4,6 +4,7 @@
 // caller's stream.
 #include <math.h>
 #include <stdint.h>
+#include <string.h>
 
 #include <mutex>
 
@@ -242,7 +243,11 @@ mea_status bwd_launch(const mea_problem* p, const void* q, const void* k, const 
 extern "C" {
 
 const char* mea_status_string(mea_status s) {
-  switch (s) {
+  // A C caller may pass any int: read the raw value instead of loading an
+  // enumeration value that may lie outside its range.
+  int code = 0;
+  memcpy(&code, &s, sizeof(code) < sizeof(s) ? sizeof(code) : sizeof(s));
+  switch (code) {
     case MEA_OK: return "ok";
     case MEA_ERR_INVALID_ARG: return "invalid argument";
     case MEA_ERR_UNSUPPORTED: return "unsupported head dimension or dtype";
