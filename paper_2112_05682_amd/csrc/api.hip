@@ -101,8 +101,11 @@ void fwd_tiles(int dtype, int64_t d, int64_t dv, int* bq, int* bk) {
   } else if (d == 64 && dv == 64) {
     *bq = mea::FwdShape<__bf16, 64>::BQ;
     *bk = mea::FwdShape<__bf16, 64>::BK;
-  } else {
+  } else if (d == 128 && dv == 128) {
     *bq = mea::FwdShape<__bf16, 128>::BQ;
+    *bk = mea::FwdShape<__bf16, 128>::BK;
+  } else {  // d_v != d: the 4-wave kernel
+    *bq = mea::kFwdBq4wave128;
     *bk = mea::FwdShape<__bf16, 128>::BK;
   }
 }

@@ -43,8 +43,14 @@ struct FwdTile {
   static constexpr int NT = NW * 64;
   static constexpr int BQ = NW * QT * 32;
   static constexpr int E = sizeof(T);
-  static constexpr int RSK = D + 16 / E;         // LDS row strides (elements), 16 B pad
-  static constexpr int RSV = DV + 16 / E;
+  // LDS row strides (elements).  K rows (read 16 bytes per lane, 16 rows
+  // per 16 lanes) carry a 16-byte pad: each row starts 4 banks after the
+  // previous one, so the 16 rows cover all 64 banks.  V rows are read by the
+  // transposing read, 4 consecutive rows x 64 bytes per 32 lanes: a 64-byte pad
+  // (16 banks) keeps those 4 rows in disjoint banks (a 16-byte pad made them
+  // overlap 4 ways).  float32 V is read by scalar loads and keeps 16 bytes.
+  static constexpr int RSK = D + 16 / E;
+  static constexpr int RSV = DV + (E == 2 ? 64 : 16) / E;
   static constexpr int TILEK = BK * RSK;         // elements of the K tile
   static constexpr int TILEV = BK * RSV;         // elements of the V tile
   static constexpr int STAGE = TILEK + TILEV;    // one K/V stage
@@ -335,14 +341,17 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// Forward for 16-bit inputs at d = 64: two wave groups in opposite phases.
+// Forward for 16-bit inputs (d = 64 and d = 128): two wave groups in opposite
+// phases.
 //
 // A workgroup is 8 waves; wave w and wave w + 4 share a SIMD.  Waves 0-3
 // (group 0) and 4-7 (group 1) alternate between an MFMA phase (scores of key
 // tile j and the PV product of tile j-1) and a vector phase (the lazy softmax
 // of the tile whose scores they computed), one barrier between phases, so that
 // on every SIMD one wave feeds the matrix cores while the other runs the
-// exponentials.  Group 1 runs one phase behind group 0.  K and V tiles go from
+// exponentials.  Group 1 runs one phase behind group 0.  A wave owns 64
+// queries at d = 64 and 32 at d = 128 (the registers of the accumulator and
+// the query fragments); both give 32 MFMAs per 64-key tile and wave.  K and V tiles go from
 // memory to LDS with global_load_lds (no staging registers), issued by group 1
 // during its vector phase two phases before they are read; rows are stored
 // unpadded with an XOR swizzle of their 16-byte chunks that keeps both the
@@ -352,22 +361,57 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 #ifndef MEA_FWD_PP_W0
 #define MEA_FWD_PP_W0 3
 #endif
+#ifndef MEA_FWD_PP128_W0
+#define MEA_FWD_PP128_W0 0
+#endif
+// LDS fetch distance (steps) of the d = 128 MFMA phase.
+#ifndef MEA_FWD_PP128_AHEAD
+#define MEA_FWD_PP128_AHEAD 3
+#endif
 namespace pp {
-constexpr int D = 64, QT = 2, BK = 64, NW = 8, BQ = NW * QT * 32, NSTAGE = 3;
-constexpr int ROWB = D * 2;          // bytes per LDS row (unpadded)
-constexpr int TILEB = BK * ROWB;     // 8 KiB per K or V tile
-// Physical 16-byte chunk of logical chunk x in row r.
-__device__ __forceinline__ int swz_k(int r) { return (r >> 1) & 7; }
-__device__ __forceinline__ int swz_v(int r) { return ((r >> 1) & 1) << 2; }
+// Tile geometry per head dimension.  K and V rows are stored unpadded; the
+// physical 16-byte chunk of logical chunk x in row r is x ^ swz(r).
+//   d = 64: 128-byte rows, two per 64-bank line.  K is read 16 rows x one
+//   chunk per 16 lanes (perm32 rows 0-15): rows 2m, 2m+1 sit in different bank
+//   halves and (r >> 1) & 7 spreads the 8 pairs over the 8 chunks.  V is read
+//   by the transposing read, 4 rows x 4 chunks per 32 lanes: rows 4m+2, 4m+3
+//   move to the other 4 chunks of their half.
+//   d = 128: 256-byte rows, one per 64-bank line.  K: r & 15 gives the 16 rows
+//   16 different chunks; V: (r & 3) << 2 gives each of the 4 rows its own
+//   4-chunk group.
+template <int D> struct Cfg;
+template <> struct Cfg<64> {
+  static constexpr int QT = 2, W0 = MEA_FWD_PP_W0;
+  __device__ static __forceinline__ int swz_k(int r) { return (r >> 1) & 7; }
+  __device__ static __forceinline__ int swz_v(int r) { return ((r >> 1) & 1) << 2; }
+};
+template <> struct Cfg<128> {
+  static constexpr int QT = 1, W0 = MEA_FWD_PP128_W0;
+  __device__ static __forceinline__ int swz_k(int r) { return r & 15; }
+  __device__ static __forceinline__ int swz_v(int r) { return (r & 3) << 2; }
+};
+constexpr int BK = 64, NW = 8, NSTAGE = 3;
+template <int D> constexpr int BQ = NW * Cfg<D>::QT * 32;  // queries per workgroup
 }  // namespace pp
 
-template <typename T, typename TO, bool CAUSAL>
+template <typename T, typename TO, int D, bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
-  using namespace pp;
+  using pp::BK;
+  using pp::NSTAGE;
+  using pp::NW;
+  using C = pp::Cfg<D>;
+  constexpr int QT = C::QT, BQ = pp::BQ<D>;
+  constexpr int ROWB = D * 2;              // bytes per LDS row (unpadded)
+  constexpr int TILEB = BK * ROWB;         // one K or V tile: 8 or 16 KiB
+  constexpr int CPR = ROWB / 16;           // 16-byte chunks per row
+  constexpr int RPU = 1024 / ROWB;         // rows per 1 KiB copy instruction
+  constexpr int UPW = TILEB / 1024 / 4;    // copy instructions per group-1 wave and tile
   constexpr int KC = D / 16, NKT = BK / 32, NPC = BK / 16, NDT = D / 32;
+  auto swz_k = [](int r) { return C::swz_k(r); };
+  auto swz_v = [](int r) { return C::swz_v(r); };
   // 16-key chunks of query sub-tile 0 whose weights are computed in the MFMA
   // phase (interleaved with the PV MFMAs); the rest go to the softmax phase.
-  constexpr int W0 = MEA_FWD_PP_W0;
+  constexpr int W0 = C::W0;
   static_assert(W0 >= 0 && W0 <= NPC, "weight chunks");
   static_assert(sizeof(T) == 2, "16-bit inputs only");
 
@@ -447,15 +491,15 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   auto vstage = [&](int j) { return vst + (j % NSTAGE) * TILEB; };
 
   // Asynchronous copy of rows [k0, k0 + BK) of K or V into an LDS stage.  One
-  // instruction moves 1 KiB = 8 rows; the lane writing physical chunk x of row
-  // r fetches logical chunk x ^ swz(r).  Rows past n_k repeat the last key row
-  // (finite data; those keys are masked).
+  // instruction moves 1 KiB = RPU rows; the lane writing physical chunk x of
+  // row r fetches logical chunk x ^ swz(r).  Rows past n_k repeat the last key
+  // row (finite data; those keys are masked).
   auto load_tile = [&](const T* g, int64_t k0, unsigned char* stage, bool is_v, int part, int nparts)
                        __attribute__((always_inline)) {
     const int64_t rs = is_v ? p.sv.r : p.sk.r;
-    for (int ii = part; ii < BK / 8; ii += nparts) {
-      const int row = 8 * ii + (lane >> 3);
-      const int x = lane & 7;
+    for (int ii = part; ii < BK / RPU; ii += nparts) {
+      const int row = RPU * ii + (int)((unsigned)lane / CPR);
+      const int x = (int)((unsigned)lane % CPR);
       const int lchunk = x ^ (is_v ? swz_v(row) : swz_k(row));
       int64_t key = k0 + row;
       if (key > p.n_k - 1) key = p.n_k - 1;
@@ -489,10 +533,14 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   // transposing LDS read (see lds_col_frag), with the V swizzle applied.
   auto pv = [&](const unsigned char* vs, Frag<T> (&pf)[QT][NPC]) __attribute__((always_inline)) {
     const int g = lane >> 4, i = lane & 15;
+    // One sub-tile (d = 128): feature tiles vary fastest, so consecutive MFMAs
+    // accumulate into different registers.
+    constexpr int NA = QT == 1 ? NPC : NDT, NB = QT == 1 ? NDT : NPC;
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
+    for (int ia = 0; ia < NA; ++ia) {
 #pragma unroll
-      for (int pc = 0; pc < NPC; ++pc) {
+      for (int ib = 0; ib < NB; ++ib) {
+        const int dt = QT == 1 ? ib : ia, pc = QT == 1 ? ia : ib;
         const int row = 16 * pc + 8 * (g >> 1) + (i >> 2);
         const int colb = 2 * (32 * dt + 16 * (g & 1) + 4 * (i & 3));
         const int addr_lo = row * ROWB + (((colb >> 4) ^ swz_v(row)) << 4) + (colb & 15);
@@ -509,6 +557,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
       }
     }
   };
+  (void)pv;
 
   // Lazy softmax (Section 3) of query sub-tile t of tile j: P = 2^(c s - m)
   // against the current reference m, rounded into pfo[t], and the lane's
@@ -575,9 +624,15 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   auto pv_weights0 = [&](const unsigned char* vs, Frag<T> (&pf_old)[QT][NPC], Frag<T> (&pf_new)[QT][NPC],
                          f32x16 (&s)[NKT][QT], float neg) __attribute__((always_inline)) {
     constexpr int NSTEP = NDT * NPC;
+    // With one query sub-tile per wave (d = 128) consecutive steps go to
+    // different accumulators (the feature tile varies fastest), so no MFMA
+    // waits for the result of the one before it, and the V fragments are
+    // read two steps ahead (one step is a single 32-cycle MFMA there).
+    constexpr bool DT_FAST = QT == 1;
+    constexpr int AHEAD = QT == 1 ? 2 : 1;
     const int g = lane >> 4, i4 = lane & 15;
     auto vfrag = [&](int step) __attribute__((always_inline)) {
-      const int dt = step / NPC, pc = step % NPC;
+      const int dt = DT_FAST ? step % NDT : step / NPC, pc = DT_FAST ? step / NDT : step % NPC;
       const int row = 16 * pc + 8 * (g >> 1) + (i4 >> 2);
       const int colb = 2 * (32 * dt + 16 * (g & 1) + 4 * (i4 & 3));
       const int addr_lo = row * ROWB + (((colb >> 4) ^ swz_v(row)) << 4) + (colb & 15);
@@ -590,21 +645,26 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
       r8[4] = hi[0]; r8[5] = hi[1]; r8[6] = hi[2]; r8[7] = hi[3];
       return __builtin_bit_cast(Frag<T>, r8);
     };
-    Frag<T> vf[2];
+    Frag<T> vf[AHEAD + 1];
     vf[0] = vfrag(0);
+    if constexpr (AHEAD > 1) vf[1] = vfrag(1);
     u32x4 packed;
     float sum0 = 0.0f, sum1 = 0.0f;
 #pragma unroll
     for (int i = 0; i < NSTEP; ++i) {
-      const int dt = i / NPC, pcv = i % NPC;
-      if (i + 1 < NSTEP) vf[(i + 1) & 1] = vfrag(i + 1);
+      const int dt = DT_FAST ? i % NDT : i / NPC, pcv = DT_FAST ? i / NDT : i % NPC;
+      if constexpr (AHEAD == 1) {
+        if (i + 1 < NSTEP) vf[(i + 1) & 1] = vfrag(i + 1);
+      } else {
+        if (i + AHEAD < NSTEP) vf[(i + AHEAD) % (AHEAD + 1)] = vfrag(i + AHEAD);
+      }
       // Step i does half of chunk pcs of the weights; with W0 < NPC chunks
       // here, the steps are spread evenly over the PV MFMAs.
       constexpr int WSTEPS = 2 * W0;
       const int wi = (i * WSTEPS) / NSTEP;
       const bool has_w = WSTEPS > 0 && (i * WSTEPS) % NSTEP < WSTEPS;
       const int pcs = wi >> 1, half = wi & 1;
-      acc[0][dt] = mma(vf[i & 1], pf_old[0][pcv], acc[0][dt]);
+      acc[0][dt] = mma(vf[AHEAD == 1 ? (i & 1) : i % (AHEAD + 1)], pf_old[0][pcv], acc[0][dt]);
       if (has_w) {
         float e4[4];
 #pragma unroll
@@ -615,7 +675,8 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
         if (pcs & 1) sum1 = tree_sum<4>(e4, sum1);
         else sum0 = tree_sum<4>(e4, sum0);
       }
-      acc[1][dt] = mma(vf[i & 1], pf_old[1][pcv], acc[1][dt]);
+#pragma unroll
+      for (int t = 1; t < QT; ++t) acc[t][dt] = mma(vf[AHEAD == 1 ? (i & 1) : i % (AHEAD + 1)], pf_old[t][pcv], acc[t][dt]);
       if (has_w && half) pf_new[0][pcs] = __builtin_bit_cast(Frag<T>, packed);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -653,23 +714,34 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   // Tile 0 multiplies the V(-1) stage by zero weights: clear it so that it
   // holds finite values.
   reinterpret_cast<u32x4*>(vstage(NSTAGE - 1))[tid] = u32x4{0u, 0u, 0u, 0u};
-  static_assert(NW * 64 * 16 == TILEB, "one 16-byte store per thread clears a stage");
-  if (n_tiles > 0) load_tile(kg, kb, kstage(0), false, wave, NW);  // K(0): one instruction per wave
+  if constexpr (TILEB > NW * 64 * 16)
+    reinterpret_cast<u32x4*>(vstage(NSTAGE - 1))[tid + NW * 64] = u32x4{0u, 0u, 0u, 0u};
+  static_assert(TILEB == NW * 64 * 16 || TILEB == 2 * NW * 64 * 16, "one or two 16-byte stores per thread clear a stage");
+  if (n_tiles > 0) load_tile(kg, kb, kstage(0), false, wave, NW);  // K(0): 1 KiB per wave and instruction
   // The barrier's fence does not cover copies the compiler cannot see.
   wait_global_loads();
   __syncthreads();
   // Group 1 issues two waves of copies ahead, as if from softmax phases -2
   // and -1, and starts one phase behind group 0.  Its wave w copies units
-  // w - 4 and w (rows 8u .. 8u + 7) of each tile; the lane's source offsets
-  // within a tile (bytes) are computed once.
-  const int urow0 = 8 * (wave - 4) + (lane >> 3), urow1 = urow0 + 32;
+  // w - 4 + 4i, i < UPW (rows RPU u .. RPU u + RPU - 1) of each tile; the
+  // lane's source offsets within a tile (bytes) are computed once.
   constexpr unsigned E = sizeof(T);
   const unsigned rk = (unsigned)p.sk.r, rv = (unsigned)p.sv.r;  // row strides (< 2^24, checked on the host)
-  const unsigned uk0 = E * (urow0 * rk + 8 * ((lane & 7) ^ swz_k(urow0)));
-  const unsigned uk1 = E * (urow1 * rk + 8 * ((lane & 7) ^ swz_k(urow1)));
-  const unsigned uv0 = E * (urow0 * rv + 8 * ((lane & 7) ^ swz_v(urow0)));
-  const unsigned uv1 = E * (urow1 * rv + 8 * ((lane & 7) ^ swz_v(urow1)));
-  auto copy_tile = [&](bool is_v, int j, unsigned char* stage, unsigned off0, unsigned off1) __attribute__((always_inline)) {
+  constexpr int LCPR = CPR == 8 ? 3 : 4;
+  static_assert(CPR == 1 << LCPR && (UPW == 2 || UPW == 4), "copy geometry");
+  const int urow0 = RPU * (wave - 4) + (lane >> LCPR), urow1 = urow0 + 4 * RPU;
+  const unsigned uk0 = E * (urow0 * rk + 8 * ((lane & (CPR - 1)) ^ swz_k(urow0)));
+  const unsigned uk1 = E * (urow1 * rk + 8 * ((lane & (CPR - 1)) ^ swz_k(urow1)));
+  const unsigned uv0 = E * (urow0 * rv + 8 * ((lane & (CPR - 1)) ^ swz_v(urow0)));
+  const unsigned uv1 = E * (urow1 * rv + 8 * ((lane & (CPR - 1)) ^ swz_v(urow1)));
+  // d = 128: units w - 4 + 8 and w - 4 + 12 as well.
+  const int urow2 = urow0 + 8 * RPU, urow3 = urow0 + 12 * RPU;
+  const unsigned uk2 = UPW > 2 ? E * (urow2 * rk + 8 * ((lane & (CPR - 1)) ^ swz_k(urow2))) : 0u;
+  const unsigned uk3 = UPW > 2 ? E * (urow3 * rk + 8 * ((lane & (CPR - 1)) ^ swz_k(urow3))) : 0u;
+  const unsigned uv2 = UPW > 2 ? E * (urow2 * rv + 8 * ((lane & (CPR - 1)) ^ swz_v(urow2))) : 0u;
+  const unsigned uv3 = UPW > 2 ? E * (urow3 * rv + 8 * ((lane & (CPR - 1)) ^ swz_v(urow3))) : 0u;
+  auto copy_tile = [&](bool is_v, int j, unsigned char* stage, unsigned off0, unsigned off1, unsigned off2,
+                       unsigned off3) __attribute__((always_inline)) {
     const int64_t k0 = kb + (int64_t)j * BK;
     const unsigned base = __builtin_amdgcn_readfirstlane(lds_addr(stage) + (wave - 4) * 1024);
     const T* g = is_v ? vg : kg;
@@ -677,13 +749,17 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
       const T* tile = g + k0 * (is_v ? p.sv.r : p.sk.r);
       copy_to_lds16_sb(tile, off0, base);
       copy_to_lds16_sb(tile, off1, base + 4096);
+      if constexpr (UPW > 2) {
+        copy_to_lds16_sb(tile, off2, base + 8192);
+        copy_to_lds16_sb(tile, off3, base + 12288);
+      }
     } else {
       load_tile(g, k0, stage, is_v, wave - 4, 4);
     }
   };
   auto issue = [&](int j) __attribute__((always_inline)) {
-    if (j + 3 < n_tiles) copy_tile(false, j + 3, kstage(j + 3), uk0, uk1);
-    if (j + 2 < n_tiles) copy_tile(true, j + 2, vstage(j + 2), uv0, uv1);
+    if (j + 3 < n_tiles) copy_tile(false, j + 3, kstage(j + 3), uk0, uk1, uk2, uk3);
+    if (j + 2 < n_tiles) copy_tile(true, j + 2, vstage(j + 2), uv0, uv1, uv2, uv3);
   };
   if (grp == 1) {
     issue(-2);
@@ -691,26 +767,82 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
     barrier();
   }
   // pf_old holds P(j-1) and pf_new receives P(j).
+  // MFMA phase with one query sub-tile per wave (d = 128): S = K Q^T of tile
+  // j and O += V P of tile j - 1 as one sequence of 32 single-MFMA steps, S
+  // and PV steps alternating (consecutive MFMAs accumulate into different
+  // registers), each step's LDS fragment read PF_AHEAD steps before its MFMA.
+  // A lone MFMA does not cover an LDS read's latency, so the fragments of the
+  // next steps must already be in flight.
+  auto mfma_phase1 = [&](const unsigned char* ks, const unsigned char* vs, Frag<T> (&pf_old)[QT][NPC],
+                         f32x16 (&sc)[NKT][QT]) __attribute__((always_inline)) {
+    constexpr int NS = KC * NKT, NP = NDT * NPC;
+    static_assert(QT != 1 || NS == NP, "alternating S and PV steps");
+    constexpr int N = NS + NP, AH = MEA_FWD_PP128_AHEAD;
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[kt][0][r] = 0.0f;
+    const int g = lane >> 4, i4 = lane & 15;
+    auto frag = [&](int step) __attribute__((always_inline)) {
+      const int k = step >> 1;
+      if ((step & 1) == 0) {  // S step k: key sub-tile k % NKT, k chunk k / NKT
+        const int row = 32 * (k % NKT) + perm32(c);
+        const int x = (2 * (k / NKT) + h) ^ swz_k(row);
+        return *reinterpret_cast<const Frag<T>*>(ks + row * ROWB + x * 16);
+      }
+      const int dt = k % NDT, pc = k / NDT;  // PV step k
+      const int row = 16 * pc + 8 * (g >> 1) + (i4 >> 2);
+      const int colb = 2 * (32 * dt + 16 * (g & 1) + 4 * (i4 & 3));
+      const int addr_lo = row * ROWB + (((colb >> 4) ^ swz_v(row)) << 4) + (colb & 15);
+      const int addr_hi = (row + 4) * ROWB + (((colb >> 4) ^ swz_v(row + 4)) << 4) + (colb & 15);
+      const v4s_t lo = lds_read_tr16(vs + addr_lo);
+      const v4s_t hi = lds_read_tr16(vs + addr_hi);
+      typedef short v8s_t __attribute__((ext_vector_type(8)));
+      v8s_t r8;
+      r8[0] = lo[0]; r8[1] = lo[1]; r8[2] = lo[2]; r8[3] = lo[3];
+      r8[4] = hi[0]; r8[5] = hi[1]; r8[6] = hi[2]; r8[7] = hi[3];
+      return __builtin_bit_cast(Frag<T>, r8);
+    };
+    Frag<T> ring[AH + 1];
+#pragma unroll
+    for (int a = 0; a < AH; ++a) ring[a] = frag(a);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      if (i + AH < N) ring[(i + AH) % (AH + 1)] = frag(i + AH);
+      const int k = i >> 1;
+      if ((i & 1) == 0) sc[k % NKT][0] = mma(ring[i % (AH + 1)], qf[0][k / NKT], sc[k % NKT][0]);
+      else acc[0][k % NDT] = mma(ring[i % (AH + 1)], pf_old[0][k / NDT], acc[0][k % NDT]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
   auto iteration = [&](auto mask_tag, int j, Frag<T> (&pf_old)[QT][NPC], Frag<T> (&pf_new)[QT][NPC])
                        __attribute__((always_inline)) {
     const unsigned char* kcur = kstage(j);
     const unsigned char* vprev = vstage(j + NSTAGE - 1);
     constexpr bool MASK = decltype(mask_tag)::value;
     mfma_phase_priority();
-    scores(kcur, s);
-    if constexpr (MASK) mask_sub(j, IntC<0>{}, s);
-    const float tsum0 = pv_weights0(vprev, pf_old, pf_new, s, -m_ref[0]);
-    if constexpr (W0 == NPC) finish_sub(IntC<0>{}, s, pf_new, tsum0);
-    // Only group 1 has copies in flight (two per wave per tile); the wait is
-    // a no-op for group 0.
-    if (j + 2 < n_tiles) wait_global_loads_upto<4>();
-    else if (j + 1 < n_tiles) wait_global_loads_upto<2>();
+    float tsum0 = 0.0f;
+    if constexpr (QT == 1 && W0 == 0) {
+      mfma_phase1(kcur, vprev, pf_old, s);
+    } else {
+      scores(kcur, s);
+      if constexpr (MASK) mask_sub(j, IntC<0>{}, s);
+      tsum0 = pv_weights0(vprev, pf_old, pf_new, s, -m_ref[0]);
+      if constexpr (W0 == NPC) finish_sub(IntC<0>{}, s, pf_new, tsum0);
+    }
+    // Only group 1 has copies in flight (UPW per wave, tile and tensor); the
+    // wait is a no-op for group 0.
+    if (j + 2 < n_tiles) wait_global_loads_upto<2 * UPW>();
+    else if (j + 1 < n_tiles) wait_global_loads_upto<UPW>();
     else wait_global_loads();
     barrier();
     valu_phase_priority();
+    if constexpr (QT == 1 && W0 == 0 && MASK) mask_sub(j, IntC<0>{}, s);
     if constexpr (W0 < NPC) finish_sub(IntC<0>{}, s, pf_new, tsum0 + weights(IntC<0>{}, s, pf_new, -m_ref[0], W0));
-    if constexpr (MASK) mask_sub(j, IntC<1>{}, s);
-    finish_sub(IntC<1>{}, s, pf_new, weights(IntC<1>{}, s, pf_new, -m_ref[1]));
+    if constexpr (QT == 2) {
+      if constexpr (MASK) mask_sub(j, IntC<QT - 1>{}, s);
+      finish_sub(IntC<QT - 1>{}, s, pf_new, weights(IntC<QT - 1>{}, s, pf_new, -m_ref[QT - 1]));
+    }
     if (grp == 1) issue(j);
     barrier();
   };
@@ -911,22 +1043,22 @@ static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
   return launch_combine<TO, DV>(p, stream);
 }
 
-template <typename T, typename TO, bool CAUSAL>
+template <typename T, typename TO, int D, bool CAUSAL>
 static hipError_t launch_fwd_pp(const FwdParams& p, hipStream_t stream) {
-  auto kern = attn_fwd_pp_kernel<T, TO, CAUSAL>;
+  auto kern = attn_fwd_pp_kernel<T, TO, D, CAUSAL>;
   const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
   FwdParams pc = p;
   void* args[] = {&pc};
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3((unsigned)grid),
                                  dim3(pp::NW * 64), args, 0, stream);
   if (e != hipSuccess || p.n_splits == 1) return e;
-  return launch_combine<TO, pp::D>(p, stream);
+  return launch_combine<TO, D>(p, stream);
 }
 
 template <typename T, typename TO, int D>
 static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t stream) {
-  if constexpr (sizeof(T) == 2 && D == 64 && FwdShape<T, D>::BQ == pp::BQ) {
-    return causal ? launch_fwd_pp<T, TO, true>(p, stream) : launch_fwd_pp<T, TO, false>(p, stream);
+  if constexpr (sizeof(T) == 2 && FwdShape<T, D>::BQ == pp::BQ<D>) {
+    return causal ? launch_fwd_pp<T, TO, D, true>(p, stream) : launch_fwd_pp<T, TO, D, false>(p, stream);
   } else {
     constexpr int QT = FwdShape<T, D>::QT, BK = FwdShape<T, D>::BK, OCC = FwdShape<T, D>::OCC;
     return causal ? launch_fwd_impl<T, TO, D, D, QT, BK, OCC, true>(p, stream)

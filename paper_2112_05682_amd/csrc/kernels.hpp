@@ -130,11 +130,18 @@ template <typename T, int D> struct FwdShape;
 template <> struct FwdShape<__bf16, 64> {
   static constexpr int BQ = MEA_T64_FWD_BQ, QT = BQ == 512 ? 2 : BQ / 128, BK = 64, OCC = MEA_T64_FWD_OCC;
 };
-template <> struct FwdShape<__bf16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128, OCC = 2; };
+// 16-bit d = 128: BQ = 256 selects the two-group kernel (8 waves of 32
+// queries); 128 the 4-wave kernel.  Problems with d_v != d always run the
+// 4-wave kernel with 128 queries per workgroup (kFwdBq4wave).
+#ifndef MEA_T128_FWD_BQ
+#define MEA_T128_FWD_BQ 256
+#endif
+constexpr int kFwdBq4wave128 = 128;
+template <> struct FwdShape<__bf16, 128> { static constexpr int QT = 1, BK = 64, BQ = MEA_T128_FWD_BQ, OCC = 2; };
 template <> struct FwdShape<_Float16, 64> {
   static constexpr int BQ = MEA_T64_FWD_BQ, QT = BQ == 512 ? 2 : BQ / 128, BK = 64, OCC = MEA_T64_FWD_OCC;
 };
-template <> struct FwdShape<_Float16, 128> { static constexpr int QT = 1, BK = 64, BQ = 128, OCC = 2; };
+template <> struct FwdShape<_Float16, 128> { static constexpr int QT = 1, BK = 64, BQ = MEA_T128_FWD_BQ, OCC = 2; };
 template <> struct FwdShape<float, 64> { static constexpr int QT = 1, BK = 32, BQ = 128, OCC = 2; };
 template <> struct FwdShape<float, 128> { static constexpr int QT = 1, BK = 32, BQ = 128, OCC = 2; };
 
