@@ -152,12 +152,52 @@ struct DkdvTile {
   static constexpr int UQ = (BQ * (CPRQ + 1) * 16 + 1023) / 1024;
   static constexpr int UO = (BQ * (CPRO + 1) * 16 + 1023) / 1024;
   static constexpr int ASTAGE_BYTES = (UQ + UO) * 1024 + 2 * BQ * 4;
-  static constexpr int stage_bytes(bool as) { return as ? ASTAGE_BYTES : STAGE_BYTES; }
+  // SWZ (asynchronous copies with d = d_v = 128): unpadded 256-byte rows whose
+  // 16-byte chunks are XOR-swizzled by the row (swz128), so that both the row
+  // fragment reads and the transposing reads of Q and dO are free of bank
+  // conflicts (a 16-byte row pad served the row reads only).
+  static constexpr bool swz(int occ, bool same_out) { return async(occ, same_out) && D == 128 && DV == 128; }
+  static constexpr int SUQ = BQ * CPRQ * 16 / 1024, SUO = BQ * CPRO * 16 / 1024;
+  static constexpr int SSTAGE_BYTES = (SUQ + SUO) * 1024 + 2 * BQ * 4;
+  static constexpr int stage_bytes(int occ, bool same_out) {
+    return swz(occ, same_out) ? SSTAGE_BYTES : (async(occ, same_out) ? ASTAGE_BYTES : STAGE_BYTES);
+  }
   static constexpr int lds_bytes(int occ, bool same_out) {
-    return 2 * stage_bytes(async(occ, same_out)) + (k_lds(occ) ? KSLOT_BYTES : 0);
+    return 2 * stage_bytes(occ, same_out) + (k_lds(occ) ? KSLOT_BYTES : 0);
   }
   static_assert(kBwdRowPad % BQ == 0, "query tiles must not pass the padded row count");
 };
+
+// Physical 16-byte chunk of logical chunk x in row r of a swizzled 256-byte
+// row tile is x ^ swz128(r): a permutation of the 16 chunks over any 16
+// consecutive rows (row fragment reads: 16 rows x one chunk per 16 lanes), and
+// 4 consecutive rows x 4 chunks land in 4 disjoint 4-chunk groups
+// (transposing reads).
+__device__ __forceinline__ int swz128(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+// Row fragment (8 elements at logical chunk x) of row r of a swizzled tile.
+template <typename T>
+__device__ __forceinline__ Frag<T> lds_frag_swz128(const T* tile, int r, int x) {
+  return *reinterpret_cast<const Frag<T>*>(reinterpret_cast<const unsigned char*>(tile) + r * 256 +
+                                           ((x ^ swz128(r)) << 4));
+}
+
+// Column fragment (as lds_col_frag) of a swizzled 256-byte row tile.
+template <typename T>
+__device__ __forceinline__ Frag<T> lds_col_frag_swz128(const T* tile, int row0, int col0, int lane) {
+  const int g = lane >> 4, i = lane & 15;
+  const int row = row0 + 8 * (g >> 1) + (i >> 2);
+  const int col = col0 + 16 * (g & 1) + 4 * (i & 3);
+  const unsigned char* b = reinterpret_cast<const unsigned char*>(tile);
+  const int off = (col & 7) << 1;
+  const v4s_t lo = lds_read_tr16(b + row * 256 + (((col >> 3) ^ swz128(row)) << 4) + off);
+  const v4s_t hi = lds_read_tr16(b + (row + 4) * 256 + (((col >> 3) ^ swz128(row + 4)) << 4) + off);
+  typedef short v8s_t __attribute__((ext_vector_type(8)));
+  v8s_t r8;
+  r8[0] = lo[0]; r8[1] = lo[1]; r8[2] = lo[2]; r8[3] = lo[3];
+  r8[4] = hi[0]; r8[5] = hi[1]; r8[6] = hi[2]; r8[7] = hi[3];
+  return __builtin_bit_cast(Frag<T>, r8);
+}
 
 template <typename T, typename TO, int D, int DV, int QS, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
@@ -195,9 +235,11 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   // ASYNC: the Q and dO tiles go global -> LDS by asynchronous copies instead
   // of through registers (only where dO needs no conversion).
   constexpr bool ASYNC = Cfg::async(OCC, __is_same(T, TO));
-  constexpr int STAGE_B = Cfg::stage_bytes(ASYNC);
-  constexpr int TILEQ_L = ASYNC ? Cfg::UQ * 1024 / Cfg::E : Cfg::TILEQ;  // dO tile offset (elements)
-  constexpr int INIT_OFF = ASYNC ? (Cfg::UQ + Cfg::UO) * 1024 : Cfg::STAGE_ELEMS * Cfg::E;
+  constexpr bool SWZ = Cfg::swz(OCC, __is_same(T, TO));
+  constexpr int STAGE_B = Cfg::stage_bytes(OCC, __is_same(T, TO));
+  constexpr int UQ = SWZ ? Cfg::SUQ : Cfg::UQ, UO = SWZ ? Cfg::SUO : Cfg::UO;  // 1 KiB copy units
+  constexpr int TILEQ_L = ASYNC ? UQ * 1024 / Cfg::E : Cfg::TILEQ;  // dO tile offset (elements)
+  constexpr int INIT_OFF = ASYNC ? (UQ + UO) * 1024 : Cfg::STAGE_ELEMS * Cfg::E;
   T* const kslot = reinterpret_cast<T*>(smem_raw + 2 * STAGE_B) + 8 * tid;
   Frag<T> kf[K_LDS ? 1 : KC], vf[KCV];
 #pragma unroll
@@ -310,20 +352,29 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   // the tile's rows and rows past n_q copy the last valid row (finite values;
   // those queries start at -inf, so their weights are 0).  Wave w issues units
   // w, w + 4, ...; the per-row initial values go through a register as above.
+  // SWZ: unit u holds rows 4u .. 4u + 3; the lane writing physical chunk
+  // x = lane % 16 of row r fetches logical chunk x ^ swz128(r).
   auto copy_stage = [&](int64_t q0, int buf) __attribute__((always_inline)) {
-    for (int u = __builtin_amdgcn_readfirstlane(wave); u < Cfg::UQ + Cfg::UO; u += 4) {
-      const bool is_o = u >= Cfg::UQ;
-      const int uu = is_o ? u - Cfg::UQ : u;
+    for (int u = __builtin_amdgcn_readfirstlane(wave); u < UQ + UO; u += 4) {
+      const bool is_o = u >= UQ;
+      const int uu = is_o ? u - UQ : u;
       const int cpr = is_o ? Cfg::CPRO : Cfg::CPRQ;
-      const int slot = 64 * uu + lane;
-      int row = slot / (cpr + 1), ch = slot % (cpr + 1);
-      if (ch == cpr) ch = cpr - 1;
-      if (row > Cfg::BQ - 1) row = Cfg::BQ - 1;
+      int row, ch;
+      if constexpr (SWZ) {
+        row = 4 * uu + (lane >> 4);
+        ch = (lane & 15) ^ swz128(row);
+      } else {
+        const int slot = 64 * uu + lane;
+        row = slot / (cpr + 1);
+        ch = slot % (cpr + 1);
+        if (ch == cpr) ch = cpr - 1;
+        if (row > Cfg::BQ - 1) row = Cfg::BQ - 1;
+      }
       int64_t q = q0 + row;
       if (q > p.n_q - 1) q = p.n_q - 1;
       const T* src = (is_o ? reinterpret_cast<const T*>(dog) + q * p.sdo.r : qg + q * p.sq.r) + ch * (16 / Cfg::E);
       const unsigned dst = __builtin_amdgcn_readfirstlane(
-          lds_addr(stage_base(buf) + (is_o ? Cfg::UQ * 1024 : 0) + 1024 * uu));
+          lds_addr(stage_base(buf) + (is_o ? UQ * 1024 : 0) + 1024 * uu));
       copy_to_lds16(src, dst);
     }
     if (tid < 2 * Cfg::BQ) {
@@ -388,11 +439,13 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
 #pragma unroll
         for (int qs = 0; qs < QS; ++qs) {
           if (kc < KC) {
-            const Frag<T> a = lds_frag<T>(qs_t + (32 * qs + qrow) * RSQ + 16 * kc + 8 * h);
+            const Frag<T> a = SWZ ? lds_frag_swz128<T>(qs_t, 32 * qs + qrow, 2 * kc + h)
+                                  : lds_frag<T>(qs_t + (32 * qs + qrow) * RSQ + 16 * kc + 8 * h);
             s[qs] = mma(a, kfrag(kc), s[qs]);
           }
           if (kc < KCV) {
-            const Frag<T> g = lds_frag<T>(dos_t + (32 * qs + qrow) * RSO + 16 * kc + 8 * h);
+            const Frag<T> g = SWZ ? lds_frag_swz128<T>(dos_t, 32 * qs + qrow, 2 * kc + h)
+                                  : lds_frag<T>(dos_t + (32 * qs + qrow) * RSO + 16 * kc + 8 * h);
             dp[qs] = mma(g, vf[kc], dp[qs]);
           }
         }
@@ -424,7 +477,9 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
         for (int dt = 0; dt < (NDT > NDTV ? NDT : NDTV); ++dt) {
           if (dt < NDTV) {
             Frag<T> bo;
-            if constexpr (sizeof(T) == 2) {
+            if constexpr (SWZ) {
+              bo = lds_col_frag_swz128<T>(dos_t, 16 * qc, 32 * dt, lane);
+            } else if constexpr (sizeof(T) == 2) {
               bo = lds_col_frag<T>(dos_t, RSO, 16 * qc, 32 * dt, lane);
             } else {
               bo = lds_col_frag_f32(reinterpret_cast<const float*>(dos_t), RSO, 16 * qc, 32 * dt, lane);
@@ -433,7 +488,9 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
           }
           if (dt < NDT) {
             Frag<T> bq;
-            if constexpr (sizeof(T) == 2) {
+            if constexpr (SWZ) {
+              bq = lds_col_frag_swz128<T>(qs_t, 16 * qc, 32 * dt, lane);
+            } else if constexpr (sizeof(T) == 2) {
               bq = lds_col_frag<T>(qs_t, RSQ, 16 * qc, 32 * dt, lane);
             } else {
               bq = lds_col_frag_f32(reinterpret_cast<const float*>(qs_t), RSQ, 16 * qc, 32 * dt, lane);
@@ -950,7 +1007,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   constexpr int NT = 256;
   constexpr int BQ = 128 * QT;  // 4 waves x QT x 32 queries
   constexpr int E = sizeof(T);
-  constexpr int RSK = D + 16 / E, RSV = DV + 16 / E;  // LDS row strides (elements)
+  constexpr int RSK = D + 16 / E, RSV = DV + 16 / E;  // LDS row strides (elements), 16 B pad
   constexpr int TILEK = BK * RSK, TILEV = BK * RSV;
   constexpr int CPRK = D * E / 16, CPRV = DV * E / 16;
   constexpr int CHUNKS = BK * (CPRK + CPRV);
