@@ -354,7 +354,36 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   // w, w + 4, ...; the per-row initial values go through a register as above.
   // SWZ: unit u holds rows 4u .. 4u + 3; the lane writing physical chunk
   // x = lane % 16 of row r fetches logical chunk x ^ swz128(r).
+  // SWZ with a full tile (q0 + BQ <= n_q, every tile but a ragged last one):
+  // wave w copies Q units w and w + 4 and dO units w and w + 4, i.e. rows
+  // 4w + lane / 16 and 16 rows further, whose swizzle is the same; the per-lane
+  // byte offsets are computed once and the tile's first row is a scalar base,
+  // so these copies cost no vector instructions.
+  constexpr bool SWZ_FAST = SWZ && UQ == 8 && UO == 8;
+  const int crow = 4 * wave + (lane >> 4);
+  const unsigned cch = (unsigned)(((lane & 15) ^ swz128(crow)) * 16);
+  const unsigned qoff = (unsigned)(crow * p.sq.r) * Cfg::E + cch;
+  const unsigned doff = (unsigned)(crow * p.sdo.r) * Cfg::E + cch;
   auto copy_stage = [&](int64_t q0, int buf) __attribute__((always_inline)) {
+    if constexpr (SWZ_FAST) {
+      if (q0 + Cfg::BQ <= p.n_q) {
+        const T* qb = qg + q0 * p.sq.r;
+        const T* db = reinterpret_cast<const T*>(dog) + q0 * p.sdo.r;
+        const T* qb16 = qb + 16 * p.sq.r;
+        const T* db16 = db + 16 * p.sdo.r;
+        const unsigned dst =
+            __builtin_amdgcn_readfirstlane(lds_addr(stage_base(buf)) + 1024u * (unsigned)wave);
+        copy_to_lds16_sb(qb, qoff, dst);
+        copy_to_lds16_sb(qb16, qoff, dst + 4096u);
+        copy_to_lds16_sb(db, doff, dst + 8192u);
+        copy_to_lds16_sb(db16, doff, dst + 12288u);
+        if (tid < 2 * Cfg::BQ) {
+          const int64_t q = q0 + (tid % Cfg::BQ);
+          stage_fa = tid < Cfg::BQ ? sinitg[q] : dpinitg[q];
+        }
+        return;
+      }
+    }
     for (int u = __builtin_amdgcn_readfirstlane(wave); u < UQ + UO; u += 4) {
       const bool is_o = u >= UQ;
       const int uu = is_o ? u - UQ : u;
@@ -451,13 +480,25 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
         }
       }
       const bool need_mask = CAUSAL && q0 < kw + 31;
+      // The mask applies to the tiles on the diagonal only: a uniform branch
+      // keeps its compares out of the other tiles (the empty volatile
+      // statement keeps the compiler from turning it into selects).  A masked
+      // score becomes -inf, so its weight 2^(c S) is exactly 0.
+      if (need_mask) {
+        asm volatile("");
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs) {
+          const int key_rel = (int)(key - q0);  // key minus the tile's first query
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (key_rel > 32 * qs + permuted_row(r, h)) s[qs][r] = -INFINITY;
+        }
+      }
 #pragma unroll
       for (int qs = 0; qs < QS; ++qs) {
-        const int key_rel = (int)(key - q0);  // key minus the tile's first query
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float pr = fast_exp2(s[qs][r] * cl2);
-          if (need_mask && key_rel > 32 * qs + permuted_row(r, h)) pr = 0.0f;
+          const float pr = fast_exp2(s[qs][r] * cl2);
           s[qs][r] = pr;                // P
           dp[qs][r] = pr * dp[qs][r];   // dS = P (dP - D)
         }
@@ -1002,6 +1043,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
 
 // ------------------------------------------------------------------- dQ
 // D: head dimension of q and k; DV: of v and dO.
+#ifndef MEA_T128_DQ_SWZ
+#define MEA_T128_DQ_SWZ 1
+#endif
 template <typename T, typename TO, int D, int DV, int QT, int BK, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   constexpr int NT = 256;
@@ -1017,6 +1061,12 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   constexpr int NKT = BK / 32;
   constexpr int NPC = BK / 16;
   constexpr int NDT = D / 32;
+  // SWZ (16-bit, d = d_v = 128, 32-key tiles): the K and V tiles go global ->
+  // LDS by asynchronous copies into unpadded 256-byte rows whose 16-byte
+  // chunks are XOR-swizzled by the row (swz128), which keeps the row and the
+  // transposing reads free of bank conflicts and frees the staging registers.
+  constexpr bool SWZ = MEA_T128_DQ_SWZ && sizeof(T) == 2 && D == 128 && DV == 128 && BK == 32;
+  constexpr int TK = SWZ ? BK * D : TILEK, TV = SWZ ? BK * DV : TILEV;  // tile sizes (elements)
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* smem = reinterpret_cast<T*>(smem_raw);
@@ -1119,14 +1169,51 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
     }
   };
 
+  // SWZ copies: a tile is 8 K units and 8 V units of 1 KiB (4 rows each);
+  // wave w copies units w and w + 4 of both, i.e. rows 4w + lane / 16 and 16
+  // rows further, which share their swizzle.  Full tiles take a scalar base
+  // and per-lane byte offsets computed once; in a ragged last tile rows past
+  // n_k copy row n_k - 1 (finite values whose weights are masked to 0).
+  const int crow = 4 * wave + (lane >> 4);
+  const int cchunk = (lane & 15) ^ swz128(crow);
+  const unsigned koff = (unsigned)(crow * p.sk.r) * E + 16u * (unsigned)cchunk;
+  const unsigned voff = (unsigned)(crow * p.sv.r) * E + 16u * (unsigned)cchunk;
+  auto copy_tile = [&](int64_t k0, int buf) __attribute__((always_inline)) {
+    const unsigned dst =
+        __builtin_amdgcn_readfirstlane(lds_addr(smem + buf * (TK + TV)) + 1024u * (unsigned)wave);
+    if (k0 + BK <= p.n_k) {
+      const T* kb = kg + k0 * p.sk.r;
+      const T* vb = vg + k0 * p.sv.r;
+      copy_to_lds16_sb(kb, koff, dst);
+      copy_to_lds16_sb(kb + 16 * p.sk.r, koff, dst + 4096u);
+      copy_to_lds16_sb(vb, voff, dst + 8192u);
+      copy_to_lds16_sb(vb + 16 * p.sv.r, voff, dst + 12288u);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        int64_t kr = k0 + crow + 16 * j;
+        if (kr > p.n_k - 1) kr = p.n_k - 1;
+        copy_to_lds16(kg + kr * p.sk.r + 8 * cchunk, dst + 4096u * j);
+        copy_to_lds16(vg + kr * p.sv.r + 8 * cchunk, dst + 8192u + 4096u * j);
+      }
+    }
+  };
+
   const int krow = perm32(c);
   const float cl2 = p.scale_log2;
 
-  if (n_tiles > 0) {
-    load_stage(BoolC<false>{}, 0);
-    store_stage(BoolC<false>{}, 0);
+  if constexpr (SWZ) {
+    if (n_tiles > 0) {
+      copy_tile(0, 0);
+      wait_global_loads();
+    }
+  } else {
+    if (n_tiles > 0) {
+      load_stage(BoolC<false>{}, 0);
+      store_stage(BoolC<false>{}, 0);
+    }
+    if (PF == 2 && n_tiles > 1) load_stage(BoolC<true>{}, BK);
   }
-  if (PF == 2 && n_tiles > 1) load_stage(BoolC<true>{}, BK);
   __syncthreads();
 
   // Leading tiles that need no mask (all keys exist and, causal, precede the
@@ -1141,8 +1228,8 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   auto tile = [&](auto mask_tag, int it) {
     constexpr bool MASK = decltype(mask_tag)::value;
     const int64_t k0 = (int64_t)it * BK;
-    const T* ks = smem + (it & 1) * (TILEK + TILEV);
-    const T* vs = ks + TILEK;
+    const T* ks = smem + (it & 1) * (TK + TV);
+    const T* vs = ks + TK;
     if (MASK && CAUSAL && k0 > qw + 32 * QT - 1) return;  // all keys after this wave's queries
     f32x16 s[NKT][QT], dp[NKT][QT];
 #pragma unroll
@@ -1161,12 +1248,14 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt) {
         if (kc < KC) {
-          const Frag<T> a = lds_frag<T>(ks + (32 * kt + krow) * RSK + 16 * kc + 8 * h);
+          const Frag<T> a = SWZ ? lds_frag_swz128<T>(ks, 32 * kt + krow, 2 * kc + h)
+                                : lds_frag<T>(ks + (32 * kt + krow) * RSK + 16 * kc + 8 * h);
 #pragma unroll
           for (int t = 0; t < QT; ++t) s[kt][t] = mma(a, qf[t][kc], s[kt][t]);
         }
         if (kc < KCV) {
-          const Frag<T> b = lds_frag<T>(vs + (32 * kt + krow) * RSV + 16 * kc + 8 * h);
+          const Frag<T> b = SWZ ? lds_frag_swz128<T>(vs, 32 * kt + krow, 2 * kc + h)
+                                : lds_frag<T>(vs + (32 * kt + krow) * RSV + 16 * kc + 8 * h);
 #pragma unroll
           for (int t = 0; t < QT; ++t) dp[kt][t] = mma(b, gf[t][kc], dp[kt][t]);
         }
@@ -1205,7 +1294,9 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) {
         Frag<T> a;
-        if constexpr (sizeof(T) == 2) {
+        if constexpr (SWZ) {
+          a = lds_col_frag_swz128<T>(ks, 16 * pc, 32 * dt, lane);
+        } else if constexpr (sizeof(T) == 2) {
           a = lds_col_frag<T>(ks, RSK, 16 * pc, 32 * dt, lane);
         } else {
           a = lds_col_frag_f32(reinterpret_cast<const float*>(ks), RSK, 16 * pc, 32 * dt, lane);
@@ -1221,6 +1312,13 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   // loaded into set A in this iteration.
   auto step = [&](auto mask_tag, auto odd_tag, int it) __attribute__((always_inline)) {
     constexpr bool ODD = decltype(odd_tag)::value;
+    if constexpr (SWZ) {
+      if (it + 1 < n_tiles) copy_tile((int64_t)(it + 1) * BK, (it + 1) & 1);
+      tile(mask_tag, it);
+      if (it + 1 < n_tiles) wait_global_loads();
+      __syncthreads();
+      return;
+    }
     if constexpr (PF == 2) {
       if (it + 2 < n_tiles) load_stage(BoolC<ODD>{}, (int64_t)(it + 2) * BK);
     } else {
