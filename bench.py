@@ -327,10 +327,34 @@ def bench_decode(dev, calls: int = 100, warmup: int = 5):
     nbytes = bh * (4 * w.n_k * w.d + 4 * w.n_q * w.d + 4 * w.n_q)
     gbs = nbytes / (ms * 1e-3) / 1e9
     del x
-    return {"workload": w.name, "kernel": "attn_decode_kernel", "bound": "hbm", "calls": calls,
-            "median_ms": round(ms, 4), "algorithmic_bytes": nbytes, "achieved": round(gbs, 1),
-            "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-            "traffic": load_traffic("attn_decode_kernel", w.name), "includes": "combine of the key ranges"}
+    out = {"workload": w.name, "kernel": "attn_decode_kernel", "bound": "hbm", "calls": calls,
+           "median_ms": round(ms, 4), "algorithmic_bytes": nbytes, "achieved": round(gbs, 1),
+           "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+           "traffic": load_traffic("attn_decode_kernel", w.name), "includes": "combine of the key ranges"}
+    ceiling = read_ceiling()
+    if ceiling:
+        out["read_ceiling"] = ceiling
+        out["frac_of_read_ceiling"] = round(gbs / ceiling["GBps"], 4)
+    return out
+
+
+def read_ceiling():
+    """Best streaming-read rate of a plain read kernel (tests/native/hbm_read:
+    2 GiB read once with 16-byte loads, several launch shapes) in a child
+    process: the practical HBM ceiling for a kernel that reads K and V once."""
+    exe = os.path.join(ROOT, "tests", "native", "hbm_read")
+    if not os.path.exists(exe):
+        return None
+    try:
+        r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    except subprocess.TimeoutExpired:
+        return None
+    lines = [json.loads(l) for l in r.stdout.splitlines() if l.startswith("{")]
+    if r.returncode != 0 or not lines or "best_shape" not in lines[-1]:
+        return None
+    best = lines[-1]
+    return {"tool": "tests/native/hbm_read", "shape": best["best_shape"], "GBps": best["GBps"],
+            "frac_of_8TBps": best["frac_of_8TBps"]}
 
 
 def bench_key_padding(dev, calls: int = 10, warmup: int = 2):

@@ -112,8 +112,8 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
     if (k0 + BK <= ke) {
 #pragma unroll
       for (int u = 0; u < C::NCOPY; ++u) {
-        copy_to_lds16_sb(kg + k0 * p.sk.r, ukoff[u], __builtin_amdgcn_readfirstlane(kl + 1024 * u));
-        copy_to_lds16_sb(vg + k0 * p.sv.r, uvoff[u], __builtin_amdgcn_readfirstlane(vl + 1024 * u));
+        copy_to_lds16_sb<true>(kg + k0 * p.sk.r, ukoff[u], __builtin_amdgcn_readfirstlane(kl + 1024 * u));
+        copy_to_lds16_sb<true>(vg + k0 * p.sv.r, uvoff[u], __builtin_amdgcn_readfirstlane(vl + 1024 * u));
       }
     } else {
       // Ragged last tile: rows past the range repeat its last key (finite
@@ -122,10 +122,10 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
       for (int u = 0; u < C::NCOPY; ++u) {
         int64_t key = k0 + urow[u];
         if (key > ke - 1) key = ke - 1;
-        copy_to_lds16(reinterpret_cast<const unsigned char*>(kg + key * p.sk.r) + ucol[u],
-                      __builtin_amdgcn_readfirstlane(kl + 1024 * u));
-        copy_to_lds16(reinterpret_cast<const unsigned char*>(vg + key * p.sv.r) + ucol[u],
-                      __builtin_amdgcn_readfirstlane(vl + 1024 * u));
+        copy_to_lds16<true>(reinterpret_cast<const unsigned char*>(kg + key * p.sk.r) + ucol[u],
+                            __builtin_amdgcn_readfirstlane(kl + 1024 * u));
+        copy_to_lds16<true>(reinterpret_cast<const unsigned char*>(vg + key * p.sv.r) + ucol[u],
+                            __builtin_amdgcn_readfirstlane(vl + 1024 * u));
       }
     }
   };

