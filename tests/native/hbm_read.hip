@@ -1,6 +1,7 @@
-// Streaming-read ceiling of the GPU's HBM: a plain kernel that reads a 2 GiB
+// Streaming-read ceiling of the GPU's HBM: plain kernels that read a 2 GiB
 // buffer once with 16-byte loads (each workgroup one contiguous chunk, UNR
-// loads in flight per thread) and writes one word per thread.  It serves as
+// loads in flight per thread, or asynchronous copies into an LDS ring) and
+// write one word per thread.  It serves as
 // the practical upper bound against which the decode-shaped forward (which
 // reads K and V once) is judged; it computes nothing of the attention path.
 //
@@ -29,6 +30,42 @@ __global__ __launch_bounds__(256) void read_chunks(const u32x4* __restrict__ src
   out[(size_t)blockIdx.x * 256 + threadIdx.x] = acc;
 }
 
+// The same read through asynchronous global -> LDS copies
+// (global_load_lds_dwordx4, the path the decode kernel uses), one wave per
+// workgroup: each 1 KiB unit lands in a RING-slot LDS ring, and the wave
+// waits for the older half of the ring before reusing it.  NT selects the
+// non-temporal cache policy.
+template <int RING, bool NT>
+__global__ __launch_bounds__(64) void read_to_lds(const u32x4* __restrict__ src, unsigned* __restrict__ out,
+                                                  size_t per_wg) {
+  __shared__ __align__(16) unsigned char ring[RING * 1024];
+  const int lane = threadIdx.x;
+  const u32x4* p = src + (size_t)blockIdx.x * per_wg;
+  const size_t units = per_wg / 64;
+  const unsigned base = (unsigned)(size_t)ring;
+  for (size_t u = 0; u < units; ++u) {
+    const void* a = p + u * 64 + lane;
+    const unsigned dst = __builtin_amdgcn_readfirstlane(base + (unsigned)(u % RING) * 1024u);
+    if (NT)
+      asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
+                   :
+                   : "v"(a), "s"(dst)
+                   : "memory", "m0");
+    else
+      asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                   :
+                   : "v"(a), "s"(dst)
+                   : "memory", "m0");
+    // vmcnt(RING / 2) after every half ring: the slots about to be reused are free.
+    // (vmcnt bits 3:0 and 15:14; expcnt and lgkmcnt left unconstrained)
+    if (u % (RING / 2) == RING / 2 - 1)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | ((RING / 2) & 15) | (((RING / 2) >> 4) << 14));
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  out[(size_t)blockIdx.x * 64 + lane] = reinterpret_cast<const unsigned*>(ring)[lane];
+}
+
 #define CHECK(x)                                                            \
   do {                                                                      \
     hipError_t e_ = (x);                                                    \
@@ -40,7 +77,7 @@ __global__ __launch_bounds__(256) void read_chunks(const u32x4* __restrict__ src
 
 struct Shape {
   const char* name;
-  int wgs, unr;
+  int wgs, unr, threads;  // unr: 16-byte loads per thread and round (ring slots for the LDS path)
   void (*kernel)(const u32x4*, unsigned*, size_t);
 };
 
@@ -56,17 +93,23 @@ int main() {
   CHECK(hipEventCreate(&a));
   CHECK(hipEventCreate(&b));
   const Shape shapes[] = {
-      {"wg2048_unr8", 2048, 8, read_chunks<8, false>},   {"wg4096_unr8", 4096, 8, read_chunks<8, false>},
-      {"wg8192_unr8", 8192, 8, read_chunks<8, false>},   {"wg16384_unr8", 16384, 8, read_chunks<8, false>},
-      {"wg8192_unr16", 8192, 16, read_chunks<16, false>}, {"wg8192_unr8_nt", 8192, 8, read_chunks<8, true>},
-      {"wg2048_unr8_nt", 2048, 8, read_chunks<8, true>},
+      {"wg2048_unr8", 2048, 8, 256, read_chunks<8, false>},
+      {"wg4096_unr8", 4096, 8, 256, read_chunks<8, false>},
+      {"wg8192_unr8", 8192, 8, 256, read_chunks<8, false>},
+      {"wg16384_unr8", 16384, 8, 256, read_chunks<8, false>},
+      {"wg8192_unr16", 8192, 16, 256, read_chunks<16, false>},
+      {"wg8192_unr8_nt", 8192, 8, 256, read_chunks<8, true>},
+      {"wg2048_unr8_nt", 2048, 8, 256, read_chunks<8, true>},
+      {"lds_wg2048_ring16", 2048, 16, 64, read_to_lds<16, false>},
+      {"lds_wg2048_ring16_nt", 2048, 16, 64, read_to_lds<16, true>},
+      {"lds_wg4096_ring32_nt", 4096, 32, 64, read_to_lds<32, true>},
   };
   double best = 0.0;
   const char* best_name = "";
   for (const Shape& s : shapes) {
     // Every shape divides the buffer into equal chunks of whole load rounds.
     const size_t per_wg = n16 / (size_t)s.wgs;
-    if (s.wgs > max_wgs || per_wg * (size_t)s.wgs != n16 || per_wg % (size_t)(256 * s.unr) != 0) {
+    if (s.wgs > max_wgs || per_wg * (size_t)s.wgs != n16 || per_wg % (size_t)(s.threads * s.unr) != 0) {
       fprintf(stderr, "shape %s does not tile the buffer\n", s.name);
       return 1;
     }
@@ -74,7 +117,7 @@ int main() {
     float times[reps];
     for (int r = 0; r < warm + reps; ++r) {
       CHECK(hipEventRecord(a, 0));
-      hipLaunchKernelGGL(s.kernel, dim3((unsigned)s.wgs), dim3(256), 0, 0, src, out, per_wg);
+      hipLaunchKernelGGL(s.kernel, dim3((unsigned)s.wgs), dim3((unsigned)s.threads), 0, 0, src, out, per_wg);
       CHECK(hipGetLastError());
       CHECK(hipEventRecord(b, 0));
       CHECK(hipEventSynchronize(b));
