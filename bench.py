@@ -408,6 +408,9 @@ ORACLE_SAMPLES = {
                        "the fp32 1x1x256x256 d = 64 workload in full, forward + backward"),
     "bf16_h8_n4096_fwd_full": (1, 8, 4096, 4096, 64, "bf16", False, False,
                                "the bf16 1x8x4096x4096 d = 64 workload in full, forward"),
+    "causal_d128_1slice": (1, 1, 8192, 8192, 128, "bf16", True, True,
+                           "1 of the 128 (batch, head) slices of the causal 4x32x8192 d = 128 workload, "
+                           "float64 forward + backward"),
 }
 
 
@@ -416,7 +419,7 @@ def oracle_sample(name: str) -> dict:
     from paper_2112_05682_amd.inputs import attention_inputs
 
     B, H, nq, nk, d, dtype, causal, bwd, desc = ORACLE_SAMPLES[name]
-    x = attention_inputs(B, H, nq, nk, d, dtype, with_grad=bwd)
+    x = attention_inputs(B, H, nq, nk, d, dtype, std=0.5 if causal and d == 128 else 1.0, with_grad=bwd)
     arrs = {k_: t.double().numpy() for k_, t in x.items()}
     t0 = time.perf_counter()
     oracle.fwd(arrs["q"], arrs["k"], arrs["v"], scale=d ** -0.5, causal=causal)
@@ -427,6 +430,29 @@ def oracle_sample(name: str) -> dict:
     flops = (14.0 if bwd else 4.0) * d * pairs
     return {"sample": desc, "seconds": round(dt, 3), "threads": oracle.num_threads(),
             "gflops": round(flops / dt / 1e9, 3), "credited_flop": flops}
+
+
+def oracle_longkv_rows(n_rows: int = 512) -> dict:
+    """The long-key workload's forward (1 head, n_q = 16384, n_k = 2^20,
+    d = 64) on n_rows query rows spread evenly over all query positions
+    (rows are independent in the forward)."""
+    import numpy as np
+
+    import oracle
+    from paper_2112_05682_amd.inputs import WORKLOADS, workload_inputs
+
+    w = WORKLOADS[LONGKV]
+    x = workload_inputs(w, with_grad=False)
+    q, k, v = (x[n][0, 0].double().numpy() for n in ("q", "k", "v"))
+    rows = np.linspace(0, w.n_q - 1, n_rows).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.fwd_rows(q, k, v, rows, scale=w.d ** -0.5, causal=w.causal)
+    dt = time.perf_counter() - t0
+    flops = 4.0 * w.d * n_rows * w.n_k
+    return {"sample": "%d of the %d query rows of the long-key workload (n_k = 2^20, d = 64), spread over all "
+                      "positions, float64 forward" % (n_rows, w.n_q),
+            "seconds": round(dt, 3), "threads": oracle.num_threads(), "gflops": round(flops / dt / 1e9, 3),
+            "credited_flop": flops}
 
 
 def cpu_model() -> str:
@@ -444,7 +470,9 @@ def cpu_model() -> str:
 def cpu_baseline() -> dict:
     all_core = oracle_sample("headline_2heads")
     extra = {"fp32_n256_full": oracle_sample("fp32_n256_full"),
-             "bf16_h8_n4096_fwd_full": oracle_sample("bf16_h8_n4096_fwd_full")}
+             "bf16_h8_n4096_fwd_full": oracle_sample("bf16_h8_n4096_fwd_full"),
+             "causal_d128_1slice": oracle_sample("causal_d128_1slice"),
+             "longkv_512rows": oracle_longkv_rows()}
     import oracle
 
     n_all = oracle.num_threads()
@@ -464,7 +492,7 @@ def cpu_baseline() -> dict:
         "host_threads": os.cpu_count(),
         "omp_num_threads_env": os.environ.get("OMP_NUM_THREADS"),
         "one_thread": one,
-        "full_small_workloads": extra,
+        "other_workloads": extra,
     }
 
 
