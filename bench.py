@@ -575,6 +575,24 @@ def main() -> int:
         clock = cs.summary()
         clock["during"] = "%d back-to-back steps of the headline workload (%.1f s)" % (
             n_clk, n_clk * ms_step / 1e3)
+        # The same for each kernel alone (half the time each): the clock and
+        # power the chip settles at under that kernel's instruction mix.
+        o1, l1, lo1 = attention_fwd(q, k, v, causal=w.causal, residual=True)
+        alone = {"fwd": lambda: attention_fwd(q, k, v, causal=w.causal),
+                 "bwd_dkdv": lambda: attention_bwd(q, k, v, o1, l1, do, causal=w.causal, need_dq=False, o_lo=lo1),
+                 "bwd_dq": lambda: attention_bwd(q, k, v, o1, l1, do, causal=w.causal, need_dkdv=False, o_lo=lo1)}
+        clock["per_kernel"] = {}
+        for name_, fn in alone.items():
+            n_k_ = max(1, int(args.clock_seconds * 0.5e3 / kernels[name_]["median_ms"]))
+            with ClockSampler() as cs:
+                time.sleep(0.3)
+                for _ in range(n_k_):
+                    fn()
+                torch.cuda.synchronize()
+            ks_ = cs.summary()
+            ks_["during"] = "%d back-to-back calls (%.1f s)" % (n_k_, n_k_ * kernels[name_]["median_ms"] / 1e3)
+            clock["per_kernel"][name_] = ks_
+        del o1, l1, lo1
 
     p = _lib.problem(w.batch, w.heads, w.n_q, w.n_k, w.d, _lib.MEA_BF16, w.causal, w.d ** -0.5)
     lib_ws = max(_lib.fwd_workspace_size(p), _lib.bwd_workspace_size(p))
