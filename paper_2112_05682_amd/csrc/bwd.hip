@@ -1832,7 +1832,10 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   void* args[] = {&p};
   const int64_t rows = (int64_t)p.bh * p.n_q_pad;
   constexpr int RPB = 256 / (DV * (int)sizeof(TO) / 16);
-  constexpr bool PP = sizeof(T) == 2 && D == 64 && DV == 64 && __is_same(T, TO);
+  constexpr bool PP = bwd_two_group(sizeof(T) == 2, D, DV, __is_same(T, TO), CAUSAL);
+  // The per-row values must be laid out as these kernels read them (records
+  // or two arrays): a plan that disagrees is refused, not launched.
+  if (PP ? p.row_rec == nullptr : (p.s_init == nullptr || p.dp_init == nullptr)) return hipErrorInvalidValue;
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, PP>),
                                  dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
   if (e != hipSuccess) return e;

@@ -1045,6 +1045,8 @@ template <typename T, typename TO, int D, int DV, int QT, int BK, int OCC, bool 
 static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
   using Cfg = FwdTile<T, D, DV, QT, BK>;
   auto kern = attn_fwd_kernel<T, TO, D, DV, QT, BK, OCC, CAUSAL>;
+  // The plan's query tiles must be this kernel's (4 waves x QT x 32 queries).
+  if (p.n_qtiles != (p.n_q + 128 * QT - 1) / (128 * QT)) return hipErrorInvalidValue;
   const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
   FwdParams pc = p;
   void* args[] = {&pc};
@@ -1057,6 +1059,7 @@ static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
 template <typename T, typename TO, int D, bool CAUSAL>
 static hipError_t launch_fwd_pp(const FwdParams& p, hipStream_t stream) {
   auto kern = attn_fwd_pp_kernel<T, TO, D, CAUSAL>;
+  if (p.n_qtiles != (p.n_q + pp::BQ<D> - 1) / pp::BQ<D>) return hipErrorInvalidValue;
   const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
   FwdParams pc = p;
   void* args[] = {&pc};
@@ -1069,7 +1072,13 @@ static hipError_t launch_fwd_pp(const FwdParams& p, hipStream_t stream) {
 template <typename T, typename TO, int D>
 static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t stream) {
   if constexpr (sizeof(T) == 2 && FwdShape<T, D>::BQ == pp::BQ<D>) {
-    return causal ? launch_fwd_pp<T, TO, D, true>(p, stream) : launch_fwd_pp<T, TO, D, false>(p, stream);
+    if (!causal) return launch_fwd_pp<T, TO, D, false>(p, stream);
+    if constexpr (D == 64) {
+      // Short causal problems: the 4-wave kernel with 128-query workgroups.
+      if (fwd_causal64_bq(p.n_q) == 128)
+        return launch_fwd_impl<T, TO, 64, 64, 1, FwdShape<T, 64>::BK, MEA_T64_FWD_OCC, true>(p, stream);
+    }
+    return launch_fwd_pp<T, TO, D, true>(p, stream);
   } else {
     constexpr int QT = FwdShape<T, D>::QT, BK = FwdShape<T, D>::BK, OCC = FwdShape<T, D>::OCC;
     return causal ? launch_fwd_impl<T, TO, D, D, QT, BK, OCC, true>(p, stream)

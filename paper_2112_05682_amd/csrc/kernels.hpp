@@ -108,11 +108,21 @@ struct BwdParams {
 // tile the backward kernels stage).
 constexpr int kBwdRowPad = 64;
 
-// Whether the backward of a problem runs the two-group kernels, which take
-// the per-row values as records (dtype: 0 float32, 1 fp16, 2 bf16; d and dv
-// the head dimensions of q, k and of v, o).
-inline bool bwd_uses_row_records(int dtype, int d, int dv, bool out_f32) {
-  return dtype != 0 && d == 64 && dv == 64 && !out_f32;
+// Whether the backward runs the two-group kernels, which take the per-row
+// values as 16-byte records; every other backward takes them as two float32
+// arrays.  The host's workspace layout and the kernels' choice both come from
+// this one predicate.  MEA_T64_BWD_CAUSAL_PP = 0 sends causal problems to
+// the 4-wave kernels instead (a build-time experiment).
+#ifndef MEA_T64_BWD_CAUSAL_PP
+#define MEA_T64_BWD_CAUSAL_PP 1
+#endif
+constexpr bool bwd_two_group(bool is16, int d, int dv, bool same_out_dtype, bool causal) {
+  return is16 && d == 64 && dv == 64 && same_out_dtype && (!causal || MEA_T64_BWD_CAUSAL_PP);
+}
+// dtype: 0 float32, 1 fp16, 2 bf16; d and dv the head dimensions of q, k and
+// of v, o.
+inline bool bwd_uses_row_records(int dtype, int d, int dv, bool out_f32, bool causal) {
+  return bwd_two_group(dtype != 0, d, dv, !out_f32, causal);
 }
 
 // Tile shapes per (element type, head dimension); shared by the host plan
@@ -130,6 +140,19 @@ template <typename T, int D> struct FwdShape;
 template <> struct FwdShape<__bf16, 64> {
   static constexpr int BQ = MEA_T64_FWD_BQ, QT = BQ == 512 ? 2 : BQ / 128, BK = 64, OCC = MEA_T64_FWD_OCC;
 };
+// 16-bit d = d_v = 64 causal forward with the two-group kernel for unmasked
+// problems: up to MEA_T64_FWD_CAUSAL_SMALL queries the 4-wave kernel with 128
+// queries per workgroup runs instead (returns 128), above it the two-group
+// kernel (512).  A 512-query workgroup of the two-group kernel spends 8 key
+// tiles on the diagonal, half of that work masked, and short sequences have
+// few tiles besides: measured on causal bf16 problems, n = 1024-8192 (16-256
+// heads) took 17-41 % less time with the 4-wave kernel, n = 16384 and 32768
+// 2-5 % more (256-query workgroups: -3 to +5 %).  Host plan and launch both
+// use this.
+#ifndef MEA_T64_FWD_CAUSAL_SMALL
+#define MEA_T64_FWD_CAUSAL_SMALL 8192
+#endif
+inline int fwd_causal64_bq(int64_t n_q) { return n_q <= MEA_T64_FWD_CAUSAL_SMALL ? 128 : 512; }
 // 16-bit d = 128: BQ = 256 selects the two-group kernel (8 waves of 32
 // queries); 128 the 4-wave kernel.  Problems with d_v != d always run the
 // 4-wave kernel with 128 queries per workgroup (kFwdBq4wave).

@@ -95,8 +95,8 @@ static void check_fwd_plan(int64_t B, int64_t H, int64_t nq, int64_t nk, int64_t
   }
 }
 
-static void check_bwd_carving(int64_t B, int64_t H, int64_t nq, int64_t d, int dtype, int out_f32) {
-  mea_problem p = prob(B, H, nq, 300, d, dtype, 0, 0, out_f32);
+static void check_bwd_carving(int64_t B, int64_t H, int64_t nq, int64_t d, int dtype, int out_f32, int causal = 0) {
+  mea_problem p = prob(B, H, nq, 300, d, dtype, causal, 0, out_f32);
   size_t need = 0;
   CHECK(mea_attention_bwd_workspace_size(&p, &need) == MEA_OK, "bwd ws size");
   CHECK(mea_attention_bwd(&p, P, P, P, P, nullptr, P, static_cast<float*>(P), P, P, P, WS, need, nullptr) == MEA_OK,
@@ -104,6 +104,10 @@ static void check_bwd_carving(int64_t B, int64_t H, int64_t nq, int64_t d, int d
   const mea::BwdParams& b = mea::g_last_bwd;
   const size_t rows = (size_t)(B * H) * (size_t)b.n_q_pad;
   CHECK(b.n_q_pad >= nq && b.n_q_pad % mea::kBwdRowPad == 0 && b.n_q_pad - nq < mea::kBwdRowPad, "row padding");
+  // The layout the host carved is the one the kernels of this problem read.
+  const bool rec = mea::bwd_two_group(dtype != MEA_F32, (int)d, (int)d, !out_f32, causal != 0);
+  CHECK((b.row_rec != nullptr) == rec && (b.s_init == nullptr) == rec && (b.dp_init == nullptr) == rec,
+        "per-row layout matches the kernels");
   if (b.row_rec) {
     CHECK(inside(b.row_rec, rows * 16, WS, need), "records inside the workspace");
   } else {
@@ -178,8 +182,10 @@ int main() {
   for (int64_t nq : {(int64_t)1, (int64_t)63, (int64_t)64, (int64_t)65, (int64_t)16384})
     for (int dt : {MEA_F32, MEA_BF16})
       for (int64_t d : {(int64_t)64, (int64_t)128}) {
-        check_bwd_carving(2, 3, nq, d, dt, 0);
-        if (dt != MEA_F32) check_bwd_carving(2, 3, nq, d, dt, 1);
+        for (int causal = 0; causal < 2; ++causal) {
+          check_bwd_carving(2, 3, nq, d, dt, 0, causal);
+          if (dt != MEA_F32) check_bwd_carving(2, 3, nq, d, dt, 1, causal);
+        }
       }
   if (failures == 0) printf("abi_check ok\n");
   return failures;
