@@ -184,7 +184,7 @@ size_t bwd_row_array_bytes(const mea_problem* p, size_t elem) {
 
 bool bwd_records(const mea_problem* p) {
   return mea::bwd_uses_row_records((int)p->dtype, (int)p->d, (int)dv_of(p), p->dtype != MEA_F32 && p->out_f32 != 0,
-                                   p->causal != 0);
+                                   p->causal != 0, p->n_q);
 }
 
 size_t bwd_workspace(const mea_problem* p) {

@@ -1832,32 +1832,45 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   void* args[] = {&p};
   const int64_t rows = (int64_t)p.bh * p.n_q_pad;
   constexpr int RPB = 256 / (DV * (int)sizeof(TO) / 16);
-  constexpr bool PP = bwd_two_group(sizeof(T) == 2, D, DV, __is_same(T, TO), CAUSAL);
+  // The two-group kernels exist for 16-bit d = d_v = 64 with dO in the input
+  // dtype; whether they run is the shared predicate's choice.
+  constexpr bool PP_CAN = bwd_two_group(sizeof(T) == 2, D, DV, __is_same(T, TO), false, 0);
+  const bool pp = PP_CAN && bwd_two_group(true, D, DV, true, CAUSAL, p.n_q);
   // The per-row values must be laid out as these kernels read them (records
   // or two arrays): a plan that disagrees is refused, not launched.
-  if (PP ? p.row_rec == nullptr : (p.s_init == nullptr || p.dp_init == nullptr)) return hipErrorInvalidValue;
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, PP>),
-                                 dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
+  if (pp ? p.row_rec == nullptr : (p.s_init == nullptr || p.dp_init == nullptr)) return hipErrorInvalidValue;
+  const void* pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, false>);
+  if constexpr (PP_CAN) {
+    if (pp) pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, true>);
+  }
+  hipError_t e = hipLaunchKernel(pre, dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
   if (e != hipSuccess) return e;
-  p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
-  p.n_qtiles = (int)((p.n_q + 128 * S::QT - 1) / (128 * S::QT));
   if (p.dk) {
-    if constexpr (PP) {
-      p.n_ktiles = (int)((p.n_k + kvpp::BKG - 1) / kvpp::BKG);
-      e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_pp_kernel<T, CAUSAL>),
-                          dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(kvpp::NW * 64), args, 0, stream);
-    } else {
+    bool launched = false;
+    if constexpr (PP_CAN) {
+      if (pp) {
+        p.n_ktiles = (int)((p.n_k + kvpp::BKG - 1) / kvpp::BKG);
+        e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_pp_kernel<T, CAUSAL>),
+                            dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(kvpp::NW * 64), args, 0, stream);
+        launched = true;
+      }
+    }
+    if (!launched) {
+      p.n_ktiles = (int)((p.n_k + Dk::BKG - 1) / Dk::BKG);
       e = hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dkdv_kernel<T, TO, D, DV, S::QS, S::KV_OCC, CAUSAL>),
                           dim3((unsigned)((int64_t)p.n_ktiles * p.bh)), dim3(256), args,
                           Dk::lds_bytes(S::KV_OCC, __is_same(T, TO)), stream);
     }
     if (e != hipSuccess || !p.dq) return e;
   }
-  if constexpr (PP) {
-    p.n_qtiles = (int)((p.n_q + qpp::BQG - 1) / qpp::BQG);
-    return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_pp_kernel<T, CAUSAL>),
-                           dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(qpp::NW * 64), args, 0, stream);
+  if constexpr (PP_CAN) {
+    if (pp) {
+      p.n_qtiles = (int)((p.n_q + qpp::BQG - 1) / qpp::BQG);
+      return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_pp_kernel<T, CAUSAL>),
+                             dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(qpp::NW * 64), args, 0, stream);
+    }
   }
+  p.n_qtiles = (int)((p.n_q + 128 * S::QT - 1) / (128 * S::QT));
   const int dq_lds = 2 * S::BK * (D + DV + 2 * 16 / (int)sizeof(T)) * (int)sizeof(T);
   return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, DV, S::QT, S::BK, S::Q_OCC, CAUSAL>),
                          dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(256), args, dq_lds, stream);

@@ -111,18 +111,20 @@ constexpr int kBwdRowPad = 64;
 // Whether the backward runs the two-group kernels, which take the per-row
 // values as 16-byte records; every other backward takes them as two float32
 // arrays.  The host's workspace layout and the kernels' choice both come from
-// this one predicate.  MEA_T64_BWD_CAUSAL_PP = 0 sends causal problems to
-// the 4-wave kernels instead (a build-time experiment).
-#ifndef MEA_T64_BWD_CAUSAL_PP
-#define MEA_T64_BWD_CAUSAL_PP 1
+// this one predicate.  Causal problems of up to MEA_T64_BWD_CAUSAL_SMALL
+// queries run the 4-wave kernels: measured on causal bf16 d = 64 problems,
+// n = 1024-4096 (128-256 heads) took 5-13 % less time with them, n = 8192
+// and 16384 6-7 % more.
+#ifndef MEA_T64_BWD_CAUSAL_SMALL
+#define MEA_T64_BWD_CAUSAL_SMALL 4096
 #endif
-constexpr bool bwd_two_group(bool is16, int d, int dv, bool same_out_dtype, bool causal) {
-  return is16 && d == 64 && dv == 64 && same_out_dtype && (!causal || MEA_T64_BWD_CAUSAL_PP);
+constexpr bool bwd_two_group(bool is16, int d, int dv, bool same_out_dtype, bool causal, int64_t n_q) {
+  return is16 && d == 64 && dv == 64 && same_out_dtype && !(causal && n_q <= MEA_T64_BWD_CAUSAL_SMALL);
 }
 // dtype: 0 float32, 1 fp16, 2 bf16; d and dv the head dimensions of q, k and
 // of v, o.
-inline bool bwd_uses_row_records(int dtype, int d, int dv, bool out_f32, bool causal) {
-  return bwd_two_group(dtype != 0, d, dv, !out_f32, causal);
+inline bool bwd_uses_row_records(int dtype, int d, int dv, bool out_f32, bool causal, int64_t n_q) {
+  return bwd_two_group(dtype != 0, d, dv, !out_f32, causal, n_q);
 }
 
 // Tile shapes per (element type, head dimension); shared by the host plan

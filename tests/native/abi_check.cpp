@@ -105,7 +105,7 @@ static void check_bwd_carving(int64_t B, int64_t H, int64_t nq, int64_t d, int d
   const size_t rows = (size_t)(B * H) * (size_t)b.n_q_pad;
   CHECK(b.n_q_pad >= nq && b.n_q_pad % mea::kBwdRowPad == 0 && b.n_q_pad - nq < mea::kBwdRowPad, "row padding");
   // The layout the host carved is the one the kernels of this problem read.
-  const bool rec = mea::bwd_two_group(dtype != MEA_F32, (int)d, (int)d, !out_f32, causal != 0);
+  const bool rec = mea::bwd_two_group(dtype != MEA_F32, (int)d, (int)d, !out_f32, causal != 0, nq);
   CHECK((b.row_rec != nullptr) == rec && (b.s_init == nullptr) == rec && (b.dp_init == nullptr) == rec,
         "per-row layout matches the kernels");
   if (b.row_rec) {
