@@ -89,6 +89,15 @@ def test_backward_without_residual_ordinary_inputs(d, causal):
     run_and_compare(2, 2, 300, 257, d, "bf16", causal, residual=False)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("nq", [4096, 4097])
+def test_backward_causal_d64_both_kernels(dtype, nq):
+    # Causal 16-bit d = 64 problems of up to 4096 queries run the 4-wave
+    # backward (per-row values as two arrays), longer ones the two-group
+    # kernels (records): both sides of the switch.
+    run_and_compare(1, 1, nq, nq, 64, dtype, True)
+
+
 def test_backward_fp32_self_attention_n256():
     w = WORKLOADS["selfattn_fp32_b1h1_n256_d64"]
     run_and_compare(w.batch, w.heads, w.n_q, w.n_k, w.d, w.dtype, w.causal)

@@ -47,6 +47,14 @@ def test_forward_small(dtype, d, causal, shape):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("nq", [8192, 8193])
+def test_forward_causal_d64_both_kernels(dtype, nq):
+    # Causal 16-bit d = 64 problems of up to 8192 queries run the 4-wave
+    # kernel, longer ones the two-group kernel: both sides of the switch.
+    run_and_compare(1, 1, nq, nq, 64, dtype, True)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("shape", [(1, 2, 7, 100), (2, 1, 300, 257), (1, 1, 64, 3000)],
