@@ -201,6 +201,9 @@ __device__ __forceinline__ Frag<T> lds_col_frag_swz128(const T* tile, int row0, 
   return __builtin_bit_cast(Frag<T>, r8);
 }
 
+#ifndef MEA_DKDV_ILV
+#define MEA_DKDV_ILV 1
+#endif
 template <typename T, typename TO, int D, int DV, int QS, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   using Cfg = DkdvTile<T, D, DV, QS>;
@@ -242,6 +245,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   constexpr int UQ = SWZ ? Cfg::SUQ : Cfg::UQ, UO = SWZ ? Cfg::SUO : Cfg::UO;  // 1 KiB copy units
   constexpr int TILEQ_L = ASYNC ? UQ * 1024 / Cfg::E : Cfg::TILEQ;  // dO tile offset (elements)
   constexpr int INIT_OFF = ASYNC ? (UQ + UO) * 1024 : Cfg::STAGE_ELEMS * Cfg::E;
+  constexpr bool ILV = MEA_DKDV_ILV && sizeof(T) == 2;
   T* const kslot = reinterpret_cast<T*>(smem_raw + 2 * STAGE_B) + 8 * tid;
   Frag<T> kf[K_LDS ? 1 : KC], vf[KCV];
 #pragma unroll
@@ -496,49 +500,92 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
             if (key_rel > 32 * qs + permuted_row(r, h)) s[qs][r] = -INFINITY;
         }
       }
+      auto col_o = [&](int qc, int dt) __attribute__((always_inline)) {
+        if constexpr (SWZ) return lds_col_frag_swz128<T>(dos_t, 16 * qc, 32 * dt, lane);
+        else if constexpr (sizeof(T) == 2) return lds_col_frag<T>(dos_t, RSO, 16 * qc, 32 * dt, lane);
+        else return lds_col_frag_f32(reinterpret_cast<const float*>(dos_t), RSO, 16 * qc, 32 * dt, lane);
+      };
+      auto col_q = [&](int qc, int dt) __attribute__((always_inline)) {
+        if constexpr (SWZ) return lds_col_frag_swz128<T>(qs_t, 16 * qc, 32 * dt, lane);
+        else if constexpr (sizeof(T) == 2) return lds_col_frag<T>(qs_t, RSQ, 16 * qc, 32 * dt, lane);
+        else return lds_col_frag_f32(reinterpret_cast<const float*>(qs_t), RSQ, 16 * qc, 32 * dt, lane);
+      };
+      constexpr int NDTM = NDT > NDTV ? NDT : NDTV;
+      if constexpr (ILV) {
+        // The weights of 16-query chunk qc + 1 (P = 2^(c S), dS = P (dP - D),
+        // rounded to fragments) are computed between the dV/dK MFMAs of chunk
+        // qc, a share per step, so this wave's VALU work overlaps its own
+        // MFMAs; each step's LDS operands are read one step ahead.
+        static_assert(8 % (2 * NDTM) == 0, "score pairs per step");
+        constexpr int PER = 8 / NDTM;
+        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+        u32x4v pw, dw;  // chunk qc + 1 as bf16 pairs
 #pragma unroll
-      for (int qs = 0; qs < QS; ++qs) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float pr = fast_exp2(s[qs][r] * cl2);
-          s[qs][r] = pr;                // P
-          dp[qs][r] = pr * dp[qs][r];   // dS = P (dP - D)
+        for (int e = 0; e < 8; e += 2) {
+          const float p0 = fast_exp2(s[0][e] * cl2), p1 = fast_exp2(s[0][e + 1] * cl2);
+          pw[e / 2] = pack2<T>(p0, p1);
+          dw[e / 2] = pack2<T>(p0 * dp[0][e], p1 * dp[0][e + 1]);
         }
-      }
-      // dV += P^T dO and dK += dS^T Q (A: lane = key row, k = queries).
+        Frag<T> pa = __builtin_bit_cast(Frag<T>, pw), da = __builtin_bit_cast(Frag<T>, dw);
+        Frag<T> bo = col_o(0, 0), bq = col_q(0, 0);
 #pragma unroll
-      for (int qc = 0; qc < NQC; ++qc) {
-        float tp[8], td[8];
+        for (int qc = 0; qc < NQC; ++qc) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          tp[e] = s[qc >> 1][8 * (qc & 1) + e];
-          td[e] = dp[qc >> 1][8 * (qc & 1) + e];
-        }
-        const Frag<T> pa = to_frag<T>(tp);
-        const Frag<T> da = to_frag<T>(td);
-#pragma unroll
-        for (int dt = 0; dt < (NDT > NDTV ? NDT : NDTV); ++dt) {
-          if (dt < NDTV) {
-            Frag<T> bo;
-            if constexpr (SWZ) {
-              bo = lds_col_frag_swz128<T>(dos_t, 16 * qc, 32 * dt, lane);
-            } else if constexpr (sizeof(T) == 2) {
-              bo = lds_col_frag<T>(dos_t, RSO, 16 * qc, 32 * dt, lane);
-            } else {
-              bo = lds_col_frag_f32(reinterpret_cast<const float*>(dos_t), RSO, 16 * qc, 32 * dt, lane);
+          for (int dt = 0; dt < NDTM; ++dt) {
+            const bool last = dt + 1 == NDTM;
+            const int nqc = last ? qc + 1 : qc, ndt = last ? 0 : dt + 1;
+            Frag<T> bo_n = bo, bq_n = bq;
+            if (nqc < NQC) {
+              if (ndt < NDTV) bo_n = col_o(nqc, ndt);
+              if (ndt < NDT) bq_n = col_q(nqc, ndt);
             }
-            dv[dt] = mma(pa, bo, dv[dt]);
+            if (dt < NDTV) dv[dt] = mma(pa, bo, dv[dt]);
+            if (dt < NDT) dk[dt] = mma(da, bq, dk[dt]);
+            if (qc + 1 < NQC) {
+              const f32x16& sn = s[(qc + 1) >> 1];
+              const f32x16& dn = dp[(qc + 1) >> 1];
+#pragma unroll
+              for (int e = PER * dt; e < PER * dt + PER; e += 2) {
+                const int r = 8 * ((qc + 1) & 1) + e;
+                const float p0 = fast_exp2(sn[r] * cl2), p1 = fast_exp2(sn[r + 1] * cl2);
+                pw[e / 2] = pack2<T>(p0, p1);
+                dw[e / 2] = pack2<T>(p0 * dn[r], p1 * dn[r + 1]);
+              }
+            }
+            bo = bo_n;
+            bq = bq_n;
+            __builtin_amdgcn_sched_barrier(0);
           }
-          if (dt < NDT) {
-            Frag<T> bq;
-            if constexpr (SWZ) {
-              bq = lds_col_frag_swz128<T>(qs_t, 16 * qc, 32 * dt, lane);
-            } else if constexpr (sizeof(T) == 2) {
-              bq = lds_col_frag<T>(qs_t, RSQ, 16 * qc, 32 * dt, lane);
-            } else {
-              bq = lds_col_frag_f32(reinterpret_cast<const float*>(qs_t), RSQ, 16 * qc, 32 * dt, lane);
-            }
-            dk[dt] = mma(da, bq, dk[dt]);
+          if (qc + 1 < NQC) {
+            pa = __builtin_bit_cast(Frag<T>, pw);
+            da = __builtin_bit_cast(Frag<T>, dw);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int qs = 0; qs < QS; ++qs) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float pr = fast_exp2(s[qs][r] * cl2);
+            s[qs][r] = pr;                // P
+            dp[qs][r] = pr * dp[qs][r];   // dS = P (dP - D)
+          }
+        }
+        // dV += P^T dO and dK += dS^T Q (A: lane = key row, k = queries).
+#pragma unroll
+        for (int qc = 0; qc < NQC; ++qc) {
+          float tp[8], td[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            tp[e] = s[qc >> 1][8 * (qc & 1) + e];
+            td[e] = dp[qc >> 1][8 * (qc & 1) + e];
+          }
+          const Frag<T> pa = to_frag<T>(tp);
+          const Frag<T> da = to_frag<T>(td);
+#pragma unroll
+          for (int dt = 0; dt < NDTM; ++dt) {
+            if (dt < NDTV) dv[dt] = mma(pa, col_o(qc, dt), dv[dt]);
+            if (dt < NDT) dk[dt] = mma(da, col_q(qc, dt), dk[dt]);
           }
         }
       }

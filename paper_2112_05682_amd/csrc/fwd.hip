@@ -63,6 +63,9 @@ struct FwdTile {
   static_assert(BK % 32 == 0 && D % 32 == 0 && DV % 32 == 0, "tile shapes are multiples of 32");
 };
 
+#ifndef MEA_FWD_ILV
+#define MEA_FWD_ILV 1
+#endif
 template <typename T, typename TO, int D, int DV, int QT, int BK, int OCC, bool CAUSAL>
 __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   using Cfg = FwdTile<T, D, DV, QT, BK>;
@@ -71,6 +74,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
   constexpr int NKT = BK / 32;  // 32-key sub-tiles per tile
   constexpr int NPC = BK / 16;  // 16-key chunks of the PV contraction
   constexpr int NDT = DV / 32;  // 32-row tiles of O^T
+  constexpr bool ILV = MEA_FWD_ILV && sizeof(T) == 2 && NDT == 2;
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* smem = reinterpret_cast<T*>(smem_raw);
@@ -230,6 +234,7 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
     // numerator and denominator share the reference, so the result is the same
     // and the accumulator rescale is skipped on most tiles.
     Frag<T> pf[QT][NPC];
+    float neg[QT];
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       float mx = -INFINITY;
@@ -251,27 +256,64 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
       }
       // A row with no visible key so far keeps m_ref = -inf; offset 0 keeps
       // its (all -inf) exponents at weight 0 instead of NaN.
-      const float neg = (MASK && m_ref[t] == -INFINITY) ? 0.0f : -m_ref[t];
+      neg[t] = (MASK && m_ref[t] == -INFINITY) ? 0.0f : -m_ref[t];
 #pragma unroll
-      for (int pc = 0; pc < NPC; ++pc) {
+      for (int pc = 0; pc < (ILV ? 1 : NPC); ++pc) {
         float e8[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg));
+        for (int e = 0; e < 8; ++e) e8[e] = fast_exp2(fmaf(s[pc >> 1][t][8 * (pc & 1) + e], cl2, neg[t]));
         pf[t][pc] = to_frag<T>(e8);
         l_run[t] = tree_sum<8>(e8, l_run[t]);
       }
+    }
+    auto col_v = [&](int pc, int dt) __attribute__((always_inline)) {
+      if constexpr (sizeof(T) == 2) return lds_col_frag<T>(vs, RSV, 16 * pc, 32 * dt, lane);
+      else return lds_col_frag_f32(reinterpret_cast<const float*>(vs), RSV, 16 * pc, 32 * dt, lane);
+    };
+    if constexpr (ILV) {
+      // O^T += V^T P^T chunk by chunk; the weights of 16-key chunk pc + 1 are
+      // computed between the MFMAs of chunk pc (half a chunk per step) so this
+      // wave's VALU work overlaps its own MFMAs; each step's V^T fragment is
+      // read one step ahead.  Same operations and order per value as below.
+      static_assert(NDT == 2, "two O^T tiles per chunk");
+      float e8[QT][8];
+      Frag<T> a = col_v(0, 0);
+#pragma unroll
+      for (int pc = 0; pc < NPC; ++pc) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const bool last = dt + 1 == NDT;
+          Frag<T> a_n = a;
+          if (!last || pc + 1 < NPC) a_n = col_v(last ? pc + 1 : pc, last ? 0 : dt + 1);
+#pragma unroll
+          for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, pf[t][pc], acc[t][dt]);
+          if (pc + 1 < NPC) {
+            const int nc = pc + 1;
+#pragma unroll
+            for (int t = 0; t < QT; ++t)
+#pragma unroll
+              for (int e = 4 * dt; e < 4 * dt + 4; ++e)
+                e8[t][e] = fast_exp2(fmaf(s[nc >> 1][t][8 * (nc & 1) + e], cl2, neg[t]));
+          }
+          a = a_n;
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if (pc + 1 < NPC) {
+#pragma unroll
+          for (int t = 0; t < QT; ++t) {
+            pf[t][pc + 1] = to_frag<T>(e8[t]);
+            l_run[t] = tree_sum<8>(e8[t], l_run[t]);
+          }
+        }
+      }
+      return;
     }
     // O^T += V^T P^T; each V^T fragment feeds every query sub-tile.
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
 #pragma unroll
       for (int pc = 0; pc < NPC; ++pc) {
-        Frag<T> a;
-        if constexpr (sizeof(T) == 2) {
-          a = lds_col_frag<T>(vs, RSV, 16 * pc, 32 * dt, lane);
-        } else {
-          a = lds_col_frag_f32(reinterpret_cast<const float*>(vs), RSV, 16 * pc, 32 * dt, lane);
-        }
+        const Frag<T> a = col_v(pc, dt);
 #pragma unroll
         for (int t = 0; t < QT; ++t) acc[t][dt] = mma(a, pf[t][pc], acc[t][dt]);
       }

@@ -147,12 +147,12 @@ template <> struct FwdShape<__bf16, 64> {
 // queries per workgroup runs instead (returns 128), above it the two-group
 // kernel (512).  A 512-query workgroup of the two-group kernel spends 8 key
 // tiles on the diagonal, half of that work masked, and short sequences have
-// few tiles besides: measured on causal bf16 problems, n = 1024-8192 (16-256
-// heads) took 17-41 % less time with the 4-wave kernel, n = 16384 and 32768
+// few tiles besides: measured on causal bf16 problems, n = 1024-12288 (16-256
+// heads) took 9-41 % less time with the 4-wave kernel, n = 16384 and 32768
 // 2-5 % more (256-query workgroups: -3 to +5 %).  Host plan and launch both
 // use this.
 #ifndef MEA_T64_FWD_CAUSAL_SMALL
-#define MEA_T64_FWD_CAUSAL_SMALL 8192
+#define MEA_T64_FWD_CAUSAL_SMALL 12288
 #endif
 inline int fwd_causal64_bq(int64_t n_q) { return n_q <= MEA_T64_FWD_CAUSAL_SMALL ? 128 : 512; }
 // 16-bit d = 128: BQ = 256 selects the two-group kernel (8 waves of 32

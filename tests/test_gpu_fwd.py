@@ -47,9 +47,9 @@ def test_forward_small(dtype, d, causal, shape):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
-@pytest.mark.parametrize("nq", [8192, 8193])
+@pytest.mark.parametrize("nq", [12288, 12289])
 def test_forward_causal_d64_both_kernels(dtype, nq):
-    # Causal 16-bit d = 64 problems of up to 8192 queries run the 4-wave
+    # Causal 16-bit d = 64 problems of up to 12288 queries run the 4-wave
     # kernel, longer ones the two-group kernel: both sides of the switch.
     run_and_compare(1, 1, nq, nq, 64, dtype, True)
 
