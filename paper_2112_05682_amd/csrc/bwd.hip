@@ -201,6 +201,9 @@ __device__ __forceinline__ Frag<T> lds_col_frag_swz128(const T* tile, int row0, 
   return __builtin_bit_cast(Frag<T>, r8);
 }
 
+#ifndef MEA_T128_DKDV_AHEAD
+#define MEA_T128_DKDV_AHEAD 1
+#endif
 #ifndef MEA_DKDV_ILV
 #define MEA_DKDV_ILV 1
 #endif
@@ -246,6 +249,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
   constexpr int TILEQ_L = ASYNC ? UQ * 1024 / Cfg::E : Cfg::TILEQ;  // dO tile offset (elements)
   constexpr int INIT_OFF = ASYNC ? (UQ + UO) * 1024 : Cfg::STAGE_ELEMS * Cfg::E;
   constexpr bool ILV = MEA_DKDV_ILV && sizeof(T) == 2;
+  constexpr int KV_AHEAD = MEA_T128_DKDV_AHEAD;
   T* const kslot = reinterpret_cast<T*>(smem_raw + 2 * STAGE_B) + 8 * tid;
   Frag<T> kf[K_LDS ? 1 : KC], vf[KCV];
 #pragma unroll
@@ -469,6 +473,25 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dkdv_kernel(BwdParams p) {
       }
       // S = Q K^T - lse/scale and dP = dO V^T - D (rows: queries in perm32
       // order; lane: key).
+      if constexpr (SWZ && QS == 1 && KV_AHEAD > 0) {
+        // The Q and dO row fragments of k chunk kc are read KV_AHEAD chunks
+        // before their MFMAs (a ring of registers).
+        constexpr int RA = KV_AHEAD + 1;
+        Frag<T> fa[RA], fg[RA];
+        auto fetch = [&](int kc) __attribute__((always_inline)) {
+          fa[kc % RA] = lds_frag_swz128<T>(qs_t, qrow, 2 * kc + h);
+          fg[kc % RA] = lds_frag_swz128<T>(dos_t, qrow, 2 * kc + h);
+        };
+#pragma unroll
+        for (int kc = 0; kc < KV_AHEAD; ++kc) fetch(kc);
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) {
+          if (kc + KV_AHEAD < KC) fetch(kc + KV_AHEAD);
+          s[0] = mma(fa[kc % RA], kfrag(kc), s[0]);
+          dp[0] = mma(fg[kc % RA], vf[kc], dp[0]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else
 #pragma unroll
       for (int kc = 0; kc < (KC > KCV ? KC : KCV); ++kc) {
 #pragma unroll
@@ -1092,6 +1115,9 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
 
 // ------------------------------------------------------------------- dQ
 // D: head dimension of q and k; DV: of v and dO.
+#ifndef MEA_T128_DQ_AHEAD
+#define MEA_T128_DQ_AHEAD 1
+#endif
 #ifndef MEA_T128_DQ_SWZ
 #define MEA_T128_DQ_SWZ 1
 #endif
@@ -1116,6 +1142,7 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
   // transposing reads free of bank conflicts and frees the staging registers.
   constexpr bool SWZ = MEA_T128_DQ_SWZ && sizeof(T) == 2 && D == 128 && DV == 128 && BK == 32;
   constexpr int TK = SWZ ? BK * D : TILEK, TV = SWZ ? BK * DV : TILEV;  // tile sizes (elements)
+  constexpr int DQ_AHEAD = MEA_T128_DQ_AHEAD;
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   T* smem = reinterpret_cast<T*>(smem_raw);
@@ -1292,6 +1319,26 @@ __global__ __launch_bounds__(256, OCC) void attn_bwd_dq_kernel(BwdParams p) {
         }
     // S^T = K Q^T - lse/scale and dP^T = V dO^T - D (rows: keys in perm32
     // order; lane: query).
+    if constexpr (SWZ && QT == 1 && NKT == 1 && DQ_AHEAD > 0) {
+      // The K and V row fragments of k chunk kc are read DQ_AHEAD chunks
+      // before their MFMAs (a ring of registers), so the MFMAs do not wait on
+      // reads issued just before them.
+      constexpr int RA = DQ_AHEAD + 1;
+      Frag<T> fa[RA], fb[RA];
+      auto fetch = [&](int kc) __attribute__((always_inline)) {
+        fa[kc % RA] = lds_frag_swz128<T>(ks, krow, 2 * kc + h);
+        fb[kc % RA] = lds_frag_swz128<T>(vs, krow, 2 * kc + h);
+      };
+#pragma unroll
+      for (int kc = 0; kc < DQ_AHEAD; ++kc) fetch(kc);
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        if (kc + DQ_AHEAD < KC) fetch(kc + DQ_AHEAD);
+        s[0][0] = mma(fa[kc % RA], qf[0][kc], s[0][0]);
+        dp[0][0] = mma(fb[kc % RA], gf[0][kc], dp[0][0]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else
 #pragma unroll
     for (int kc = 0; kc < (KC > KCV ? KC : KCV); ++kc)
 #pragma unroll
