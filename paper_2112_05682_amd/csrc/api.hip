@@ -94,12 +94,12 @@ struct FwdPlan {
   size_t workspace;
 };
 
-void fwd_tiles(int dtype, int64_t d, int64_t dv, bool causal, int64_t n_q, int* bq, int* bk) {
+void fwd_tiles(int dtype, int64_t d, int64_t dv, bool causal, int64_t n_q, int64_t bh, int* bq, int* bk) {
   if (dtype == MEA_F32) {
     *bq = mea::FwdShape<float, 64>::BQ;
     *bk = mea::FwdShape<float, 64>::BK;
   } else if (d == 64 && dv == 64) {
-    *bq = causal && mea::FwdShape<__bf16, 64>::BQ == 512 ? mea::fwd_causal64_bq(n_q) : mea::FwdShape<__bf16, 64>::BQ;
+    *bq = causal && mea::FwdShape<__bf16, 64>::BQ == 512 ? mea::fwd_causal64_bq(n_q, bh) : mea::FwdShape<__bf16, 64>::BQ;
     *bk = mea::FwdShape<__bf16, 64>::BK;
   } else if (d == 128 && dv == 128) {
     *bq = mea::FwdShape<__bf16, 128>::BQ;
@@ -147,8 +147,8 @@ FwdPlan plan_decode(const mea_problem* p) {
 FwdPlan plan_fwd(const mea_problem* p) {
   if (mea::fwd_uses_decode((int)p->dtype, (int)p->d, (int)dv_of(p), p->n_q)) return plan_decode(p);
   FwdPlan pl;
-  fwd_tiles(p->dtype, p->d, dv_of(p), p->causal != 0, p->n_q, &pl.bq, &pl.bk);
   const int64_t bh = p->batch * p->heads;
+  fwd_tiles(p->dtype, p->d, dv_of(p), p->causal != 0, p->n_q, bh, &pl.bq, &pl.bk);
   pl.n_qtiles = (p->n_q + pl.bq - 1) / pl.bq;
   const int64_t k_tiles = (p->n_k + pl.bk - 1) / pl.bk;
   const int64_t base = bh * pl.n_qtiles;

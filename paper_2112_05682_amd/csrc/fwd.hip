@@ -400,6 +400,9 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
 // row-fragment reads of K and the transposing reads of V free of bank
 // conflicts.
 // ---------------------------------------------------------------------------
+#ifndef MEA_FWD_PP_LEAN_COPY
+#define MEA_FWD_PP_LEAN_COPY 1
+#endif
 #ifndef MEA_FWD_PP_W0
 #define MEA_FWD_PP_W0 3
 #endif
@@ -799,9 +802,41 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
       load_tile(g, k0, stage, is_v, wave - 4, 4);
     }
   };
+  // LEAN (causal, d = 64): the register allocator spilled the offsets above
+  // and reloaded them before each tile's copies, and the reload's wait
+  // (vmcnt 0) also waited for the copies still in flight.  Instead the lane
+  // offset is recomputed at each issue from an opaque copy of the lane index
+  // (a few VALU instructions), one per tensor: the wave's units are 4 RPU
+  // rows apart and both swizzles repeat every 16 rows, so the row shift goes
+  // into the scalar base.
+  constexpr bool LEAN = MEA_FWD_PP_LEAN_COPY && CAUSAL && D == 64;
+  static_assert(!LEAN || (4 * RPU) % 16 == 0, "swizzle period");
+  auto copy_tile_lean = [&](bool is_v, int j, unsigned char* stage) __attribute__((always_inline)) {
+    const int64_t k0 = kb + (int64_t)j * BK;
+    const unsigned base = __builtin_amdgcn_readfirstlane(lds_addr(stage) + (wave - 4) * 1024);
+    const T* g = is_v ? vg : kg;
+    if (k0 + BK <= p.n_k) {
+      int l = lane;
+      asm volatile("" : "+v"(l));
+      const int row = RPU * (wave - 4) + (l >> LCPR);
+      const int x = (l & (CPR - 1)) ^ (is_v ? swz_v(row) : swz_k(row));
+      const int64_t rs = is_v ? p.sv.r : p.sk.r;
+      const unsigned off = E * ((unsigned)row * (unsigned)rs + 8u * (unsigned)x);
+      const T* tile = g + k0 * rs;
+#pragma unroll
+      for (int i = 0; i < UPW; ++i) copy_to_lds16_sb(tile + 4 * RPU * i * rs, off, base + 4096 * i);
+    } else {
+      load_tile(g, k0, stage, is_v, wave - 4, 4);
+    }
+  };
   auto issue = [&](int j) __attribute__((always_inline)) {
-    if (j + 3 < n_tiles) copy_tile(false, j + 3, kstage(j + 3), uk0, uk1, uk2, uk3);
-    if (j + 2 < n_tiles) copy_tile(true, j + 2, vstage(j + 2), uv0, uv1, uv2, uv3);
+    if constexpr (LEAN) {
+      if (j + 3 < n_tiles) copy_tile_lean(false, j + 3, kstage(j + 3));
+      if (j + 2 < n_tiles) copy_tile_lean(true, j + 2, vstage(j + 2));
+    } else {
+      if (j + 3 < n_tiles) copy_tile(false, j + 3, kstage(j + 3), uk0, uk1, uk2, uk3);
+      if (j + 2 < n_tiles) copy_tile(true, j + 2, vstage(j + 2), uv0, uv1, uv2, uv3);
+    }
   };
   if (grp == 1) {
     issue(-2);
@@ -1116,8 +1151,9 @@ static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t str
   if constexpr (sizeof(T) == 2 && FwdShape<T, D>::BQ == pp::BQ<D>) {
     if (!causal) return launch_fwd_pp<T, TO, D, false>(p, stream);
     if constexpr (D == 64) {
-      // Short causal problems: the 4-wave kernel with 128-query workgroups.
-      if (fwd_causal64_bq(p.n_q) == 128)
+      // Short or small causal problems: the 4-wave kernel with 128-query
+      // workgroups.
+      if (fwd_causal64_bq(p.n_q, p.bh) == 128)
         return launch_fwd_impl<T, TO, 64, 64, 1, FwdShape<T, 64>::BK, MEA_T64_FWD_OCC, true>(p, stream);
     }
     return launch_fwd_pp<T, TO, D, true>(p, stream);

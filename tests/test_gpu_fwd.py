@@ -47,11 +47,27 @@ def test_forward_small(dtype, d, causal, shape):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
-@pytest.mark.parametrize("nq", [12288, 12289])
-def test_forward_causal_d64_both_kernels(dtype, nq):
-    # Causal 16-bit d = 64 problems of up to 12288 queries run the 4-wave
-    # kernel, longer ones the two-group kernel: both sides of the switch.
-    run_and_compare(1, 1, nq, nq, 64, dtype, True)
+@pytest.mark.parametrize("shape", [(1, 16, 12288), (1, 16, 12800), (4, 64, 4096), (4, 64, 4097)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_forward_causal_d64_both_kernels(dtype, shape):
+    # Causal 16-bit d = 64 problems run the two-group kernel when they have
+    # more than 4096 queries and at least 2.5e9 query-key pairs (batch x heads
+    # x n^2), else the 4-wave kernel: both sides of both bounds (12288 / 12800
+    # queries at 16 heads: 2.42e9 / 2.62e9 pairs; 4096 / 4097 queries at 256
+    # heads), sampled rows of a few slices against the oracle.
+    B, H, n = shape
+    print("causal d64 switch case", shape, dtype, flush=True)
+    x = attention_inputs(B, H, n, n, 64, dtype, with_grad=False)
+    g = to_gpu(x)
+    o, lse = attention_fwd(g["q"], g["k"], g["v"], causal=True)
+    torch.cuda.synchronize()
+    o_c, l_c = o.cpu(), lse.cpu()
+    for b, h in sorted({(0, 0), (B - 1, H - 1), (B // 2, H // 3)}):
+        rows = sampled_rows(n, 48, 7 + b * 5 + h)
+        ro, rl = oracle.fwd_rows(f64(x["q"][b, h]), f64(x["k"][b, h]), f64(x["v"][b, h]), rows,
+                                 scale=0.125, causal=True)
+        check("O", f64(o_c[b, h, rows]), ro, TOL[dtype])
+        check_lse(f64(l_c[b, h, rows]), rl)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
