@@ -1019,10 +1019,12 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
   // dV/dK of the previous tile and S/dP of this one.  A tile active for a wave
   // stays active for its later tiles (the queries only grow), so the modes
   // come in this order and each loop below runs one of them.
-  auto iteration = [&](auto mode_tag, int i) __attribute__((always_inline)) {
+  auto iteration = [&](auto mode_tag, auto mask_tag, int i) __attribute__((always_inline)) {
     constexpr int MODE = decltype(mode_tag)::value;
     const int64_t q0 = q_begin + (int64_t)i * BQ;
-    const bool need_mask = CAUSAL && q0 < kw + 31;
+    // MASK: the tile may hold queries before some of the wave's keys; the
+    // tiles after those are compiled without the compare and select per score.
+    const bool need_mask = decltype(mask_tag)::value && q0 < kw + 31;
     const int key_rel = (int)(key - q0);  // key minus the tile's first query
     // ---- MFMA phase (S and dP are free: the last softmax phase converted them)
     mfma_phase_priority();
@@ -1089,10 +1091,19 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dkdv_pp_kernel(BwdParams p) {
     i_first = t > 0 ? (int)((t + BQ - 1) / BQ) : 0;
     if (i_first > n_iters) i_first = n_iters;
   }
+  // Tiles from i_plain on start at or after query kw + 31: no query of theirs
+  // precedes a key of the wave, so they need no mask.
+  int i_plain = 0;
+  if (CAUSAL) {
+    const int64_t t = kw + 31 - q_begin;
+    i_plain = t > 0 ? (int)((t + BQ - 1) / BQ) : 0;
+    if (i_plain > n_iters) i_plain = n_iters;
+  }
   int i = 0;
-  for (; i < i_first; ++i) iteration(IntC<0>{}, i);
-  if (i < n_iters) iteration(IntC<1>{}, i++);
-  for (; i < n_iters; ++i) iteration(IntC<2>{}, i);
+  for (; i < i_first; ++i) iteration(IntC<0>{}, BoolC<false>{}, i);
+  if (i < n_iters) iteration(IntC<1>{}, BoolC<CAUSAL>{}, i++);
+  for (; i < i_plain; ++i) iteration(IntC<2>{}, BoolC<CAUSAL>{}, i);
+  for (; i < n_iters; ++i) iteration(IntC<2>{}, BoolC<false>{}, i);
   // dV/dK of the last tile.
   if (i_first < n_iters) dvdk(n_iters - 1);
   // Group 0 issued one barrier fewer (group 1's start delay): balance it so
