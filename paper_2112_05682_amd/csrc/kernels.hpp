@@ -113,10 +113,11 @@ constexpr int kBwdRowPad = 64;
 // arrays.  The host's workspace layout and the kernels' choice both come from
 // this one predicate.  Causal problems of up to MEA_T64_BWD_CAUSAL_SMALL
 // queries run the 4-wave kernels: measured on causal bf16 d = 64 problems,
-// n = 1024-4096 (128-256 heads) took 5-13 % less time with them, n = 8192
-// and 16384 6-7 % more.
+// n = 1024-2048 (128-256 heads) took 5-13 % less time with them; at 3072 the
+// two kinds tie, and from 4096 queries on the two-group kernels take 3-12 %
+// less (6-7 % more before their plain tiles dropped the mask).
 #ifndef MEA_T64_BWD_CAUSAL_SMALL
-#define MEA_T64_BWD_CAUSAL_SMALL 4096
+#define MEA_T64_BWD_CAUSAL_SMALL 2048
 #endif
 constexpr bool bwd_two_group(bool is16, int d, int dv, bool same_out_dtype, bool causal, int64_t n_q) {
   return is16 && d == 64 && dv == 64 && same_out_dtype && !(causal && n_q <= MEA_T64_BWD_CAUSAL_SMALL);

@@ -179,7 +179,7 @@ int main() {
       for (int causal : {0, 1})
         for (int64_t nq : {(int64_t)1, (int64_t)100, (int64_t)300, (int64_t)4096}) check_fwd_plan(1, 1, nq, nk, 64, dt, causal);
   check_fwd_plan(2, 3, 256, 1 << 20, 128, MEA_F16, 0);
-  for (int64_t nq : {(int64_t)1, (int64_t)63, (int64_t)64, (int64_t)65, (int64_t)16384})
+  for (int64_t nq : {(int64_t)1, (int64_t)63, (int64_t)64, (int64_t)65, (int64_t)2048, (int64_t)2049, (int64_t)16384})
     for (int dt : {MEA_F32, MEA_BF16})
       for (int64_t d : {(int64_t)64, (int64_t)128}) {
         for (int causal = 0; causal < 2; ++causal) {

@@ -90,9 +90,9 @@ def test_backward_without_residual_ordinary_inputs(d, causal):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
-@pytest.mark.parametrize("nq", [4096, 4097])
+@pytest.mark.parametrize("nq", [2048, 2049])
 def test_backward_causal_d64_both_kernels(dtype, nq):
-    # Causal 16-bit d = 64 problems of up to 4096 queries run the 4-wave
+    # Causal 16-bit d = 64 problems of up to 2048 queries run the 4-wave
     # backward (per-row values as two arrays), longer ones the two-group
     # kernels (records): both sides of the switch.
     run_and_compare(1, 1, nq, nq, 64, dtype, True)
