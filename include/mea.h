@@ -122,7 +122,12 @@ mea_status mea_attention_fwd_workspace_size(const mea_problem* p, size_t* bytes)
  * (B*H*ceil(n_q/64)*64 rows) the values -lse/scale and -D_i with
  * D_i = sum_t dO_it O_it (Section 5.2's recompute needs only these and the
  * inputs), O(n) like the lse: 16 bytes per row for 16-bit inputs and outputs
- * at d = 64 (each value as three bf16 parts), else two float32 values. */
+ * at d = 64 (each value as three bf16 parts), else two float32 values.  For
+ * 16-bit inputs with float32 o and dO (out_f32) it also holds dO rounded to
+ * the input dtype (B*H*n_q*d_v 16-bit values, O(n d) like dO itself), so that
+ * the kernels of 16-bit outputs run; the rounding is the one those problems'
+ * kernels would otherwise apply while staging dO, so the results are the
+ * same, and the per-row values then take the 16-bit-output layout. */
 mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes);
 
 /* Forward (Sections 2-4): o = softmax(scale * q k^T) v, computed tile by
@@ -172,9 +177,11 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
 
 /* mea_attention_bwd without the workspace arguments, for callers that cannot
  * allocate device memory: code being captured into a HIP graph, tight
- * serving loops, harnesses that forbid allocation.  The per-row workspace
- * (mea_attention_bwd_workspace_size bytes) lives in a file-scope device
- * array of MEA_NOALLOC_SCRATCH_BYTES per GPU instead; the call itself
+ * serving loops, harnesses that forbid allocation.  The per-row values (the
+ * workspace of mea_attention_bwd without its 16-bit copy of a float32 dO:
+ * those problems run the kernels that round dO while staging it) live in a
+ * file-scope device array of MEA_NOALLOC_SCRATCH_BYTES per GPU instead; the
+ * call itself
  * allocates nothing (no hipMalloc, no library allocation).  Problems whose
  * workspace exceeds that size return MEA_ERR_SCRATCH before anything is
  * enqueued: B * H * ceil(n_q / 64) * 64 padded query rows must not exceed
@@ -187,7 +194,7 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
  * part it reads before reading it (nothing needs to start at zero): calls
  * that overlap on one GPU (different streams, or threads) race and must be
  * serialised by the caller.  Results are identical to mea_attention_bwd's
- * (same kernels). */
+ * (the same arithmetic in the same order). */
 mea_status mea_attention_bwd_noalloc(const mea_problem* p, const void* q, const void* k,
                                      const void* v, const void* o, const void* o_lo,
                                      const void* d_o, const float* lse, void* dq, void* dk,

@@ -182,15 +182,29 @@ size_t bwd_row_array_bytes(const mea_problem* p, size_t elem) {
   return (b + 255) / 256 * 256;
 }
 
-bool bwd_records(const mea_problem* p) {
-  return mea::bwd_uses_row_records((int)p->dtype, (int)p->d, (int)dv_of(p), p->dtype != MEA_F32 && p->out_f32 != 0,
-                                   p->causal != 0, p->n_q);
+// Whether the backward keeps a 16-bit copy of a float32 dO (16-bit inputs,
+// float32 outputs) so that the kernels of 16-bit outputs run: `allow` is false
+// for the allocation-free entry point, whose scratch holds the per-row values
+// only (those problems then run the kernels that convert dO while staging it;
+// the results are the same).
+bool bwd_do16(const mea_problem* p, bool allow) { return allow && p->dtype != MEA_F32 && p->out_f32 != 0; }
+
+bool bwd_records(const mea_problem* p, bool allow_do16) {
+  const bool f32_do = p->dtype != MEA_F32 && p->out_f32 != 0 && !bwd_do16(p, allow_do16);
+  return mea::bwd_uses_row_records((int)p->dtype, (int)p->d, (int)dv_of(p), f32_do, p->causal != 0, p->n_q);
 }
 
-size_t bwd_workspace(const mea_problem* p) {
+size_t bwd_do16_bytes(const mea_problem* p) {
+  const size_t b = (size_t)p->batch * (size_t)p->heads * (size_t)p->n_q * (size_t)dv_of(p) * 2;
+  return (b + 255) / 256 * 256;
+}
+
+size_t bwd_workspace(const mea_problem* p, bool allow_do16) {
   // One 16-byte record per padded row (two-group kernels), or s_init and
-  // dp_init as [B*H, n_q_pad] float32 arrays; 256-byte aligned.
-  return (bwd_records(p) ? bwd_row_array_bytes(p, 16) : 2 * bwd_row_array_bytes(p, 4)) + 256;
+  // dp_init as [B*H, n_q_pad] float32 arrays; then the 16-bit dO copy, if
+  // any; 256-byte aligned.
+  const size_t rows = bwd_records(p, allow_do16) ? bwd_row_array_bytes(p, 16) : 2 * bwd_row_array_bytes(p, 4);
+  return rows + (bwd_do16(p, allow_do16) ? bwd_do16_bytes(p) : 0) + 256;
 }
 
 float* align256(void* base, size_t off) {
@@ -244,7 +258,7 @@ mea_status check_bwd_pointers(const mea_problem* p, const void* q, const void* k
 
 mea_status bwd_launch(const mea_problem* p, const void* q, const void* k, const void* v, const void* o,
                       const void* o_lo, const void* d_o, const float* lse, void* dq, void* dk, void* dv,
-                      void* workspace, hipStream_t stream);
+                      void* workspace, bool allow_do16, hipStream_t stream);
 
 }  // namespace
 
@@ -278,7 +292,7 @@ mea_status mea_attention_bwd_workspace_size(const mea_problem* p, size_t* bytes)
   const mea_status st = check_problem(p);
   if (st != MEA_OK) return st;
   if (!bytes) return MEA_ERR_INVALID_ARG;
-  *bytes = bwd_workspace(p);
+  *bytes = bwd_workspace(p, true);
   return MEA_OK;
 }
 
@@ -351,9 +365,9 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
   if (st != MEA_OK) return st;
   st = check_bwd_pointers(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv);
   if (st != MEA_OK) return st;
-  const size_t need = bwd_workspace(p);
+  const size_t need = bwd_workspace(p, true);
   if (!workspace || workspace_bytes < need) return MEA_ERR_WORKSPACE;
-  return bwd_launch(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, workspace, stream);
+  return bwd_launch(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, workspace, true, stream);
 }
 
 mea_status mea_attention_bwd_noalloc(const mea_problem* p, const void* q, const void* k, const void* v,
@@ -363,11 +377,11 @@ mea_status mea_attention_bwd_noalloc(const mea_problem* p, const void* q, const 
   if (st != MEA_OK) return st;
   st = check_bwd_pointers(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv);
   if (st != MEA_OK) return st;
-  if (bwd_workspace(p) > MEA_NOALLOC_SCRATCH_BYTES) return MEA_ERR_SCRATCH;
+  if (bwd_workspace(p, false) > MEA_NOALLOC_SCRATCH_BYTES) return MEA_ERR_SCRATCH;
   void* ws = nullptr;
   st = scratch_of_device(stream, &ws);
   if (st != MEA_OK) return st;
-  return bwd_launch(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, ws, stream);
+  return bwd_launch(p, q, k, v, o, o_lo, d_o, lse, dq, dk, dv, ws, false, stream);
 }
 
 }  // extern "C"
@@ -375,10 +389,10 @@ mea_status mea_attention_bwd_noalloc(const mea_problem* p, const void* q, const 
 namespace {
 
 // The backward after validation: kernel arguments, stride checks, launches.
-// `workspace` holds at least bwd_workspace(p) bytes.
+// `workspace` holds at least bwd_workspace(p, allow_do16) bytes.
 mea_status bwd_launch(const mea_problem* p, const void* q, const void* k, const void* v, const void* o,
                       const void* o_lo, const void* d_o, const float* lse, void* dq, void* dk, void* dv,
-                      void* workspace, hipStream_t stream) {
+                      void* workspace, bool allow_do16, hipStream_t stream) {
   BwdParams bp = {};
   bp.q = q;
   bp.k = k;
@@ -391,12 +405,15 @@ mea_status bwd_launch(const mea_problem* p, const void* q, const void* k, const 
   bp.dk = dk;
   bp.dv = dv;
   bp.n_q_pad = bwd_row_pad(p->n_q);
-  if (bwd_records(p)) {
+  const bool rec = bwd_records(p, allow_do16);
+  if (rec) {
     bp.row_rec = reinterpret_cast<uint4*>(align256(workspace, 0));
   } else {
     bp.s_init = align256(workspace, 0);
     bp.dp_init = bp.s_init + bwd_row_array_bytes(p, 4) / 4;
   }
+  if (bwd_do16(p, allow_do16))
+    bp.do16 = align256(workspace, rec ? bwd_row_array_bytes(p, 16) : 2 * bwd_row_array_bytes(p, 4));
   bp.kv_len = p->kv_len;
   bp.n_q = p->n_q;
   bp.n_k = p->n_k;

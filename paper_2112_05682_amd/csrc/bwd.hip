@@ -64,8 +64,10 @@ __device__ __forceinline__ void split3_bf16(float x, __bf16& hi, __bf16& mid, __
 
 // D_i = dO_i . O_i and the accumulator initial values of every (padded) row,
 // as records (REC) or as two float32 arrays.  For a 16-bit O with the
-// forward's residual, O_i is taken as o_i + o_lo_i.
-template <typename TO, int D, bool REC>
+// forward's residual, O_i is taken as o_i + o_lo_i.  With TC != TO (float32
+// o and dO, 16-bit inputs) it also writes dO rounded to TC (to nearest even,
+// as the kernels' staging rounds it) to p.do16.
+template <typename TO, int D, bool REC, typename TC = TO>
 __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
   using T = TO;  // o and do share the output dtype
   constexpr int E = sizeof(T);
@@ -86,6 +88,13 @@ __global__ __launch_bounds__(256) void attn_bwd_pre_kernel(BwdParams p) {
     // 15 % faster with that cache policy).
     const vec16 o = __builtin_nontemporal_load(reinterpret_cast<const vec16*>(orow + part * (16 / E)));
     const vec16 g = __builtin_nontemporal_load(reinterpret_cast<const vec16*>(grow + part * (16 / E)));
+    if constexpr (!__is_same(TC, TO)) {
+      typedef TC cvec __attribute__((ext_vector_type(16 / E)));
+      cvec gc;
+#pragma unroll
+      for (int e = 0; e < 16 / E; ++e) gc[e] = (TC)g[e];
+      *reinterpret_cast<cvec*>(static_cast<TC*>(p.do16) + (bh * p.n_q + i) * D + part * (16 / E)) = gc;
+    }
     float of[16 / E];
 #pragma unroll
     for (int e = 0; e < 16 / E; ++e) of[e] = (float)o[e];
@@ -1928,28 +1937,15 @@ template <> struct BwdShape<float, 128> {
   static constexpr int QS = 1, KV_OCC = 1, QT = 1, BK = 32, Q_OCC = 1;
 };
 
-// D: head dimension of q and k; DV: of v, o and dO (tile shapes of the
-// larger of the two).
+// dK/dV, then dQ (the per-row values already written by the preprocess);
+// pp: the two-group kernels (which the caller has checked the layout for).
 template <typename T, typename TO, int D, int DV, bool CAUSAL>
-static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
+static hipError_t launch_bwd_kernels(BwdParams p, bool pp, hipStream_t stream) {
   using S = BwdShape<T, (D > DV ? D : DV)>;
   using Dk = DkdvTile<T, D, DV, S::QS>;
   void* args[] = {&p};
-  const int64_t rows = (int64_t)p.bh * p.n_q_pad;
-  constexpr int RPB = 256 / (DV * (int)sizeof(TO) / 16);
-  // The two-group kernels exist for 16-bit d = d_v = 64 with dO in the input
-  // dtype; whether they run is the shared predicate's choice.
   constexpr bool PP_CAN = bwd_two_group(sizeof(T) == 2, D, DV, __is_same(T, TO), false, 0);
-  const bool pp = PP_CAN && bwd_two_group(true, D, DV, true, CAUSAL, p.n_q);
-  // The per-row values must be laid out as these kernels read them (records
-  // or two arrays): a plan that disagrees is refused, not launched.
-  if (pp ? p.row_rec == nullptr : (p.s_init == nullptr || p.dp_init == nullptr)) return hipErrorInvalidValue;
-  const void* pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, false>);
-  if constexpr (PP_CAN) {
-    if (pp) pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, true>);
-  }
-  hipError_t e = hipLaunchKernel(pre, dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
   if (p.dk) {
     bool launched = false;
     if constexpr (PP_CAN) {
@@ -1979,6 +1975,49 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   const int dq_lds = 2 * S::BK * (D + DV + 2 * 16 / (int)sizeof(T)) * (int)sizeof(T);
   return hipLaunchKernel(reinterpret_cast<const void*>(attn_bwd_dq_kernel<T, TO, D, DV, S::QT, S::BK, S::Q_OCC, CAUSAL>),
                          dim3((unsigned)((int64_t)p.n_qtiles * p.bh)), dim3(256), args, dq_lds, stream);
+}
+
+// D: head dimension of q and k; DV: of v, o and dO (tile shapes of the
+// larger of the two).
+template <typename T, typename TO, int D, int DV, bool CAUSAL>
+static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
+  void* args[] = {&p};
+  const int64_t rows = (int64_t)p.bh * p.n_q_pad;
+  constexpr int RPB = 256 / (DV * (int)sizeof(TO) / 16);
+  if constexpr (sizeof(T) == 2 && !__is_same(T, TO)) {
+    if (p.do16) {
+      // Float32 o and dO with 16-bit inputs: the preprocess also writes dO
+      // rounded to T (the rounding the staging of these kernels applies), and
+      // the kernels of 16-bit outputs run on that copy.
+      constexpr bool PP_CAN = bwd_two_group(true, D, DV, true, false, 0);
+      const bool pp = PP_CAN && bwd_two_group(true, D, DV, true, CAUSAL, p.n_q);
+      if (pp ? p.row_rec == nullptr : (p.s_init == nullptr || p.dp_init == nullptr)) return hipErrorInvalidValue;
+      const void* pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, false, T>);
+      if constexpr (PP_CAN) {
+        if (pp) pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, true, T>);
+      }
+      const hipError_t e = hipLaunchKernel(pre, dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
+      if (e != hipSuccess) return e;
+      BwdParams p16 = p;
+      p16.d_o = p.do16;
+      p16.sdo = TensorStrides{(int64_t)p.heads * p.n_q * DV, p.n_q * DV, DV};
+      return launch_bwd_kernels<T, T, D, DV, CAUSAL>(p16, pp, stream);
+    }
+  }
+  // The two-group kernels exist for 16-bit d = d_v = 64 with dO in the input
+  // dtype; whether they run is the shared predicate's choice.
+  constexpr bool PP_CAN = bwd_two_group(sizeof(T) == 2, D, DV, __is_same(T, TO), false, 0);
+  const bool pp = PP_CAN && bwd_two_group(true, D, DV, true, CAUSAL, p.n_q);
+  // The per-row values must be laid out as these kernels read them (records
+  // or two arrays): a plan that disagrees is refused, not launched.
+  if (pp ? p.row_rec == nullptr : (p.s_init == nullptr || p.dp_init == nullptr)) return hipErrorInvalidValue;
+  const void* pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, false>);
+  if constexpr (PP_CAN) {
+    if (pp) pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, true>);
+  }
+  const hipError_t e = hipLaunchKernel(pre, dim3((unsigned)((rows + RPB - 1) / RPB)), dim3(256), args, 0, stream);
+  if (e != hipSuccess) return e;
+  return launch_bwd_kernels<T, TO, D, DV, CAUSAL>(p, pp, stream);
 }
 
 template <typename T, typename TO, int D, int DV = D>

@@ -91,6 +91,10 @@ struct BwdParams {
   float* s_init;
   float* dp_init;
   uint4* row_rec;
+  // 16-bit inputs with float32 o and dO: dO rounded to the input dtype
+  // (contiguous [B*H, n_q, DV]), written by the preprocess, so that the
+  // dK/dV and dQ kernels of 16-bit outputs run on it; or null.
+  void* do16;
   const int* kv_len;  // [B] valid keys per batch, or null (all n_k)
   int64_t n_q_pad;  // n_q rounded up to kBwdRowPad
   int64_t n_q;

@@ -104,8 +104,12 @@ static void check_bwd_carving(int64_t B, int64_t H, int64_t nq, int64_t d, int d
   const mea::BwdParams& b = mea::g_last_bwd;
   const size_t rows = (size_t)(B * H) * (size_t)b.n_q_pad;
   CHECK(b.n_q_pad >= nq && b.n_q_pad % mea::kBwdRowPad == 0 && b.n_q_pad - nq < mea::kBwdRowPad, "row padding");
+  // 16-bit inputs with float32 outputs keep a 16-bit copy of dO, and the
+  // kernels of 16-bit outputs (and their per-row layout) then run.
+  const bool do16 = dtype != MEA_F32 && out_f32;
+  CHECK((b.do16 != nullptr) == do16, "dO copy carved exactly for 16-bit inputs with float32 outputs");
   // The layout the host carved is the one the kernels of this problem read.
-  const bool rec = mea::bwd_two_group(dtype != MEA_F32, (int)d, (int)d, !out_f32, causal != 0, nq);
+  const bool rec = mea::bwd_two_group(dtype != MEA_F32, (int)d, (int)d, !out_f32 || do16, causal != 0, nq);
   CHECK((b.row_rec != nullptr) == rec && (b.s_init == nullptr) == rec && (b.dp_init == nullptr) == rec,
         "per-row layout matches the kernels");
   if (b.row_rec) {
@@ -113,6 +117,13 @@ static void check_bwd_carving(int64_t B, int64_t H, int64_t nq, int64_t d, int d
   } else {
     CHECK(inside(b.s_init, rows * 4, WS, need) && inside(b.dp_init, rows * 4, WS, need), "arrays inside");
     CHECK(disjoint(b.s_init, rows * 4, b.dp_init, rows * 4), "per-row arrays overlap");
+  }
+  if (b.do16) {
+    const size_t cbytes = (size_t)(B * H) * (size_t)nq * (size_t)d * 2;
+    CHECK(inside(b.do16, cbytes, WS, need), "dO copy inside the workspace");
+    CHECK(b.row_rec ? disjoint(b.do16, cbytes, b.row_rec, rows * 16)
+                    : disjoint(b.do16, cbytes, b.s_init, rows * 4) && disjoint(b.do16, cbytes, b.dp_init, rows * 4),
+          "dO copy overlaps the per-row values");
   }
   CHECK(mea_attention_bwd(&p, P, P, P, P, nullptr, P, static_cast<float*>(P), P, P, P, WS, need - 1, nullptr) ==
             MEA_ERR_WORKSPACE,

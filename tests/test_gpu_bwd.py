@@ -150,3 +150,34 @@ def test_autograd_function_matches_direct_calls():
     o.backward(g["do"])
     dq, dk, dv = gpu_grads(g, True)
     assert torch.equal(q.grad, dq) and torch.equal(k.grad, dk) and torch.equal(v.grad, dv)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_float32_output_backward_matches_the_staging_path(dtype, d, causal):
+    # With float32 o and dO, mea_attention_bwd rounds dO to the input dtype in
+    # the preprocess and runs the kernels of 16-bit outputs on the copy; the
+    # allocation-free entry point keeps no copy and runs the kernels that
+    # round dO while staging it.  The rounding is the same, so the gradients
+    # must be bitwise equal (and within the bar against the oracle, which the
+    # float32-output cases above check).
+    from paper_2112_05682_amd import _lib
+    from paper_2112_05682_amd.attention import _problem
+    B, H, nq, nk = 2, 3, 700, 650
+    print("f32-out staging case", dtype, d, causal, flush=True)
+    x = to_gpu(attention_inputs(B, H, nq, nk, d, dtype))
+    q, k, v = x["q"], x["k"], x["v"]
+    o, lse = attention_fwd(q, k, v, causal=causal, out_dtype=torch.float32)
+    do = x["do"].to(torch.float32)
+    ref = attention_bwd(q, k, v, o, lse, do, causal=causal)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    p = _problem(q, k, causal, None, True, {"q": q, "k": k, "v": v, "o": o, "d_o": do,
+                                            "dq": dq, "dk": dk, "dv": dv})
+    st = _lib.bwd_noalloc(p, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), None, do.data_ptr(),
+                          lse.data_ptr(), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                          torch.cuda.current_stream().cuda_stream)
+    _lib.check("mea_attention_bwd_noalloc", st)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
+        assert torch.equal(a, b), name
