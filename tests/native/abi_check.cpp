@@ -69,6 +69,11 @@ static void check_fwd_plan(int64_t B, int64_t H, int64_t nq, int64_t nk, int64_t
                                           need ? WS : nullptr, need, nullptr);
   CHECK(st == MEA_OK && mea::g_fwd_calls == before + 1, "fwd call %d", (int)st);
   const mea::FwdParams& f = mea::g_last_fwd;
+  if (dtype != MEA_F32 && d == 64 && causal && nq > 64) {
+    // The causal 16-bit d = 64 plan tiles the queries as the kernel it picks.
+    const int64_t bq = mea::fwd_causal64_bq(nq, B * H);
+    CHECK(f.n_qtiles == (nq + bq - 1) / bq, "causal query tiles of %lld", (long long)bq);
+  }
   // Keys the plan must cover: all of them, except that a decode-shaped causal
   // problem (16-bit, at most 64 queries) can see only its first n_q keys.
   const bool decode = dtype != MEA_F32 && nq <= 64;
@@ -188,7 +193,8 @@ int main() {
   for (int64_t nk : nks)
     for (int dt : {MEA_F32, MEA_BF16})
       for (int causal : {0, 1})
-        for (int64_t nq : {(int64_t)1, (int64_t)100, (int64_t)300, (int64_t)4096}) check_fwd_plan(1, 1, nq, nk, 64, dt, causal);
+        for (int64_t nq : {(int64_t)1, (int64_t)100, (int64_t)300, (int64_t)4096, (int64_t)4097})
+          check_fwd_plan(1, 1, nq, nk, 64, dt, causal);
   check_fwd_plan(2, 3, 256, 1 << 20, 128, MEA_F16, 0);
   for (int64_t nq : {(int64_t)1, (int64_t)63, (int64_t)64, (int64_t)65, (int64_t)2048, (int64_t)2049, (int64_t)16384})
     for (int dt : {MEA_F32, MEA_BF16})

@@ -47,13 +47,15 @@ def test_forward_small(dtype, d, causal, shape):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
-@pytest.mark.parametrize("shape", [(1, 16, 12288), (1, 16, 12800), (4, 64, 4096), (4, 64, 4097)],
+@pytest.mark.parametrize("shape", [(1, 16, 12288), (1, 16, 12800), (4, 64, 4096), (4, 64, 4097),
+                                   (1, 4, 4096), (1, 4, 4097)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_forward_causal_d64_both_kernels(dtype, shape):
-    # Causal 16-bit d = 64 problems run the two-group kernel when they have
-    # more than 4096 queries and at least 2.5e9 query-key pairs (batch x heads
-    # x n^2), else the 4-wave kernel: both sides of both bounds (12288 / 12800
-    # queries at 16 heads: 2.42e9 / 2.62e9 pairs; 4096 / 4097 queries at 256
+    # Causal 16-bit d = 64 problems of up to 4096 queries run the 4-wave
+    # kernel; longer ones the two-group kernel, with 512-query workgroups when
+    # they have at least 2.5e9 query-key pairs (batch x heads x n^2), else with
+    # 256-query ones: every side of each bound (12288 / 12800 queries at 16
+    # heads: 2.42e9 / 2.62e9 pairs; 4096 / 4097 queries at 256 and at 4
     # heads), sampled rows of a few slices against the oracle.
     B, H, n = shape
     print("causal d64 switch case", shape, dtype, flush=True)
