@@ -439,15 +439,13 @@ constexpr int BK = 64, NW = 8, NSTAGE = 3;
 template <int D> constexpr int BQ = NW * Cfg<D>::QT * 32;  // queries per workgroup
 }  // namespace pp
 
-// QTP: query sub-tiles of 32 per wave (d = 64: 2, or 1 for 256-query
-// workgroups on smaller causal problems).
-template <typename T, typename TO, int D, bool CAUSAL, int QTP = pp::Cfg<D>::QT>
+template <typename T, typename TO, int D, bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   using pp::BK;
   using pp::NSTAGE;
   using pp::NW;
   using C = pp::Cfg<D>;
-  constexpr int QT = QTP, BQ = NW * QT * 32;
+  constexpr int QT = C::QT, BQ = pp::BQ<D>;
   constexpr int ROWB = D * 2;              // bytes per LDS row (unpadded)
   constexpr int TILEB = BK * ROWB;         // one K or V tile: 8 or 16 KiB
   constexpr int CPR = ROWB / 16;           // 16-byte chunks per row
@@ -458,7 +456,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_pp_kernel(FwdParams p) {
   auto swz_v = [](int r) { return C::swz_v(r); };
   // 16-key chunks of query sub-tile 0 whose weights are computed in the MFMA
   // phase (interleaved with the PV MFMAs); the rest go to the softmax phase.
-  constexpr int W0 = QT == C::QT ? C::W0 : 0;
+  constexpr int W0 = C::W0;
   static_assert(W0 >= 0 && W0 <= NPC, "weight chunks");
   static_assert(sizeof(T) == 2, "16-bit inputs only");
 
@@ -1135,11 +1133,10 @@ static hipError_t launch_fwd_impl(const FwdParams& p, hipStream_t stream) {
   return launch_combine<TO, DV>(p, stream);
 }
 
-template <typename T, typename TO, int D, bool CAUSAL, int QTP = pp::Cfg<D>::QT>
+template <typename T, typename TO, int D, bool CAUSAL>
 static hipError_t launch_fwd_pp(const FwdParams& p, hipStream_t stream) {
-  auto kern = attn_fwd_pp_kernel<T, TO, D, CAUSAL, QTP>;
-  constexpr int BQ = pp::NW * QTP * 32;
-  if (p.n_qtiles != (p.n_q + BQ - 1) / BQ) return hipErrorInvalidValue;
+  auto kern = attn_fwd_pp_kernel<T, TO, D, CAUSAL>;
+  if (p.n_qtiles != (p.n_q + pp::BQ<D> - 1) / pp::BQ<D>) return hipErrorInvalidValue;
   const int64_t grid = (int64_t)p.n_qtiles * p.bh * p.n_splits;
   FwdParams pc = p;
   void* args[] = {&pc};
@@ -1156,10 +1153,8 @@ static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t str
     if constexpr (D == 64) {
       // Short or small causal problems: the 4-wave kernel with 128-query
       // workgroups.
-      const int bq = fwd_causal64_bq(p.n_q, p.bh);
-      if (bq == 128)
+      if (fwd_causal64_bq(p.n_q, p.bh) == 128)
         return launch_fwd_impl<T, TO, 64, 64, 1, FwdShape<T, 64>::BK, MEA_T64_FWD_OCC, true>(p, stream);
-      if (bq == 256) return launch_fwd_pp<T, TO, 64, true, 1>(p, stream);
     }
     return launch_fwd_pp<T, TO, D, true>(p, stream);
   } else {

@@ -140,41 +140,43 @@ inline bool bwd_uses_row_records(int dtype, int d, int dv, bool out_f32, bool ca
 #ifndef MEA_T64_FWD_BQ
 #define MEA_T64_FWD_BQ 512
 #endif
+// Three workgroups per CU (166 registers, no spills) measured 4-10 % faster
+// than two on the causal problems this kernel runs (4x32x4096, 8x16x2048,
+// 16x16x1024).
 #ifndef MEA_T64_FWD_OCC
-#define MEA_T64_FWD_OCC 2
+#define MEA_T64_FWD_OCC 3
 #endif
 template <typename T, int D> struct FwdShape;
 template <> struct FwdShape<__bf16, 64> {
   static constexpr int BQ = MEA_T64_FWD_BQ, QT = BQ == 512 ? 2 : BQ / 128, BK = 64, OCC = MEA_T64_FWD_OCC;
 };
-// 16-bit d = d_v = 64 causal forward, by workgroup size (returned): up to
-// MEA_T64_FWD_CAUSAL_SMALL queries the 4-wave kernel with 128-query
-// workgroups; above that the two-group kernel with 512-query workgroups
-// (two 32-query sub-tiles per wave) for problems of at least
-// MEA_T64_FWD_CAUSAL_MIN_PAIRS (batch x heads x n_q^2) query-key pairs, and
-// with 256-query workgroups (one sub-tile per wave) for smaller ones.  A
-// 512-query workgroup spends 8 key tiles on the diagonal, half of that work
-// masked, which short sequences do not amortise, and a small grid of such
-// workgroups (a few hundred, for 256 CUs) balances poorly.  Measured on causal
-// bf16 problems: the 4-wave kernel 7-18 % faster than the 256-query one at
-// n <= 4096 (16-256 heads); the 256-query one 5-15 % faster than the 4-wave
-// one at 2x8x8192, 1x32x8192, 1x12x12288, 1x8x16384 and 4x16x4608 (at most
-// 2.1e9 pairs), the 512-query one 7-14 % faster than the 256-query one at
-// 4x32x4608, 8x16x6144, 4x32x8192, 2x16x12288, 1x16x16384 and 1x8x32768 (at
-// least 2.7e9).  Host plan and launch both use this.
+// 16-bit d = d_v = 64 causal forward: the two-group kernel (512-query
+// workgroups, returns 512) for problems of more than MEA_T64_FWD_CAUSAL_SMALL
+// queries with at least MEA_T64_FWD_CAUSAL_MIN_PAIRS (batch x heads x n_q^2)
+// query-key pairs and at least MEA_T64_FWD_CAUSAL_MIN_WGS such workgroups,
+// else the 4-wave kernel with 128-query workgroups (128).  A 512-query
+// workgroup spends 8 key tiles on the diagonal, half of that work masked,
+// which short sequences do not amortise, and a small grid of such workgroups
+// (a few hundred, for 256 CUs) balances poorly.  Measured on causal bf16
+// problems, the 4-wave kernel at three workgroups per CU against the
+// two-group kernel: 2-3 % faster at 4x32x4608 and 8x16x6144, 5 % at
+// 1x4x32768 (256 two-group workgroups), and faster at every n <= 4096; the
+// two-group kernel 3.5, 8 and 18 % faster at 4x32x8192, 2x16x12288 and
+// 1x16x16384.  Host plan and launch both use this.
 #ifndef MEA_T64_FWD_CAUSAL_SMALL
-#define MEA_T64_FWD_CAUSAL_SMALL 4096
+#define MEA_T64_FWD_CAUSAL_SMALL 6144
 #endif
 #ifndef MEA_T64_FWD_CAUSAL_MIN_PAIRS
 #define MEA_T64_FWD_CAUSAL_MIN_PAIRS 2.5e9
 #endif
-#ifndef MEA_T64_FWD_CAUSAL_MID
-#define MEA_T64_FWD_CAUSAL_MID 256
+#ifndef MEA_T64_FWD_CAUSAL_MIN_WGS
+#define MEA_T64_FWD_CAUSAL_MIN_WGS 384
 #endif
 inline int fwd_causal64_bq(int64_t n_q, int64_t bh) {
-  if (n_q <= MEA_T64_FWD_CAUSAL_SMALL) return 128;
-  const bool big = (double)bh * (double)n_q * (double)n_q >= (double)MEA_T64_FWD_CAUSAL_MIN_PAIRS;
-  return big ? 512 : MEA_T64_FWD_CAUSAL_MID;
+  const bool big = n_q > MEA_T64_FWD_CAUSAL_SMALL &&
+                   (double)bh * (double)n_q * (double)n_q >= (double)MEA_T64_FWD_CAUSAL_MIN_PAIRS &&
+                   bh * ((n_q + 511) / 512) >= MEA_T64_FWD_CAUSAL_MIN_WGS;
+  return big ? 512 : 128;
 }
 // 16-bit d = 128: BQ = 256 selects the two-group kernel (8 waves of 32
 // queries); 128 the 4-wave kernel.  Problems with d_v != d always run the

@@ -196,6 +196,15 @@ int main() {
         for (int64_t nq : {(int64_t)1, (int64_t)100, (int64_t)300, (int64_t)4096, (int64_t)4097})
           check_fwd_plan(1, 1, nq, nk, 64, dt, causal);
   check_fwd_plan(2, 3, 256, 1 << 20, 128, MEA_F16, 0);
+  // Both sides of each bound of the causal d = 64 kernel choice.
+  for (int64_t nq : {(int64_t)6144, (int64_t)6145})
+    check_fwd_plan(2, 64, nq, nq, 64, MEA_BF16, 1);
+  for (int64_t h : {(int64_t)4, (int64_t)6}) check_fwd_plan(1, h, 32768, 32768, 64, MEA_F16, 1);
+  for (int64_t nq : {(int64_t)12288, (int64_t)12800}) check_fwd_plan(1, 16, nq, nq, 64, MEA_BF16, 1);
+  CHECK(mea::fwd_causal64_bq(6144, 128) == 128 && mea::fwd_causal64_bq(6145, 128) == 512 &&
+            mea::fwd_causal64_bq(32768, 4) == 128 && mea::fwd_causal64_bq(32768, 6) == 512 &&
+            mea::fwd_causal64_bq(12288, 16) == 128 && mea::fwd_causal64_bq(12800, 16) == 512,
+        "causal d = 64 kernel choice");
   for (int64_t nq : {(int64_t)1, (int64_t)63, (int64_t)64, (int64_t)65, (int64_t)2048, (int64_t)2049, (int64_t)16384})
     for (int dt : {MEA_F32, MEA_BF16})
       for (int64_t d : {(int64_t)64, (int64_t)128}) {

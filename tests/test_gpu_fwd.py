@@ -47,16 +47,17 @@ def test_forward_small(dtype, d, causal, shape):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
-@pytest.mark.parametrize("shape", [(1, 16, 12288), (1, 16, 12800), (4, 64, 4096), (4, 64, 4097),
-                                   (1, 4, 4096), (1, 4, 4097)],
+@pytest.mark.parametrize("shape", [(1, 16, 12288), (1, 16, 12800), (2, 64, 6144), (2, 64, 6145),
+                                   (1, 4, 32768), (1, 6, 32768)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_forward_causal_d64_both_kernels(dtype, shape):
-    # Causal 16-bit d = 64 problems of up to 4096 queries run the 4-wave
-    # kernel; longer ones the two-group kernel, with 512-query workgroups when
-    # they have at least 2.5e9 query-key pairs (batch x heads x n^2), else with
-    # 256-query ones: every side of each bound (12288 / 12800 queries at 16
-    # heads: 2.42e9 / 2.62e9 pairs; 4096 / 4097 queries at 256 and at 4
-    # heads), sampled rows of a few slices against the oracle.
+    # Causal 16-bit d = 64 problems run the two-group kernel when they have
+    # more than 6144 queries, at least 2.5e9 query-key pairs (batch x heads x
+    # n^2) and at least 384 workgroups of 512 queries, else the 4-wave kernel:
+    # both sides of each bound (12288 / 12800 queries at 16 heads: 2.42e9 /
+    # 2.62e9 pairs; 6144 / 6145 queries at 128 heads; 32768 queries at 4 / 6
+    # heads: 256 / 384 workgroups), sampled rows of a few slices against the
+    # oracle.
     B, H, n = shape
     print("causal d64 switch case", shape, dtype, flush=True)
     x = attention_inputs(B, H, n, n, 64, dtype, with_grad=False)
