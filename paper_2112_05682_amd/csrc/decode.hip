@@ -10,10 +10,12 @@
 // 16-bit inputs against 4 d n_q flops), so the kernel is shaped for bytes in
 // flight rather than for matrix throughput: one wave per workgroup, a
 // two-stage LDS ring of asynchronous copies per wave, and enough workgroups
-// per CU (the ring is 36 KiB) to keep about 64 KiB of copies in flight per
-// CU.  The scores and the weighted values still go through MFMA with the
+// per CU (the ring is 36 KiB, 32 KiB with swizzled rows) to keep about
+// 64 KiB of copies in flight per CU.  The scores and the weighted values still go through MFMA with the
 // query group padded to 32 or 64 columns: at n_q <= 64 the padded matrix work
 // stays below the HBM time.
+#include <type_traits>
+
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -36,6 +38,23 @@ struct Cfg {
   static constexpr int STAGEB = 2 * TILEB;  // K tile, V tile
   static_assert(BK * RSB <= TILEB, "rows fit the tile");
 };
+// The same tiles in unpadded 256-byte rows (d = 128) whose 16-byte chunks are
+// XOR-swizzled: the physical chunk of logical chunk x in row r is
+// x ^ swz(r), with r & 15 for K (row reads) and (r & 3) << 2 for V
+// (transposing reads), so that both touch distinct banks.  A copy moves RPU = 4
+// rows; the K swizzle repeats every KP = 4 copies and the V swizzle within
+// one, so a lane needs KP + 1 copy offsets instead of the padded layout's
+// 4 NCOPY (row, column and both offsets per copy).
+struct Swz128 {
+  static constexpr int BK = 32, ROWB = 256, CPR = 16, RPU = 4, KP = 4;
+  static constexpr int NCOPY = BK * ROWB / 1024;
+  static constexpr int TILEB = BK * ROWB;
+  static constexpr int NSTAGE = 2;
+  static constexpr int STAGEB = 2 * TILEB;
+  __device__ static __forceinline__ int swz_k(int r) { return r & 15; }
+  __device__ static __forceinline__ int swz_v(int r) { return (r & 3) << 2; }
+  static_assert(NCOPY % KP == 0 && RPU * KP == 16, "copy geometry");
+};
 }  // namespace dec
 
 // Top-left causal (key j visible to query i iff j <= i): only the first n_q
@@ -48,11 +67,18 @@ __host__ __device__ inline int64_t decode_keys(int64_t n_q, int64_t n_k, bool ca
 // [split * keys_per_split, ...).  Scores in the orientation S^T = K Q^T (lane =
 // query, registers = keys, K rows read in the perm32 order so that the
 // weights convert in place into the B operand of O^T += V^T P^T).
+// With two query sub-tiles at d = 128 the padded layout's copy offsets (36
+// registers) spilled and were reloaded in the tile loop; that variant uses the
+// swizzled rows (SWZ).  The others keep the padded rows, whose reads need no
+// per-fragment address arithmetic.
 template <typename T, typename TO, int D, int QT, bool CAUSAL>
 __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
-  using C = dec::Cfg<D>;
+  constexpr bool SWZ = D == 128 && QT == 2;
+  using C = std::conditional_t<SWZ, dec::Swz128, dec::Cfg<D>>;
+  using P = dec::Cfg<D>;
+  using S = dec::Swz128;
   constexpr int BK = C::BK, NKT = BK / 32, KC = D / 16, NDT = D / 32, NPC = BK / 16;
-  constexpr int RS = C::RSB / 2;  // LDS row stride in elements
+  constexpr int RS = P::RSB / 2;  // padded LDS row stride in elements
   __shared__ __align__(16) unsigned char smem[C::NSTAGE * C::STAGEB];
 
   const int lane = threadIdx.x;
@@ -88,36 +114,71 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
     }
   }
 
-  // Copy u of a tile moves lane slots 64 u + lane: row slot / SPR, 16-byte
-  // chunk slot % SPR (the pad slot gets a copy of the last chunk); slots past
-  // the tile's rows repeat its last slot.  The row and the byte column of
-  // each copy are computed once, and the byte offsets within a tile of K and
-  // of V (row strides < 2^24 elements, checked on the host).
-  int urow[C::NCOPY];
-  unsigned ucol[C::NCOPY], ukoff[C::NCOPY], uvoff[C::NCOPY];
+  // Padded rows: copy u of a tile moves lane slots 64 u + lane: row
+  // slot / SPR, 16-byte chunk slot % SPR (the pad slot gets a copy of the last
+  // chunk); slots past the tile's rows repeat its last slot.  The row and the
+  // byte column of each copy are computed once, and the byte offsets within a
+  // tile of K and of V (row strides < 2^24 elements, checked on the host).
+  // Swizzled rows: copy u moves rows 4 u .. 4 u + 3, lane l writing physical
+  // chunk l % 16 of row 4 u + l / 16; the K offset of copy u is that of copy
+  // u % KP (plus a scalar shift of 16 (u / KP) rows), the V offset is the same
+  // for every copy.
+  constexpr int NPAD = SWZ ? 1 : C::NCOPY;
+  int urow[NPAD];
+  unsigned ucol[NPAD], ukoff[NPAD], uvoff[NPAD];
+  unsigned skoff[S::KP], svoff = 0;
+  const int lrow = lane / S::CPR, lx = lane % S::CPR;
+  if constexpr (SWZ) {
 #pragma unroll
-  for (int u = 0; u < C::NCOPY; ++u) {
-    int slot = 64 * u + lane;
-    if (slot >= C::NSLOT) slot = C::NSLOT - 1;
-    const int ch = slot % C::SPR;
-    urow[u] = slot / C::SPR;
-    ucol[u] = (unsigned)(16 * (ch < C::SPR - 1 ? ch : C::SPR - 2));
-    ukoff[u] = (unsigned)urow[u] * (unsigned)(2 * p.sk.r) + ucol[u];
-    uvoff[u] = (unsigned)urow[u] * (unsigned)(2 * p.sv.r) + ucol[u];
+    for (int b = 0; b < S::KP; ++b) {
+      const int row = S::RPU * b + lrow;
+      skoff[b] = 2u * ((unsigned)row * (unsigned)p.sk.r + 8u * (unsigned)(lx ^ S::swz_k(row)));
+    }
+    svoff = 2u * ((unsigned)lrow * (unsigned)p.sv.r + 8u * (unsigned)(lx ^ S::swz_v(lrow)));
+  } else {
+#pragma unroll
+    for (int u = 0; u < NPAD; ++u) {
+      int slot = 64 * u + lane;
+      if (slot >= P::NSLOT) slot = P::NSLOT - 1;
+      const int ch = slot % P::SPR;
+      urow[u] = slot / P::SPR;
+      ucol[u] = (unsigned)(16 * (ch < P::SPR - 1 ? ch : P::SPR - 2));
+      ukoff[u] = (unsigned)urow[u] * (unsigned)(2 * p.sk.r) + ucol[u];
+      uvoff[u] = (unsigned)urow[u] * (unsigned)(2 * p.sv.r) + ucol[u];
+    }
   }
   auto copy_tile = [&](int j) __attribute__((always_inline)) {
     const int64_t k0 = kb + (int64_t)j * BK;
     unsigned char* st = smem + (j % C::NSTAGE) * C::STAGEB;
     const unsigned kl = lds_addr(st), vl = lds_addr(st + C::TILEB);
-    if (k0 + BK <= ke) {
+    const bool full = k0 + BK <= ke;
+    if constexpr (SWZ) {
+      if (full) {
+#pragma unroll
+        for (int u = 0; u < C::NCOPY; ++u) {
+          copy_to_lds16_sb<true>(kg + (k0 + 16 * (u / S::KP)) * p.sk.r, skoff[u % S::KP],
+                                 __builtin_amdgcn_readfirstlane(kl + 1024 * u));
+          copy_to_lds16_sb<true>(vg + (k0 + S::RPU * u) * p.sv.r, svoff, __builtin_amdgcn_readfirstlane(vl + 1024 * u));
+        }
+      } else {
+        // Ragged last tile: rows past the range repeat its last key (finite
+        // values, masked below).
+#pragma unroll
+        for (int u = 0; u < C::NCOPY; ++u) {
+          const int row = S::RPU * u + lrow;
+          int64_t key = k0 + row;
+          if (key > ke - 1) key = ke - 1;
+          copy_to_lds16<true>(kg + key * p.sk.r + 8 * (lx ^ S::swz_k(row)), __builtin_amdgcn_readfirstlane(kl + 1024 * u));
+          copy_to_lds16<true>(vg + key * p.sv.r + 8 * (lx ^ S::swz_v(row)), __builtin_amdgcn_readfirstlane(vl + 1024 * u));
+        }
+      }
+    } else if (full) {
 #pragma unroll
       for (int u = 0; u < C::NCOPY; ++u) {
         copy_to_lds16_sb<true>(kg + k0 * p.sk.r, ukoff[u], __builtin_amdgcn_readfirstlane(kl + 1024 * u));
         copy_to_lds16_sb<true>(vg + k0 * p.sv.r, uvoff[u], __builtin_amdgcn_readfirstlane(vl + 1024 * u));
       }
     } else {
-      // Ragged last tile: rows past the range repeat its last key (finite
-      // values, masked below).
 #pragma unroll
       for (int u = 0; u < C::NCOPY; ++u) {
         int64_t key = k0 + urow[u];
@@ -167,7 +228,13 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc) {
-        const Frag<T> kf = lds_frag<T>(ks + (32 * kt + krow) * RS + 16 * kc + 8 * h);
+        const int row = 32 * kt + krow;
+        Frag<T> kf;
+        if constexpr (SWZ)
+          kf = *reinterpret_cast<const Frag<T>*>(reinterpret_cast<const unsigned char*>(ks) + row * S::ROWB +
+                                                   16 * ((2 * kc + h) ^ S::swz_k(row)));
+        else
+          kf = lds_frag<T>(ks + row * RS + 16 * kc + 8 * h);
 #pragma unroll
         for (int t = 0; t < QT; ++t) s[t][kt] = mma(kf, qf[t][kc], s[t][kt]);
       }
@@ -216,12 +283,29 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
       }
     }
 
-    // O^T += V^T P^T (one V fragment serves every query sub-tile).
+    // O^T += V^T P^T (one V fragment serves every query sub-tile); swizzled
+    // rows: the transposing reads of lds_col_frag with the V swizzle applied.
+    const int g4 = lane >> 4, i4 = lane & 15;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
       for (int pc = 0; pc < NPC; ++pc) {
-        const Frag<T> vf = lds_col_frag<T>(vs, RS, 16 * pc, 32 * dt, lane);
+        Frag<T> vf;
+        if constexpr (SWZ) {
+          const unsigned char* vb = reinterpret_cast<const unsigned char*>(vs);
+          const int row = 16 * pc + 8 * (g4 >> 1) + (i4 >> 2);
+          const int colb = 2 * (32 * dt + 16 * (g4 & 1) + 4 * (i4 & 3));
+          const v4s_t lo = lds_read_tr16(vb + row * S::ROWB + (((colb >> 4) ^ S::swz_v(row)) << 4) + (colb & 15));
+          const v4s_t hi =
+              lds_read_tr16(vb + (row + 4) * S::ROWB + (((colb >> 4) ^ S::swz_v(row + 4)) << 4) + (colb & 15));
+          typedef short v8s_t __attribute__((ext_vector_type(8)));
+          v8s_t r8;
+          r8[0] = lo[0]; r8[1] = lo[1]; r8[2] = lo[2]; r8[3] = lo[3];
+          r8[4] = hi[0]; r8[5] = hi[1]; r8[6] = hi[2]; r8[7] = hi[3];
+          vf = __builtin_bit_cast(Frag<T>, r8);
+        } else {
+          vf = lds_col_frag<T>(vs, RS, 16 * pc, 32 * dt, lane);
+        }
 #pragma unroll
         for (int t = 0; t < QT; ++t) acc[t][dt] = mma(vf, pf[t][pc], acc[t][dt]);
       }

@@ -52,9 +52,11 @@ def test_decode_causal(d, nq, nk):
 
 
 @pytest.mark.parametrize("d", [64, 128])
-def test_decode_many_ranges(d):
-    # One (batch, head): the keys are split into many ranges (workspace > 0).
-    B, H, nq, nk = 1, 1, 3, 200000
+@pytest.mark.parametrize("nq", [3, 48])
+def test_decode_many_ranges(d, nq):
+    # One (batch, head): the keys are split into many ranges (workspace > 0);
+    # 48 queries run two 32-query sub-tiles per wave.
+    B, H, nk = 1, 1, 200001
     assert _lib.fwd_workspace_size(_lib.problem(B, H, nq, nk, d, 2, False, d ** -0.5)) > 0
     run_case(B, H, nq, nk, d, "bf16")
 
