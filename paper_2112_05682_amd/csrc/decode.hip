@@ -253,7 +253,12 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
       }
     }
 
-    // Online softmax per query (lane): running maximum in units of c S.
+    // Online softmax per query (lane), with the lazy reference m_run (in units
+    // of c S): it rises only when a score exceeds it by more than
+    // kRescaleSlack powers of two, so most tiles skip the rescale of the
+    // running numerator and denominator (both share the reference, so the
+    // result is the same).  A query with no visible key yet keeps
+    // m_run = -inf and offset 0 (its weights are 2^-inf = 0).
     Frag<T> pf[QT][NPC];
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
@@ -262,22 +267,26 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][kt][r]);
-      mx = xhalf_max(mx) * cl2;
-      const float m_new = fmaxf(m_run[t], mx);
-      // No visible key yet: reference 0 (every weight is 2^-inf = 0).
-      const float mref = m_new == -INFINITY ? 0.0f : m_new;
-      const float alpha = fast_exp2(m_run[t] - mref);
-      m_run[t] = m_new;
-      l_run[t] *= alpha;
+      const float mx_c = xhalf_max(mx) * cl2;
+      const bool raise = mx_c > m_run[t] + kRescaleSlack;
+      if (__builtin_amdgcn_ballot_w64(raise)) {
+        const float m_new = raise ? mx_c : m_run[t];
+        // 0 on a first raise; 1 for a lane that does not raise (also one
+        // still at -inf, where the difference would be NaN).
+        const float alpha = raise ? fast_exp2(m_run[t] - m_new) : 1.0f;
+        m_run[t] = m_new;
+        l_run[t] *= alpha;
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
+        for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[t][dt][r] *= alpha;
+          for (int r = 0; r < 16; ++r) acc[t][dt][r] *= alpha;
+      }
+      const float neg = m_run[t] == -INFINITY ? 0.0f : -m_run[t];
 #pragma unroll
       for (int pc = 0; pc < NPC; ++pc) {
         float w8[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) w8[e] = fast_exp2(fmaf(s[t][pc >> 1][8 * (pc & 1) + e], cl2, -mref));
+        for (int e = 0; e < 8; ++e) w8[e] = fast_exp2(fmaf(s[t][pc >> 1][8 * (pc & 1) + e], cl2, neg));
         pf[t][pc] = to_frag<T>(w8);
         l_run[t] = tree_sum<8>(w8, l_run[t]);
       }
@@ -352,7 +361,7 @@ __global__ __launch_bounds__(64) void attn_decode_kernel(FwdParams p) {
           *reinterpret_cast<f32x4*>(po + 32 * dt + 8 * a4 + 4 * h) = v4;
         }
       if (h == 0) {
-        p.part_m[prow] = m_run[t];  // log2 units (scaled), -inf if the range has no visible key
+        p.part_m[prow] = m_run[t];  // reference, log2 units (scaled); -inf if the range has no visible key
         p.part_l[prow] = l_tot;
       }
     }

@@ -27,10 +27,6 @@
 
 namespace mea {
 
-// A tile raises the reference maximum only when one of its scores exceeds it
-// by more than this many powers of two (weights then stay <= 2^8).
-constexpr float kRescaleSlack = 8.0f;
-constexpr float kRescaleBound = 256.0f;  // 2^kRescaleSlack
 constexpr float kLn2 = 0.6931471805599453f;
 
 template <bool B> struct BoolC { static constexpr bool value = B; };

@@ -59,6 +59,13 @@ struct FwdParams {
 // that the work stays parallel when there are few rows and many ranges.
 constexpr int kCombineGroup = 16;
 
+// Lazy reference maximum of the forward kernels (Section 3's running maximum,
+// raised lazily): a tile raises the reference only when one of its scores
+// exceeds it by more than this many powers of two, so weights stay <= 2^8 and
+// the running numerator and denominator are rescaled only on such tiles.
+constexpr float kRescaleSlack = 8.0f;
+constexpr float kRescaleBound = 256.0f;  // 2^kRescaleSlack
+
 // Floats of the second partial buffer (0 when the combine is one stage).
 inline size_t combine_stage_floats(int64_t n_splits, int64_t rows, int64_t d) {
   if (n_splits <= kCombineGroup) return 0;
