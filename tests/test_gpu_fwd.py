@@ -102,6 +102,45 @@ def test_forward_key_splits_float32_output():
     run_and_compare(1, 1, 256, 40000, 128, "bf16", False, out_dtype=torch.float32)
 
 
+def rising_inputs(B, H, nq, nk, d, dtype, seed=0):
+    """Logits that climb and fall across key tiles: feature 0 of every key
+    carries a level L_j = 40 sin(2 pi j / 700) + 60 j / n_k (log2 units at
+    q_0 = 4), which rises by up to 23 powers of two per 64 keys, so the lazy
+    reference of the forward kernels is raised on tile after tile and left
+    alone on the falling stretches.  Query feature 0 is 4 +- 0.5 per row, so
+    rows differ in slope."""
+    x = attention_inputs(B, H, nq, nk, d, dtype, with_grad=False, seeds=(seed, seed + 1, seed + 2, seed + 3))
+    j = torch.arange(nk, dtype=torch.float64)
+    level = 40.0 * torch.sin(2 * np.pi * j / 700.0) + 60.0 * j / nk
+    k0 = level / (4.0 * d ** -0.5 * np.log2(np.e))
+    u = torch.linspace(-0.5, 0.5, nq, dtype=torch.float64)
+    q = x["q"].to(torch.float64)
+    k = x["k"].to(torch.float64)
+    q[..., 0] = 4.0 + u
+    k[..., 0] = k0
+    x["q"], x["k"] = q.to(x["v"].dtype), k.to(x["v"].dtype)
+    return x
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("shape", [(1, 2, 1, 3000), (1, 2, 48, 3000), (1, 2, 300, 3000), (1, 1, 256, 40000)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_forward_rising_and_falling_logits(d, causal, shape):
+    # Decode (1 and 48 queries), the tiled kernels (300 queries) and key
+    # splits (256 x 40000): every lazy-reference path against the oracle.
+    B, H, nq, nk = shape
+    print("rising logits case", shape, d, causal, flush=True)
+    x = rising_inputs(B, H, nq, nk, d, "bf16")
+    g = to_gpu(x)
+    o, lse = attention_fwd(g["q"], g["k"], g["v"], causal=causal)
+    torch.cuda.synchronize()
+    ro, rl = oracle.fwd(f64(x["q"]), f64(x["k"]), f64(x["v"]), scale=d ** -0.5, causal=causal)
+    assert np.all(np.isfinite(f64(lse)))
+    check("O", f64(o), ro, TOL["bf16"])
+    check_lse(f64(lse), rl)
+
+
 @pytest.mark.parametrize("d", [64, 128])
 def test_forward_large_logits(d):
     # Q and K scaled by 30 before rounding: logits reach ~1e3, far beyond the
