@@ -30,6 +30,7 @@ CASES = [  # B, H, nq, nk, d, dtype, causal, kv_len, out_f32
     (2, 3, 150, 200, 64, "fp32", True, [200, 33], False),
     (3, 4, 5, 3000, 64, "bf16", False, [3000, 1234, 0], False),  # decode kernel
     (2, 2, 40, 2000, 128, "fp16", True, [1, 1999], False),
+    (2, 2, 48, 3000, 128, "bf16", False, [3000, 1001], False),   # two sub-tiles, swizzled rows
     (2, 1, 256, 40000, 64, "bf16", False, [40000, 777], False),  # key splits + staged combine
     (2, 2, 100, 300, 64, "bf16", False, [-5, 1 << 20], False),   # lengths clamp to [0, n_k]
 ]
@@ -79,7 +80,7 @@ def test_key_padding_matches_oracle(case):
         check_lse(gl[b], rl[b])
 
 
-@pytest.mark.parametrize("case", [CASES[0], CASES[4], CASES[7], CASES[9]], ids=_ids)
+@pytest.mark.parametrize("case", [CASES[0], CASES[4], CASES[7], CASES[10]], ids=_ids)
 def test_padded_values_do_not_matter_and_full_length_is_unpadded(case):
     B, H, nq, nk, d, dtype, causal, kv_len, out_f32 = case
     print("kv_len invariance", _ids(case), flush=True)
