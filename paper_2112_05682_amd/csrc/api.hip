@@ -99,10 +99,10 @@ void fwd_tiles(int dtype, int64_t d, int64_t dv, bool causal, int64_t n_q, int64
     *bq = mea::FwdShape<float, 64>::BQ;
     *bk = mea::FwdShape<float, 64>::BK;
   } else if (d == 64 && dv == 64) {
-    *bq = causal && mea::FwdShape<__bf16, 64>::BQ == 512 ? mea::fwd_causal64_bq(n_q, bh) : mea::FwdShape<__bf16, 64>::BQ;
+    *bq = mea::FwdShape<__bf16, 64>::BQ == 512 ? mea::fwd64_bq(n_q, bh, causal) : mea::FwdShape<__bf16, 64>::BQ;
     *bk = mea::FwdShape<__bf16, 64>::BK;
   } else if (d == 128 && dv == 128) {
-    *bq = mea::FwdShape<__bf16, 128>::BQ;
+    *bq = mea::FwdShape<__bf16, 128>::BQ == 256 ? mea::fwd128_bq(n_q, causal) : mea::FwdShape<__bf16, 128>::BQ;
     *bk = mea::FwdShape<__bf16, 128>::BK;
   } else {  // d_v != d: the 4-wave kernel
     *bq = mea::kFwdBq4wave128;

@@ -1145,14 +1145,19 @@ static hipError_t launch_fwd_pp(const FwdParams& p, hipStream_t stream) {
 template <typename T, typename TO, int D>
 static hipError_t launch_fwd_dt(const FwdParams& p, bool causal, hipStream_t stream) {
   if constexpr (sizeof(T) == 2 && FwdShape<T, D>::BQ == pp::BQ<D>) {
-    if (!causal) return launch_fwd_pp<T, TO, D, false>(p, stream);
+    // Short or small problems: the 4-wave kernel with 128-query workgroups
+    // (the same choice as the host plan's).
     if constexpr (D == 64) {
-      // Short or small causal problems: the 4-wave kernel with 128-query
-      // workgroups.
-      if (fwd_causal64_bq(p.n_q, p.bh) == 128)
-        return launch_fwd_impl<T, TO, 64, 64, 1, FwdShape<T, 64>::BK, MEA_T64_FWD_OCC, true>(p, stream);
+      if (fwd64_bq(p.n_q, p.bh, causal) == 128)
+        return causal ? launch_fwd_impl<T, TO, 64, 64, 1, FwdShape<T, 64>::BK, MEA_T64_FWD_OCC, true>(p, stream)
+                      : launch_fwd_impl<T, TO, 64, 64, 1, FwdShape<T, 64>::BK, MEA_T64_FWD_OCC, false>(p, stream);
+    } else {
+      using S = FwdShape<T, 128>;
+      if (fwd128_bq(p.n_q, causal) == kFwdBq4wave128)
+        return causal ? launch_fwd_impl<T, TO, 128, 128, S::QT, S::BK, S::OCC, true>(p, stream)
+                      : launch_fwd_impl<T, TO, 128, 128, S::QT, S::BK, S::OCC, false>(p, stream);
     }
-    return launch_fwd_pp<T, TO, D, true>(p, stream);
+    return causal ? launch_fwd_pp<T, TO, D, true>(p, stream) : launch_fwd_pp<T, TO, D, false>(p, stream);
   } else {
     constexpr int QT = FwdShape<T, D>::QT, BK = FwdShape<T, D>::BK, OCC = FwdShape<T, D>::OCC;
     return causal ? launch_fwd_impl<T, TO, D, D, QT, BK, OCC, true>(p, stream)

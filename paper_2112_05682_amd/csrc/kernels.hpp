@@ -185,6 +185,22 @@ inline int fwd_causal64_bq(int64_t n_q, int64_t bh) {
                    bh * ((n_q + 511) / 512) >= MEA_T64_FWD_CAUSAL_MIN_WGS;
   return big ? 512 : 128;
 }
+// 16-bit d = d_v forward without the causal mask: the 4-wave kernel with
+// 128-query workgroups when the two-group kernel's one query tile (BQ_pp =
+// 512 queries at d = 64, 256 at d = 128) would be at least half padding,
+// else the two-group kernel.  Measured (bf16, two-group / 4-wave): d = 64,
+// 8x16 heads, 65536 keys: 0.907 / 0.497 ms at 65 queries, 1.009 / 0.797 at
+// 256, 1.036 / 1.118 at 300, 1.184 / 1.532 at 512; d = 128: 1.003 / 0.781 at
+// 65, 1.060 / 0.840 at 128, 1.041 / 1.361 at 160, 1.169 / 1.479 at 256.
+// Above that the two kernels measured within about 10 % either way, with
+// the two-group kernel ahead on the larger problems.
+inline bool fwd_pp_unmasked(int64_t n_q, int bq_pp) { return 2 * n_q > bq_pp; }
+// 16-bit d = d_v = 64 forward: queries per workgroup (512: the two-group
+// kernel; 128: the 4-wave kernel).
+inline int fwd64_bq(int64_t n_q, int64_t bh, bool causal) {
+  if (causal) return fwd_causal64_bq(n_q, bh);
+  return fwd_pp_unmasked(n_q, 512) ? 512 : 128;
+}
 // 16-bit d = 128: BQ = 256 selects the two-group kernel (8 waves of 32
 // queries); 128 the 4-wave kernel.  Problems with d_v != d always run the
 // 4-wave kernel with 128 queries per workgroup (kFwdBq4wave).
@@ -192,6 +208,12 @@ inline int fwd_causal64_bq(int64_t n_q, int64_t bh) {
 #define MEA_T128_FWD_BQ 256
 #endif
 constexpr int kFwdBq4wave128 = 128;
+// 16-bit d = d_v = 128 forward: 256 (the two-group kernel) or 128 (the 4-wave
+// kernel) queries per workgroup; causal problems always run the two-group
+// kernel.
+inline int fwd128_bq(int64_t n_q, bool causal) {
+  return causal || fwd_pp_unmasked(n_q, MEA_T128_FWD_BQ) ? MEA_T128_FWD_BQ : kFwdBq4wave128;
+}
 template <> struct FwdShape<__bf16, 128> { static constexpr int QT = 1, BK = 64, BQ = MEA_T128_FWD_BQ, OCC = 2; };
 template <> struct FwdShape<_Float16, 64> {
   static constexpr int BQ = MEA_T64_FWD_BQ, QT = BQ == 512 ? 2 : BQ / 128, BK = 64, OCC = MEA_T64_FWD_OCC;

@@ -69,10 +69,10 @@ static void check_fwd_plan(int64_t B, int64_t H, int64_t nq, int64_t nk, int64_t
                                           need ? WS : nullptr, need, nullptr);
   CHECK(st == MEA_OK && mea::g_fwd_calls == before + 1, "fwd call %d", (int)st);
   const mea::FwdParams& f = mea::g_last_fwd;
-  if (dtype != MEA_F32 && d == 64 && causal && nq > 64) {
-    // The causal 16-bit d = 64 plan tiles the queries as the kernel it picks.
-    const int64_t bq = mea::fwd_causal64_bq(nq, B * H);
-    CHECK(f.n_qtiles == (nq + bq - 1) / bq, "causal query tiles of %lld", (long long)bq);
+  if (dtype != MEA_F32 && nq > 64) {
+    // The 16-bit plan tiles the queries as the kernel it picks.
+    const int64_t bq = d == 64 ? mea::fwd64_bq(nq, B * H, causal) : mea::fwd128_bq(nq, causal);
+    CHECK(f.n_qtiles == (nq + bq - 1) / bq, "query tiles of %lld", (long long)bq);
   }
   // Keys the plan must cover: all of them, except that a decode-shaped causal
   // problem (16-bit, at most 64 queries) can see only its first n_q keys.
@@ -201,6 +201,12 @@ int main() {
     check_fwd_plan(2, 64, nq, nq, 64, MEA_BF16, 1);
   for (int64_t h : {(int64_t)4, (int64_t)6}) check_fwd_plan(1, h, 32768, 32768, 64, MEA_F16, 1);
   for (int64_t nq : {(int64_t)12288, (int64_t)12800}) check_fwd_plan(1, 16, nq, nq, 64, MEA_BF16, 1);
+  // Unmasked: the 4-wave kernel up to half of the two-group kernel's tile.
+  for (int64_t nq : {(int64_t)256, (int64_t)257}) check_fwd_plan(2, 3, nq, 1000, 64, MEA_BF16, 0);
+  for (int64_t nq : {(int64_t)128, (int64_t)129}) check_fwd_plan(2, 3, nq, 1000, 128, MEA_F16, 0);
+  CHECK(mea::fwd64_bq(256, 6, false) == 128 && mea::fwd64_bq(257, 6, false) == 512 &&
+            mea::fwd128_bq(128, false) == 128 && mea::fwd128_bq(129, false) == 256 && mea::fwd128_bq(100, true) == 256,
+        "unmasked kernel choice");
   CHECK(mea::fwd_causal64_bq(6144, 128) == 128 && mea::fwd_causal64_bq(6145, 128) == 512 &&
             mea::fwd_causal64_bq(32768, 4) == 128 && mea::fwd_causal64_bq(32768, 6) == 512 &&
             mea::fwd_causal64_bq(12288, 16) == 128 && mea::fwd_causal64_bq(12800, 16) == 512,

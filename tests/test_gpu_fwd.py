@@ -74,6 +74,20 @@ def test_forward_causal_d64_both_kernels(dtype, shape):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("shape", [(2, 3, 256, 1000, 64), (2, 3, 257, 1000, 64), (1, 2, 200, 70000, 64),
+                                   (2, 3, 128, 1000, 128), (2, 3, 129, 1000, 128), (1, 2, 100, 70000, 128)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_forward_unmasked_both_kernels(dtype, shape):
+    # Unmasked 16-bit problems run the 4-wave kernel when the two-group
+    # kernel's query tile (512 queries at d = 64, 256 at d = 128) would be at
+    # least half padding: both sides of both bounds, and long keys (key splits)
+    # through the 4-wave kernel.
+    B, H, nq, nk, d = shape
+    print("unmasked kernel choice case", shape, dtype, flush=True)
+    run_and_compare(B, H, nq, nk, d, dtype, False)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("shape", [(1, 2, 7, 100), (2, 1, 300, 257), (1, 1, 64, 3000)],
