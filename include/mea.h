@@ -186,7 +186,8 @@ mea_status mea_attention_bwd(const mea_problem* p, const void* q, const void* k,
  * workspace exceeds that size return MEA_ERR_SCRATCH before anything is
  * enqueued: B * H * ceil(n_q / 64) * 64 padded query rows must not exceed
  * 2^20 where the backward keeps 16 bytes per row (16-bit inputs and outputs
- * at d = d_v = 64, except causal problems of up to 2048 queries), or 2^21
+ * at d = d_v = 64, except causal problems of up to 2048 queries and
+ * unmasked ones of up to 512), or 2^21
  * otherwise (8 bytes per row).  The first call on a device
  * looks up that device's copy of the array; `stream` must belong to the
  * current device (0 = its null stream), else MEA_ERR_INVALID_ARG.

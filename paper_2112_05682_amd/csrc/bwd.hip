@@ -1944,7 +1944,7 @@ static hipError_t launch_bwd_kernels(BwdParams p, bool pp, hipStream_t stream) {
   using S = BwdShape<T, (D > DV ? D : DV)>;
   using Dk = DkdvTile<T, D, DV, S::QS>;
   void* args[] = {&p};
-  constexpr bool PP_CAN = bwd_two_group(sizeof(T) == 2, D, DV, __is_same(T, TO), false, 0);
+  constexpr bool PP_CAN = bwd_two_group_exists(sizeof(T) == 2, D, DV, __is_same(T, TO));
   hipError_t e = hipSuccess;
   if (p.dk) {
     bool launched = false;
@@ -1989,7 +1989,7 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
       // Float32 o and dO with 16-bit inputs: the preprocess also writes dO
       // rounded to T (the rounding the staging of these kernels applies), and
       // the kernels of 16-bit outputs run on that copy.
-      constexpr bool PP_CAN = bwd_two_group(true, D, DV, true, false, 0);
+      constexpr bool PP_CAN = bwd_two_group_exists(true, D, DV, true);
       const bool pp = PP_CAN && bwd_two_group(true, D, DV, true, CAUSAL, p.n_q);
       if (pp ? p.row_rec == nullptr : (p.s_init == nullptr || p.dp_init == nullptr)) return hipErrorInvalidValue;
       const void* pre = reinterpret_cast<const void*>(attn_bwd_pre_kernel<TO, DV, false, T>);
@@ -2006,7 +2006,7 @@ static hipError_t launch_bwd_impl(BwdParams p, hipStream_t stream) {
   }
   // The two-group kernels exist for 16-bit d = d_v = 64 with dO in the input
   // dtype; whether they run is the shared predicate's choice.
-  constexpr bool PP_CAN = bwd_two_group(sizeof(T) == 2, D, DV, __is_same(T, TO), false, 0);
+  constexpr bool PP_CAN = bwd_two_group_exists(sizeof(T) == 2, D, DV, __is_same(T, TO));
   const bool pp = PP_CAN && bwd_two_group(true, D, DV, true, CAUSAL, p.n_q);
   // The per-row values must be laid out as these kernels read them (records
   // or two arrays): a plan that disagrees is refused, not launched.

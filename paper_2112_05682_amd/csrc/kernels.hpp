@@ -126,12 +126,28 @@ constexpr int kBwdRowPad = 64;
 // queries run the 4-wave kernels: measured on causal bf16 d = 64 problems,
 // n = 1024-2048 (128-256 heads) took 5-13 % less time with them; at 3072 the
 // two kinds tie, and from 4096 queries on the two-group kernels take 3-12 %
-// less (6-7 % more before their plain tiles dropped the mask).
+// less (6-7 % more before their plain tiles dropped the mask).  Unmasked
+// problems of up to MEA_T64_BWD_SHORT queries run them too (the two-group dQ
+// kernel's 256-query tiles are mostly padding there): bf16 d = 64, two-group /
+// 4-wave, dK/dV + dQ: 2.796 / 2.293 ms at 8x16 heads, 65 queries, 65536
+// keys; 3.123 / 2.886 at 256; 4.543 / 4.563 at 512; 0.226 / 0.180 at 4x32
+// heads, 128 queries, 4096 keys; 0.343 / 0.324 at 512; 0.550 / 0.552 at
+// 1024; 0.292 / 0.303 at 4x16x2048^2.  The two kinds give bitwise the same
+// gradients.
 #ifndef MEA_T64_BWD_CAUSAL_SMALL
 #define MEA_T64_BWD_CAUSAL_SMALL 2048
 #endif
+#ifndef MEA_T64_BWD_SHORT
+#define MEA_T64_BWD_SHORT 512
+#endif
+// Whether the two-group backward kernels exist for these types and head
+// dimensions (whatever the problem's shape).
+constexpr bool bwd_two_group_exists(bool is16, int d, int dv, bool same_out_dtype) {
+  return is16 && d == 64 && dv == 64 && same_out_dtype;
+}
 constexpr bool bwd_two_group(bool is16, int d, int dv, bool same_out_dtype, bool causal, int64_t n_q) {
-  return is16 && d == 64 && dv == 64 && same_out_dtype && !(causal && n_q <= MEA_T64_BWD_CAUSAL_SMALL);
+  return bwd_two_group_exists(is16, d, dv, same_out_dtype) && !(causal && n_q <= MEA_T64_BWD_CAUSAL_SMALL) &&
+         !(!causal && n_q <= MEA_T64_BWD_SHORT);
 }
 // dtype: 0 float32, 1 fp16, 2 bf16; d and dv the head dimensions of q, k and
 // of v, o.

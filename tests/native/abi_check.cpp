@@ -211,7 +211,8 @@ int main() {
             mea::fwd_causal64_bq(32768, 4) == 128 && mea::fwd_causal64_bq(32768, 6) == 512 &&
             mea::fwd_causal64_bq(12288, 16) == 128 && mea::fwd_causal64_bq(12800, 16) == 512,
         "causal d = 64 kernel choice");
-  for (int64_t nq : {(int64_t)1, (int64_t)63, (int64_t)64, (int64_t)65, (int64_t)2048, (int64_t)2049, (int64_t)16384})
+  for (int64_t nq : {(int64_t)1, (int64_t)63, (int64_t)64, (int64_t)65, (int64_t)512, (int64_t)513, (int64_t)2048,
+                     (int64_t)2049, (int64_t)16384})
     for (int dt : {MEA_F32, MEA_BF16})
       for (int64_t d : {(int64_t)64, (int64_t)128}) {
         for (int causal = 0; causal < 2; ++causal) {

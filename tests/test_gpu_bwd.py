@@ -98,6 +98,17 @@ def test_backward_causal_d64_both_kernels(dtype, nq):
     run_and_compare(1, 1, nq, nq, 64, dtype, True)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("shape", [(2, 3, 512, 700), (2, 3, 513, 700), (1, 2, 100, 40000)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_backward_unmasked_d64_both_kernels(dtype, shape):
+    # Unmasked 16-bit d = 64 problems of up to 512 queries run the 4-wave
+    # backward, longer ones the two-group kernels: both sides of the switch,
+    # and few queries against many keys.
+    B, H, nq, nk = shape
+    run_and_compare(B, H, nq, nk, 64, dtype, False)
+
+
 def test_backward_fp32_self_attention_n256():
     w = WORKLOADS["selfattn_fp32_b1h1_n256_d64"]
     run_and_compare(w.batch, w.heads, w.n_q, w.n_k, w.d, w.dtype, w.causal)
