@@ -242,7 +242,9 @@ __global__ __launch_bounds__(256, OCC) void attn_fwd_kernel(FwdParams p) {
       const bool raise = mx_c > m_ref[t] + kRescaleSlack;
       if (__builtin_amdgcn_ballot_w64(raise)) {
         const float m_new = raise ? mx_c : m_ref[t];
-        const float alpha = fast_exp2(m_ref[t] - m_new);  // 0 on the first raise
+        // 0 on a first raise; 1 for a lane that does not raise (also one still
+        // at -inf, where the difference would be NaN).
+        const float alpha = raise ? fast_exp2(m_ref[t] - m_new) : 1.0f;
         l_run[t] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt)
