@@ -121,8 +121,10 @@ mea_status mea_attention_fwd_workspace_size(const mea_problem* p, size_t* bytes)
 /* Bytes of device workspace mea_attention_bwd needs for `p`: per padded row
  * (B*H*ceil(n_q/64)*64 rows) the values -lse/scale and -D_i with
  * D_i = sum_t dO_it O_it (Section 5.2's recompute needs only these and the
- * inputs), O(n) like the lse: 16 bytes per row for 16-bit inputs and outputs
- * at d = 64 (each value as three bf16 parts), else two float32 values.  For
+ * inputs), O(n) like the lse: 16 bytes per row (each value as three bf16
+ * parts) where the backward runs its two-group kernels -- 16-bit inputs and
+ * outputs at d = d_v = 64, except causal problems of up to 2048 queries and
+ * unmasked ones of up to 512 -- else two float32 values.  For
  * 16-bit inputs with float32 o and dO (out_f32) it also holds dO rounded to
  * the input dtype (B*H*n_q*d_v 16-bit values, O(n d) like dO itself), so that
  * the kernels of 16-bit outputs run; the rounding is the one those problems'
