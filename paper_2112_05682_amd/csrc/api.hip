@@ -153,7 +153,12 @@ FwdPlan plan_fwd(const mea_problem* p) {
   const int64_t k_tiles = (p->n_k + pl.bk - 1) / pl.bk;
   const int64_t base = bh * pl.n_qtiles;
   int64_t splits = 1;
-  const int64_t kTargetWorkgroups = 1024;  // 4 per CU
+  // Whole rounds of workgroups: 1024 (four per CU) for the kernels that fit
+  // one or two per CU, one round of MEA_T64_FWD_OCC per CU for the 16-bit
+  // d = 64 4-wave kernel (three: 768 workgroups measured 2-12 % faster than
+  // 1024 on 65-256 queries against 32768-262144 keys, and the same as 1536).
+  const bool four_wave64 = pl.bq == 128 && p->dtype != MEA_F32 && p->d == 64 && dv_of(p) == 64;
+  const int64_t kTargetWorkgroups = four_wave64 ? 256 * MEA_T64_FWD_OCC : 1024;
   const int64_t kMinTilesPerSplit = 16;
   if (base < 512 && k_tiles >= 2 * kMinTilesPerSplit) {
     splits = (kTargetWorkgroups + base - 1) / base;
